@@ -1,0 +1,387 @@
+"""Seeded synthetic inputs for the integer low-bit detector path.
+
+This module describes layer shapes and wiring and draws random codes and
+parameters from a seed. It performs none of the method's integer arithmetic
+(no convolution, rounding, requantisation or skip alignment): both the GPU
+path and the CPU oracle consume what it produces, each with its own code.
+
+Tensors are NHWC. Activation tensors hold b-bit unsigned codes (the integer
+part of the representation of Sec. 3.1.1, Eq. 1); a tensor with ``bits=32``
+holds raw int32 values (the output of a convolution whose normalisation is
+applied but which is not requantised, as the skip operand of Eq. 7 allows).
+
+Weights are handed over as their b-bit fields, the form a packed weight
+tensor stores, in one of two grids: two's complement (field ``w & (2^b - 1)``
+of a signed value w drawn uniformly from [-2^(b-1), 2^(b-1) - 1]), or the
+paper's odd grid of Eq. 3 (field eta_w uniform in [0, 2^b - 1], weight value
+2*eta_w - (2^b - 1)). The network workloads use the odd grid (zero mean, as
+trained weights are); the single-layer workloads state two's-complement ranges.
+
+Two parameter modes:
+
+* ``literal``: integer epilogue parameters drawn directly (bias, multiplier,
+  shift, skip numerator/exponent/side), as the single-layer workloads state.
+* ``calibrated``: per-channel affine normalisation parameters (gamma, beta)
+  are drawn; the running mean and variance are the exact statistics of each
+  layer's integer accumulator on the calibration images, so every layer's
+  output codes stay spread over [0, 2^b - 1] however deep the network is.
+  Each side computes those statistics with its own convolution and turns them
+  into integers with its own implementation of Eq. 5-8.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+
+# Clip range nu of every synthetic activation quantizer (Eq. 2): the step of a
+# b-bit code tensor is NU / (2^b - 1).
+NU = 3.0
+# BN epsilon used by every synthetic normalisation layer.
+BN_EPS = 1e-5
+
+
+def out_size(size: int, k: int, stride: int, pad: int) -> int:
+    return (size + 2 * pad - k) // stride + 1
+
+
+def qmax(bits: int) -> int:
+    return (1 << bits) - 1
+
+
+WENC_TWOS = 0       # two's-complement weight fields
+WENC_PAPER_ODD = 1  # Eq. 3 fields: value 2*eta_w - (2^b - 1)
+
+
+# --------------------------------------------------------------------------
+# network description
+# --------------------------------------------------------------------------
+@dataclass
+class TensorSpec:
+    name: str
+    n: int
+    h: int
+    w: int
+    c: int
+    bits: int  # 2/4/8: unsigned codes; 32: raw int32 values
+
+    @property
+    def shape(self) -> Tuple[int, int, int, int]:
+        return (self.n, self.h, self.w, self.c)
+
+
+@dataclass
+class ConvSpec:
+    """One set of conv weights applied to one or more (x, skip, y) segments.
+
+    Segments share the weights and each has its own epilogue table; the
+    detection heads use one segment per pyramid level (multi-level BN,
+    Sec. 3.2.2, Fig. 3).
+    """
+    name: str
+    cin: int
+    cout: int
+    k: int
+    stride: int
+    bits_w: int
+    segs: List[Tuple[str, Optional[str], str]]
+    skip_up2: bool = False
+    wenc: int = WENC_TWOS
+
+    @property
+    def pad(self) -> int:
+        return self.k // 2
+
+
+@dataclass
+class NetSpec:
+    tensors: Dict[str, TensorSpec] = field(default_factory=dict)
+    convs: List[ConvSpec] = field(default_factory=list)
+    inputs: List[str] = field(default_factory=list)
+    outputs: List[str] = field(default_factory=list)
+    wenc: int = WENC_TWOS  # weight grid of every conv added afterwards
+
+    def add_tensor(self, name, n, h, w, c, bits) -> TensorSpec:
+        assert name not in self.tensors, name
+        t = TensorSpec(name, n, h, w, c, bits)
+        self.tensors[name] = t
+        return t
+
+    def conv(self, name, x, y, cout, k, stride, bits_w, bits_out, skip=None,
+             skip_up2=False) -> ConvSpec:
+        """Single-segment conv; creates the output tensor."""
+        tx = self.tensors[x]
+        ho = out_size(tx.h, k, stride, k // 2)
+        wo = out_size(tx.w, k, stride, k // 2)
+        self.add_tensor(y, tx.n, ho, wo, cout, bits_out)
+        c = ConvSpec(name, tx.c, cout, k, stride, bits_w, [(x, skip, y)], skip_up2, self.wenc)
+        self.convs.append(c)
+        return c
+
+    def conv_levels(self, name, xs, ys, cout, k, bits_w, bits_out) -> ConvSpec:
+        """Stride-1 conv with shared weights over several levels."""
+        segs = []
+        for x, y in zip(xs, ys):
+            tx = self.tensors[x]
+            self.add_tensor(y, tx.n, tx.h, tx.w, cout, bits_out)
+            segs.append((x, None, y))
+        c = ConvSpec(name, self.tensors[xs[0]].c, cout, k, 1, bits_w, segs, False, self.wenc)
+        self.convs.append(c)
+        return c
+
+    def macs(self, conv: ConvSpec) -> int:
+        total = 0
+        for _, _, y in conv.segs:
+            t = self.tensors[y]
+            total += t.n * t.h * t.w * conv.cout * conv.k * conv.k * conv.cin
+        return total
+
+    def total_macs(self) -> int:
+        return sum(self.macs(c) for c in self.convs)
+
+
+# --------------------------------------------------------------------------
+# networks of the five workloads
+# --------------------------------------------------------------------------
+def single_conv_net(n, h, w, cin, cout, k, stride, bits_in, bits_w, bits_out,
+                    skip_bits=None, skip_up2=False) -> NetSpec:
+    net = NetSpec()
+    net.add_tensor("x", n, h, w, cin, bits_in)
+    net.inputs.append("x")
+    skip = None
+    if skip_bits is not None:
+        ho, wo = out_size(h, k, stride, k // 2), out_size(w, k, stride, k // 2)
+        hs, ws = ((ho + 1) // 2, (wo + 1) // 2) if skip_up2 else (ho, wo)
+        net.add_tensor("skip", n, hs, ws, cout, skip_bits)
+        net.inputs.append("skip")
+        skip = "skip"
+    net.conv("conv", "x", "y", cout, k, stride, bits_w, bits_out, skip, skip_up2)
+    net.outputs.append("y")
+    return net
+
+
+def basic_block_net(n, h, w, c, bits) -> NetSpec:
+    """ResNet-18 basic block: 3x3 conv, BN, ReLU; 3x3 conv, BN, + identity, ReLU."""
+    net = NetSpec()
+    net.add_tensor("x", n, h, w, c, bits)
+    net.inputs.append("x")
+    net.conv("conv1", "x", "h", c, 3, 1, bits, bits)
+    net.conv("conv2", "h", "y", c, 3, 1, bits, bits, skip="x")
+    net.outputs.append("y")
+    return net
+
+
+LEVELS = ("p3", "p4", "p5", "p6", "p7")
+NUM_ANCHORS = 9
+NUM_CLASSES = 80
+
+
+def pyramid_sizes(h: int, w: int) -> List[Tuple[int, int]]:
+    """Spatial sizes of P3..P7 for an h x w image (ResNet strides 8..128)."""
+    sizes = []
+    ch, cw = out_size(out_size(h, 7, 2, 3), 3, 2, 1), out_size(out_size(w, 7, 2, 3), 3, 2, 1)
+    for _ in range(3):  # C3, C4, C5 (3x3 stride-2 convs, pad 1)
+        ch, cw = out_size(ch, 3, 2, 1), out_size(cw, 3, 2, 1)
+        sizes.append((ch, cw))
+    for _ in range(2):  # P6, P7
+        ch, cw = out_size(ch, 3, 2, 1), out_size(cw, 3, 2, 1)
+        sizes.append((ch, cw))
+    return sizes
+
+
+def add_retina_heads(net: NetSpec, levels, bits, towers=("cls", "box")):
+    """RetinaNet heads shared over the pyramid levels, with a private epilogue
+    table per level (multi-level BN)."""
+    for tower in towers:
+        xs = list(levels)
+        for i in range(1, 5):
+            ys = [f"{tower}{i}.{lv}" for lv in levels]
+            net.conv_levels(f"{tower}.t{i}", xs, ys, 256, 3, bits, bits)
+            xs = ys
+        cout = NUM_ANCHORS * NUM_CLASSES if tower == "cls" else NUM_ANCHORS * 4
+        ys = [f"{tower}_out.{lv}" for lv in levels]
+        net.conv_levels(f"{tower}.pred", xs, ys, cout, 3, bits, 32)
+        net.outputs.extend(ys)
+
+
+def head_tower_net(n, h, w, bits, wenc=WENC_PAPER_ODD) -> NetSpec:
+    """Class tower of the RetinaNet head on the five pyramid levels of an
+    h x w image: four 3x3 256->256 convs and the 3x3 256->720 prediction."""
+    net = NetSpec(wenc=wenc)
+    for lv, (lh, lw) in zip(LEVELS, pyramid_sizes(h, w)):
+        net.add_tensor(lv, n, lh, lw, 256, bits)
+        net.inputs.append(lv)
+    add_retina_heads(net, LEVELS, bits, towers=("cls",))
+    return net
+
+
+def retinanet_r50_net(n, h, w, bits, heads=True, wenc=WENC_PAPER_ODD) -> NetSpec:
+    """ResNet-50 (bottleneck, stride on the 3x3) without the stem, FPN with
+    fused top-down adds, P6/P7, and optionally the RetinaNet heads."""
+    net = NetSpec(wenc=wenc)
+    h2 = out_size(out_size(h, 7, 2, 3), 3, 2, 1)
+    w2 = out_size(out_size(w, 7, 2, 3), 3, 2, 1)
+    net.add_tensor("c2in", n, h2, w2, 64, bits)
+    net.inputs.append("c2in")
+    x = "c2in"
+    cin = 64
+    stage_out = {}
+    for si, (width, blocks, stride) in enumerate(((64, 3, 1), (128, 4, 2), (256, 6, 2), (512, 3, 2))):
+        st = si + 2
+        for bi in range(blocks):
+            s = stride if bi == 0 else 1
+            p = f"res{st}.{bi}"
+            net.conv(f"{p}.conv1", x, f"{p}.a", width, 1, 1, bits, bits)
+            net.conv(f"{p}.conv2", f"{p}.a", f"{p}.b", width, 3, s, bits, bits)
+            if bi == 0:
+                net.conv(f"{p}.down", x, f"{p}.ds", 4 * width, 1, s, bits, 32)
+                skip = f"{p}.ds"
+            else:
+                skip = x
+            net.conv(f"{p}.conv3", f"{p}.b", f"{p}.out", 4 * width, 1, 1, bits, bits, skip=skip)
+            x = f"{p}.out"
+            cin = 4 * width
+        stage_out[st] = x
+    c3, c4, c5 = stage_out[3], stage_out[4], stage_out[5]
+    net.conv("fpn.lat5", c5, "p5in", 256, 1, 1, bits, bits)
+    net.conv("fpn.lat4", c4, "p4in", 256, 1, 1, bits, bits, skip="p5in", skip_up2=True)
+    net.conv("fpn.lat3", c3, "p3in", 256, 1, 1, bits, bits, skip="p4in", skip_up2=True)
+    net.conv("fpn.out3", "p3in", "p3", 256, 3, 1, bits, bits)
+    net.conv("fpn.out4", "p4in", "p4", 256, 3, 1, bits, bits)
+    net.conv("fpn.out5", "p5in", "p5", 256, 3, 1, bits, bits)
+    net.conv("fpn.p6", c5, "p6", 256, 3, 2, bits, bits)
+    net.conv("fpn.p7", "p6", "p7", 256, 3, 2, bits, bits)
+    if heads:
+        add_retina_heads(net, LEVELS, bits)
+    else:
+        net.outputs.extend(LEVELS)
+    return net
+
+
+# --------------------------------------------------------------------------
+# random draws
+# --------------------------------------------------------------------------
+def draw_codes(rng, shape, bits) -> np.ndarray:
+    return rng.integers(0, qmax(bits), size=shape, endpoint=True).astype(np.uint8)
+
+
+def draw_weights(rng, cout, k, cin, bits, wenc):
+    """(fields, values) of a [cout][k][k][cin] weight tensor."""
+    shape = (cout, k, k, cin)
+    if wenc == WENC_PAPER_ODD:
+        fields = rng.integers(0, qmax(bits), size=shape, endpoint=True)
+        values = 2 * fields - qmax(bits)
+    else:
+        lo, hi = -(1 << (bits - 1)), (1 << (bits - 1)) - 1
+        values = rng.integers(lo, hi, size=shape, endpoint=True)
+        fields = values & qmax(bits)
+    return fields.astype(np.uint8), values.astype(np.int32)
+
+
+def draw_literal_epilogue(rng, cout, with_skip):
+    """Integer epilogue parameters as the single-layer workloads state them:
+    bias U[-2^12, 2^12], multiplier U[2^30, 2^31), right shift U[8, 16];
+    skip numerator U[2^30, 2^31), exponent U[22, 30], side U{0, 1}."""
+    p = {
+        "bias": rng.integers(-(1 << 12), 1 << 12, size=cout, endpoint=True).astype(np.int32),
+        "mult": rng.integers(1 << 30, 1 << 31, size=cout).astype(np.int32),
+        "shift": rng.integers(8, 16, size=cout, endpoint=True).astype(np.int32),
+    }
+    if with_skip:
+        p["skip_c"] = rng.integers(1 << 30, 1 << 31, size=cout).astype(np.int32)
+        p["skip_d"] = rng.integers(22, 30, size=cout, endpoint=True).astype(np.int32)
+        p["skip_side"] = rng.integers(0, 1, size=cout, endpoint=True).astype(np.int32)
+    return p
+
+
+@dataclass
+class NetParams:
+    mode: str
+    inputs: Dict[str, np.ndarray]
+    alpha: Dict[str, float]            # step of each code tensor
+    weights: Dict[str, np.ndarray]     # b-bit fields [cout][k][k][cin]
+    alpha_w: Dict[str, float]
+    segs: Dict[str, List[dict]]        # per conv, per segment
+    bn_eps: float = BN_EPS
+    calib_images: Tuple[int, ...] = (0,)
+
+
+def make_params(net: NetSpec, seed: int, mode: str) -> NetParams:
+    """Draw every input and parameter of ``net`` from PCG64(seed).
+
+    Draw order: each input tensor (in ``net.inputs`` order), then per conv:
+    weights, then per segment the epilogue draws (literal: bias, multiplier,
+    shift, then skip numerator, exponent, side; calibrated: gamma U[0.5, 1.5],
+    beta U[0, 1]).
+
+    In calibrated mode the running mean and variance of each normalisation are
+    not drawn: they are the statistics of that layer's integer accumulator
+    over the images ``calib_images`` of the batch, which each side computes
+    with its own convolution.
+    """
+    rng = np.random.Generator(np.random.PCG64(seed))
+    inputs = {name: draw_codes(rng, net.tensors[name].shape, net.tensors[name].bits)
+              for name in net.inputs}
+    alpha = {name: NU / qmax(t.bits) for name, t in net.tensors.items() if t.bits != 32}
+    weights, alpha_w, segs = {}, {}, {}
+    for conv in net.convs:
+        weights[conv.name], _ = draw_weights(rng, conv.cout, conv.k, conv.cin, conv.bits_w,
+                                             conv.wenc)
+        alpha_w[conv.name] = 1.0 / qmax(conv.bits_w)
+        seg_params = []
+        for (x, skip, y) in conv.segs:
+            if mode == "literal":
+                seg_params.append(draw_literal_epilogue(rng, conv.cout, skip is not None))
+            else:
+                gamma = rng.uniform(0.5, 1.5, size=conv.cout)
+                beta = rng.uniform(0.0, 1.0, size=conv.cout)
+                seg_params.append({"gamma": gamma, "beta": beta})
+        segs[conv.name] = seg_params
+    return NetParams(mode, inputs, alpha, weights, alpha_w, segs)
+
+
+# --------------------------------------------------------------------------
+# the five workloads
+# --------------------------------------------------------------------------
+CONFIG_NAMES = (
+    "conv3x3_64x64_32x32_4bit",
+    "r18_basic_block_stage2_n2_100x168_2bit",
+    "retina_cls_tower_p3p7_800x1333_4bit",
+    "r50_fpn_n1_800x1333_2bit",
+    "retinanet_r50_fpn_n8_800x1333_4bit",
+)
+
+
+def config(idx: int):
+    """(NetSpec, NetParams) of workload ``idx`` with seed = idx."""
+    if idx == 0:
+        net = single_conv_net(1, 32, 32, 64, 64, 3, 1, 4, 4, 4)
+        return net, make_params(net, 0, "literal")
+    if idx == 1:
+        net = basic_block_net(2, 100, 168, 128, 2)
+        return net, make_params(net, 1, "literal")
+    if idx == 2:
+        net = head_tower_net(1, 800, 1333, 4)
+        return net, make_params(net, 2, "calibrated")
+    if idx == 3:
+        net = retinanet_r50_net(1, 800, 1333, 2, heads=False)
+        return net, make_params(net, 3, "calibrated")
+    if idx == 4:
+        net = retinanet_r50_net(8, 800, 1333, 4, heads=True)
+        return net, make_params(net, 4, "calibrated")
+    raise ValueError(idx)
+
+
+def scaled_config(idx: int, n: int, h: int, w: int, seed: Optional[int] = None):
+    """Workloads 2-4 at a reduced image size / batch (same wiring and recipe)."""
+    seed = idx if seed is None else seed
+    if idx == 2:
+        net = head_tower_net(n, h, w, 4)
+    elif idx == 3:
+        net = retinanet_r50_net(n, h, w, 2, heads=False)
+    elif idx == 4:
+        net = retinanet_r50_net(n, h, w, 4, heads=True)
+    else:
+        raise ValueError(idx)
+    return net, make_params(net, seed, "calibrated")

@@ -1,0 +1,67 @@
+"""Seeded workload generator and the oracle's whole-network evaluation (CPU)."""
+import numpy as np
+import pytest
+
+from oracle import network, ref
+from paper_2007_06919_amd import workloads as W
+
+
+def test_workload_sizes():
+    """Layer counts and MACs of the five workloads (N * Ho * Wo * Cout * k^2 * Cin)."""
+    want = [(1, 37_748_736), (2, 9_909_043_200), (25, 89_605_324_800),
+            (60, 102_943_883_264), (110, 1_976_089_280_512)]
+    nets = [W.single_conv_net(1, 32, 32, 64, 64, 3, 1, 4, 4, 4),
+            W.basic_block_net(2, 100, 168, 128, 2),
+            W.head_tower_net(1, 800, 1333, 4),
+            W.retinanet_r50_net(1, 800, 1333, 2, heads=False),
+            W.retinanet_r50_net(8, 800, 1333, 4, heads=True)]
+    for net, (segs, macs) in zip(nets, want):
+        assert sum(len(c.segs) for c in net.convs) == segs
+        assert net.total_macs() == macs
+    assert W.pyramid_sizes(800, 1333) == [(100, 167), (50, 84), (25, 42), (13, 21), (7, 11)]
+
+
+def test_seeded_draws_are_deterministic_and_in_range():
+    net1, p1 = W.config(0)
+    _, p2 = W.config(0)
+    assert np.array_equal(p1.inputs["x"], p2.inputs["x"])
+    assert np.array_equal(p1.weights["conv"], p2.weights["conv"])
+    s = p1.segs["conv"][0]
+    assert p1.inputs["x"].max() <= 15
+    assert -4096 <= s["bias"].min() and s["bias"].max() <= 4096
+    assert (1 << 30) <= s["mult"].min() and s["mult"].max() < (1 << 31)
+    assert 8 <= s["shift"].min() and s["shift"].max() <= 16
+    net, p = W.config(1)
+    s = p.segs["conv2"][0]
+    assert 22 <= s["skip_d"].min() and s["skip_d"].max() <= 30
+    assert set(np.unique(s["skip_side"])) <= {0, 1}
+    assert p.inputs["x"].max() <= 3
+
+
+def test_calibrated_network_keeps_codes_spread_and_bn_centered():
+    """Calibrated mode: BN statistics from the accumulator of the calibration
+    image make z_bar = (acc + bias) * alpha_z have mean ~beta and spread ~gamma
+    per channel (Eq. 5-6); codes stay spread through the whole network."""
+    net, p = W.scaled_config(4, 2, 128, 192)
+    vals, tables = network.run(net, p)
+    for conv in net.convs[:6]:
+        x, skip, y = conv.segs[0]
+        acc = ref.qconv(vals[x][:1], p.weights[conv.name], conv.bits_w, conv.stride, conv.pad,
+                        np.zeros(conv.cout), wenc=conv.wenc, out_int32=True)
+        s1, s2, cnt = ref.channel_sums(acc)
+        ac = p.alpha[x] * p.alpha_w[conv.name]
+        mean, var = ref.bn_stats_from_sums(s1, s2, cnt, ac)
+        bias, az = ref.fold_bn(p.segs[conv.name][0]["gamma"], p.segs[conv.name][0]["beta"],
+                               mean, var, p.bn_eps, ac)
+        assert np.array_equal(bias, tables[conv.name][0]["bias"])
+        z = (acc.reshape(-1, conv.cout) + bias) * az
+        g, b = p.segs[conv.name][0]["gamma"], p.segs[conv.name][0]["beta"]
+        assert np.all(np.abs(z.mean(0) - b) <= az)
+        assert np.allclose(z.std(0), g, rtol=0.05)
+    for name, t in net.tensors.items():
+        if t.bits == 32 or name in net.inputs:
+            continue
+        a = vals[name]
+        q = (1 << t.bits) - 1
+        interior = np.mean((a > 0) & (a < q))
+        assert interior > 0.2, (name, interior)
