@@ -1,0 +1,642 @@
+// C-ABI host code: argument validation, handle creation (weight decoding and
+// tiling, epilogue tables), kernel selection and launch, and the host-side
+// parameter derivation helpers. Declarations and contracts: include/aqd.h.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "aqd.h"
+#include "internal.h"
+
+using namespace aqd;
+
+namespace {
+
+thread_local std::string g_err;
+
+aqd_status_t fail(aqd_status_t st, const std::string &msg)
+{
+    g_err = msg;
+    return st;
+}
+
+#define REQUIRE(cond, msg)                            \
+    do {                                              \
+        if (!(cond))                                  \
+            return fail(AQD_ERR_INVALID, (msg));      \
+    } while (0)
+
+bool code_bits(int b) { return b == 2 || b == 4 || b == 8; }
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool overlap(const void *a, size_t na, const void *b, size_t nb)
+{
+    uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return na && nb && a0 < b0 + nb && b0 < a0 + na;
+}
+
+// Positions of the 64 channels of one K step after the kernel's widening of
+// packed codes (see qconv_mfma.hip): LDS byte p holds channel sigma(p).
+int widened_channel(int bits_in, int p)
+{
+    if (bits_in == 4)
+        return 8 * (p / 8) + 2 * (p % 4) + ((p / 4) % 2);
+    return 16 * (p / 16) + 4 * (p % 4) + ((p / 4) % 4);  // bits_in == 2
+}
+
+// Weight row of MFMA row rho (0..127) of a channel tile: lane group g of
+// accumulator tile i of wave slice wc ends up holding channel 16g + 4i + e.
+int tile_row_channel(int rho)
+{
+    int wc = rho / 64, rr = rho % 64;
+    int i = rr / 16, g = (rr % 16) / 4, e = rr % 4;
+    return wc * 64 + 16 * g + 4 * i + e;
+}
+
+int weight_value(int field, int bits, int wenc)
+{
+    if (wenc == AQD_WENC_PAPER_ODD)
+        return 2 * field - ((1 << bits) - 1);
+    return field >= (1 << (bits - 1)) ? field - (1 << bits) : field;
+}
+
+}  // namespace
+
+struct qconv_s {
+    qconv_desc_t d;
+    bool mfma;
+    int co_tiles, ksteps, cout_pad;
+    void *w_dev;
+    int32_t *epi_dev;  // [num_levels][6][cout_pad]
+};
+
+extern "C" {
+
+const char *aqd_last_error(void) { return g_err.c_str(); }
+
+static aqd_status_t validate_desc(const qconv_desc_t *d)
+{
+    REQUIRE(d->cin >= 1 && d->cout >= 1, "cin and cout must be >= 1");
+    REQUIRE(d->cin <= 65536 && d->cout <= 65536, "cin and cout must be <= 65536");
+    REQUIRE(d->kh >= 1 && d->kh <= 7 && d->kw >= 1 && d->kw <= 7, "kh and kw must be in 1..7");
+    REQUIRE(d->stride >= 1 && d->stride <= 4, "stride must be in 1..4");
+    REQUIRE(d->pad >= 0 && d->pad < d->kh && d->pad < d->kw, "pad must be in 0..k-1");
+    REQUIRE(code_bits(d->bits_in), "bits_in must be 2, 4 or 8");
+    REQUIRE(code_bits(d->bits_w), "bits_w must be 2, 4 or 8");
+    REQUIRE(d->wenc == AQD_WENC_TWOS || d->wenc == AQD_WENC_PAPER_ODD, "unknown weight grid");
+    REQUIRE(d->out_mode == AQD_OUT_CODES || d->out_mode == AQD_OUT_INT32, "unknown output mode");
+    REQUIRE((d->cin * d->bits_in) % 8 == 0, "cin * bits_in must be a multiple of 8");
+    REQUIRE((d->cin * d->bits_w) % 8 == 0, "cin * bits_w must be a multiple of 8");
+    if (d->out_mode == AQD_OUT_CODES) {
+        REQUIRE(code_bits(d->bits_out), "bits_out must be 2, 4 or 8");
+        REQUIRE((d->cout * d->bits_out) % 8 == 0, "cout * bits_out must be a multiple of 8");
+    }
+    REQUIRE(d->skip_bits == 0 || code_bits(d->skip_bits) || d->skip_bits == 32,
+            "skip_bits must be 0, 2, 4, 8 or 32");
+    if (d->skip_bits) {
+        REQUIRE(d->out_mode == AQD_OUT_CODES, "a skip add needs code output");
+        REQUIRE((d->cout * d->skip_bits) % 8 == 0, "cout * skip_bits must be a multiple of 8");
+    }
+    REQUIRE(d->skip_up2 == 0 || (d->skip_up2 == 1 && d->skip_bits), "skip_up2 needs a skip");
+    REQUIRE(d->num_levels >= 1 && d->num_levels <= 64, "num_levels must be in 1..64");
+    return AQD_OK;
+}
+
+aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
+                          const qconv_epilogue_t *levels, qconv_t *out)
+{
+    REQUIRE(desc && w_packed && levels && out, "null argument");
+    *out = nullptr;
+    aqd_status_t st = validate_desc(desc);
+    if (st != AQD_OK)
+        return st;
+    const qconv_desc_t d = *desc;
+    const bool codes = d.out_mode == AQD_OUT_CODES;
+    for (int l = 0; l < d.num_levels; ++l) {
+        const qconv_epilogue_t &e = levels[l];
+        REQUIRE(e.bias, "epilogue bias is null");
+        if (codes) {
+            REQUIRE(e.mult && e.shift, "epilogue mult/shift is null");
+            for (int c = 0; c < d.cout; ++c)
+                REQUIRE(e.shift[c] >= -31 && e.shift[c] <= 31, "shift outside [-31, 31]");
+        }
+        if (d.skip_bits) {
+            REQUIRE(e.skip_c && e.skip_d && e.skip_side, "skip parameters are null");
+            for (int c = 0; c < d.cout; ++c) {
+                REQUIRE(e.skip_c[c] >= 0, "skip_c must be >= 0");
+                REQUIRE(e.skip_d[c] >= 0 && e.skip_d[c] <= 31, "skip_d outside [0, 31]");
+                REQUIRE(e.skip_side[c] == 0 || e.skip_side[c] == 1, "skip_side must be 0 or 1");
+            }
+        }
+    }
+    // accumulator bound: K * max code * max |weight| < 2^31
+    const long long K = (long long)d.kh * d.kw * d.cin;
+    const long long wmax = d.wenc == AQD_WENC_PAPER_ODD ? (1 << d.bits_w) - 1 : (1 << (d.bits_w - 1));
+    if (K * ((1 << d.bits_in) - 1) * wmax >= (1LL << 31))
+        return fail(AQD_ERR_UNSUPPORTED, "accumulator could exceed int32 for this K and bitwidths");
+
+    // decode weight fields
+    const int wrow = d.cin * d.bits_w / 8;
+    const int taps = d.kh * d.kw;
+    std::vector<int16_t> wv((size_t)d.cout * taps * d.cin);
+    for (int co = 0; co < d.cout; ++co)
+        for (int t = 0; t < taps; ++t) {
+            const uint8_t *row = w_packed + ((size_t)co * taps + t) * wrow;
+            for (int ci = 0; ci < d.cin; ++ci) {
+                int bit = ci * d.bits_w;
+                int f = (row[bit >> 3] >> (bit & 7)) & ((1 << d.bits_w) - 1);
+                wv[((size_t)co * taps + t) * d.cin + ci] = (int16_t)weight_value(f, d.bits_w, d.wenc);
+            }
+        }
+
+    const bool w_fits_i8 = d.bits_w <= 4 || d.wenc == AQD_WENC_TWOS;
+    const bool mfma = (d.bits_in == 2 || d.bits_in == 4) && d.cin % KC == 0 && w_fits_i8 &&
+                      (codes ? d.cout % 16 == 0 : d.cout % 4 == 0);
+    qconv_s h{};
+    h.d = d;
+    h.mfma = mfma;
+    h.co_tiles = mfma ? (d.cout + BLK_CO - 1) / BLK_CO : 1;
+    h.cout_pad = mfma ? h.co_tiles * BLK_CO : d.cout;
+    h.ksteps = mfma ? taps * (d.cin / KC) : 0;
+
+    std::vector<uint8_t> wbuf;
+    if (mfma) {
+        // tiles [co_tile][k step][row rho][byte p]: channel tile_row_channel(rho) of the tile,
+        // input channel widened_channel(p) of the K step's 64-channel chunk
+        const int kpt = d.cin / KC;
+        wbuf.assign((size_t)h.co_tiles * h.ksteps * BLK_CO * KC, 0);
+        for (int ct = 0; ct < h.co_tiles; ++ct)
+            for (int ks = 0; ks < h.ksteps; ++ks) {
+                const int tap = ks / kpt, cc = ks % kpt;
+                for (int rho = 0; rho < BLK_CO; ++rho) {
+                    const int co = ct * BLK_CO + tile_row_channel(rho);
+                    if (co >= d.cout)
+                        continue;
+                    int8_t *dst = (int8_t *)wbuf.data() + (((size_t)ct * h.ksteps + ks) * BLK_CO + rho) * KC;
+                    const int16_t *src = wv.data() + ((size_t)co * taps + tap) * d.cin + cc * KC;
+                    for (int p = 0; p < KC; ++p)
+                        dst[p] = (int8_t)src[widened_channel(d.bits_in, p)];
+                }
+            }
+    } else {
+        wbuf.resize(wv.size() * sizeof(int16_t));
+        std::memcpy(wbuf.data(), wv.data(), wbuf.size());
+    }
+    std::vector<int32_t> epi((size_t)d.num_levels * 6 * h.cout_pad, 0);
+    for (int l = 0; l < d.num_levels; ++l) {
+        const qconv_epilogue_t &e = levels[l];
+        int32_t *t = epi.data() + (size_t)l * 6 * h.cout_pad;
+        for (int c = 0; c < d.cout; ++c) {
+            t[c] = e.bias[c];
+            if (codes) {
+                t[h.cout_pad + c] = e.mult[c];
+                t[2 * h.cout_pad + c] = e.shift[c];
+            }
+            if (d.skip_bits) {
+                t[3 * h.cout_pad + c] = e.skip_c[c];
+                t[4 * h.cout_pad + c] = e.skip_d[c];
+                t[5 * h.cout_pad + c] = e.skip_side[c];
+            }
+        }
+    }
+
+    const char *inject = std::getenv("AQD_FAULT_INJECT");
+    if (inject && std::strcmp(inject, "alloc") == 0)
+        return fail(AQD_ERR_NOMEM, "device allocation failed (injected)");
+
+    qconv_s *hp = new (std::nothrow) qconv_s(h);
+    if (!hp)
+        return fail(AQD_ERR_NOMEM, "host allocation failed");
+    if (hipMalloc(&hp->w_dev, wbuf.size()) != hipSuccess) {
+        delete hp;
+        return fail(AQD_ERR_NOMEM, "hipMalloc of the weights failed");
+    }
+    if (hipMalloc((void **)&hp->epi_dev, epi.size() * sizeof(int32_t)) != hipSuccess) {
+        (void)hipFree(hp->w_dev);
+        delete hp;
+        return fail(AQD_ERR_NOMEM, "hipMalloc of the epilogue tables failed");
+    }
+    if (hipMemcpy(hp->w_dev, wbuf.data(), wbuf.size(), hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(hp->epi_dev, epi.data(), epi.size() * sizeof(int32_t), hipMemcpyHostToDevice) !=
+            hipSuccess) {
+        (void)hipFree(hp->w_dev);
+        (void)hipFree(hp->epi_dev);
+        delete hp;
+        return fail(AQD_ERR_DEVICE, "copy of the weights to the device failed");
+    }
+    *out = hp;
+    return AQD_OK;
+}
+
+void qconv_destroy(qconv_t conv)
+{
+    if (!conv)
+        return;
+    (void)hipFree(conv->w_dev);
+    (void)hipFree(conv->epi_dev);
+    delete conv;
+}
+
+aqd_status_t qconv_out_shape(qconv_t conv, int h, int w, int *ho, int *wo)
+{
+    REQUIRE(conv && ho && wo, "null argument");
+    REQUIRE(h >= 1 && w >= 1, "h and w must be >= 1");
+    const qconv_desc_t &d = conv->d;
+    REQUIRE(h + 2 * d.pad >= d.kh && w + 2 * d.pad >= d.kw, "input smaller than the filter");
+    *ho = (h + 2 * d.pad - d.kh) / d.stride + 1;
+    *wo = (w + 2 * d.pad - d.kw) / d.stride + 1;
+    return AQD_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+struct SegCheck {
+    int ho, wo;
+    size_t xbytes, sbytes, ybytes;
+};
+
+aqd_status_t check_seg(const qconv_seg_t &s, SegCheck *out)
+{
+    REQUIRE(s.conv, "null handle");
+    const qconv_desc_t &d = s.conv->d;
+    REQUIRE(s.level >= 0 && s.level < d.num_levels, "level out of range");
+    REQUIRE(s.n >= 0, "n must be >= 0");
+    int ho = 0, wo = 0;
+    aqd_status_t st = qconv_out_shape(s.conv, s.h, s.w, &ho, &wo);
+    if (st != AQD_OK)
+        return st;
+    REQUIRE((long long)s.n * ho * wo < (1LL << 31) && (long long)s.n * s.h * s.w < (1LL << 31),
+            "too many pixels for one call");
+    out->ho = ho;
+    out->wo = wo;
+    out->xbytes = (size_t)s.n * s.h * s.w * d.cin * d.bits_in / 8;
+    out->ybytes = (size_t)s.n * ho * wo * d.cout * (d.out_mode == AQD_OUT_INT32 ? 32 : d.bits_out) / 8;
+    out->sbytes = 0;
+    if (s.n == 0)
+        return AQD_OK;
+    REQUIRE(s.x && s.y, "null tensor");
+    REQUIRE(aligned16(s.x) && aligned16(s.y), "tensors must be 16-byte aligned");
+    if (d.skip_bits) {
+        REQUIRE(s.skip, "the handle has a skip but skip is null");
+        REQUIRE(aligned16(s.skip), "skip must be 16-byte aligned");
+        if (d.skip_up2)
+            REQUIRE((ho - 1) / 2 < s.hs && (wo - 1) / 2 < s.ws && s.hs >= 1 && s.ws >= 1,
+                    "upsampled skip too small for the output");
+        else
+            REQUIRE(s.hs == ho && s.ws == wo, "skip size must equal the output size");
+        out->sbytes = (size_t)s.n * s.hs * s.ws * d.cout * d.skip_bits / 8;
+    } else {
+        REQUIRE(!s.skip, "skip given to a handle without a skip");
+    }
+    REQUIRE(!overlap(s.y, out->ybytes, s.x, out->xbytes), "output overlaps the input");
+    REQUIRE(!overlap(s.y, out->ybytes, s.skip, out->sbytes), "output overlaps the skip");
+    return AQD_OK;
+}
+
+bool same_config(const qconv_desc_t &a, const qconv_desc_t &b)
+{
+    return a.cin == b.cin && a.cout == b.cout && a.kh == b.kh && a.kw == b.kw &&
+           a.stride == b.stride && a.pad == b.pad && a.bits_in == b.bits_in &&
+           a.bits_w == b.bits_w && a.wenc == b.wenc && a.out_mode == b.out_mode &&
+           (a.out_mode == AQD_OUT_INT32 || a.bits_out == b.bits_out) &&
+           a.skip_bits == b.skip_bits && a.skip_up2 == b.skip_up2;
+}
+
+aqd_status_t launch_direct(const qconv_seg_t &s, const SegCheck &c, hipStream_t stream)
+{
+    const qconv_s &h = *s.conv;
+    DirectArgs a{};
+    a.x = (const uint8_t *)s.x;
+    a.skip = s.skip;
+    a.y = s.y;
+    a.wt = (const int16_t *)h.w_dev;
+    a.epi = h.epi_dev + (size_t)s.level * 6 * h.cout_pad;
+    a.n = s.n;
+    a.h = s.h;
+    a.w = s.w;
+    a.ho = c.ho;
+    a.wo = c.wo;
+    a.hs = s.hs;
+    a.ws = s.ws;
+    a.cin = h.d.cin;
+    a.cout = h.d.cout;
+    a.kh = h.d.kh;
+    a.kw = h.d.kw;
+    a.stride = h.d.stride;
+    a.pad = h.d.pad;
+    a.bits_in = h.d.bits_in;
+    a.out_bits = h.d.out_mode == AQD_OUT_INT32 ? 32 : h.d.bits_out;
+    a.skip_bits = h.d.skip_bits;
+    a.up2 = h.d.skip_up2;
+    if (launch_qconv_direct(a, stream) != hipSuccess)
+        return fail(AQD_ERR_DEVICE, "direct conv launch failed");
+    return AQD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t stream_)
+{
+    REQUIRE(segs && count >= 1 && count <= AQD_MAX_SEGS, "count must be in 1..AQD_MAX_SEGS");
+    hipStream_t stream = (hipStream_t)stream_;
+    SegCheck chk[AQD_MAX_SEGS];
+    for (int i = 0; i < count; ++i) {
+        aqd_status_t st = check_seg(segs[i], &chk[i]);
+        if (st != AQD_OK)
+            return st;
+        REQUIRE(same_config(segs[0].conv->d, segs[i].conv->d),
+                "grouped handles must share shapes, bitwidths and modes");
+    }
+    for (int i = 0; i < count; ++i)
+        for (int j = 0; j < count; ++j) {
+            if (i == j || segs[j].n == 0 || segs[i].n == 0)
+                continue;
+            REQUIRE(!overlap(segs[i].y, chk[i].ybytes, segs[j].y, chk[j].ybytes) &&
+                        !overlap(segs[i].y, chk[i].ybytes, segs[j].x, chk[j].xbytes) &&
+                        !overlap(segs[i].y, chk[i].ybytes, segs[j].skip, chk[j].sbytes),
+                    "a segment output overlaps another segment's tensors");
+        }
+    const qconv_s &h0 = *segs[0].conv;
+    if (!h0.mfma) {
+        for (int i = 0; i < count; ++i)
+            if (segs[i].n > 0) {
+                aqd_status_t st = launch_direct(segs[i], chk[i], stream);
+                if (st != AQD_OK)
+                    return st;
+            }
+        return AQD_OK;
+    }
+    MfmaArgs a{};
+    int tiles = 0;
+    for (int i = 0; i < count; ++i) {
+        const qconv_seg_t &s = segs[i];
+        if (s.n == 0)
+            continue;
+        MfmaSeg &m = a.seg[a.nseg++];
+        m.x = (const uint8_t *)s.x;
+        m.skip = s.skip;
+        m.y = s.y;
+        m.wt = (const int8_t *)s.conv->w_dev;
+        m.epi = s.conv->epi_dev + (size_t)s.level * 6 * s.conv->cout_pad;
+        m.P = (long long)s.n * chk[i].ho * chk[i].wo;
+        m.n = s.n;
+        m.h = s.h;
+        m.w = s.w;
+        m.ho = chk[i].ho;
+        m.wo = chk[i].wo;
+        m.hs = s.hs;
+        m.ws = s.ws;
+        m.tile_begin = tiles;
+        const long long px_tiles = (m.P + BLK_PX - 1) / BLK_PX;
+        REQUIRE(tiles + px_tiles * h0.co_tiles < (1LL << 30), "too many tiles for one launch");
+        tiles += (int)(px_tiles * h0.co_tiles);
+    }
+    if (a.nseg == 0)
+        return AQD_OK;
+    a.total_tiles = tiles;
+    a.tiles_per_xcd = (tiles + 7) / 8;
+    a.cin = h0.d.cin;
+    a.cout = h0.d.cout;
+    a.cout_pad = h0.cout_pad;
+    a.kh = h0.d.kh;
+    a.kw = h0.d.kw;
+    a.stride = h0.d.stride;
+    a.pad = h0.d.pad;
+    a.co_tiles = h0.co_tiles;
+    a.ksteps = h0.ksteps;
+    a.up2 = h0.d.skip_up2;
+    const int out_bits = h0.d.out_mode == AQD_OUT_INT32 ? 32 : h0.d.bits_out;
+    if (launch_qconv_mfma(h0.d.bits_in, out_bits, h0.d.skip_bits, a, stream) != hipSuccess)
+        return fail(AQD_ERR_DEVICE, "MFMA conv launch failed");
+    return AQD_OK;
+}
+
+aqd_status_t qconv_run(qconv_t conv, int level, int n, int h, int w, const void *x, const void *skip,
+                       int hs, int ws, void *y, aqd_stream_t stream)
+{
+    qconv_seg_t s{conv, level, n, h, w, x, skip, hs, ws, y};
+    return qconv_run_group(1, &s, stream);
+}
+
+aqd_status_t qadd_run(const qadd_desc_t *desc, const void *a, const void *b, void *y,
+                      const qadd_params_t *p, aqd_stream_t stream)
+{
+    REQUIRE(desc && p, "null argument");
+    const qadd_desc_t d = *desc;
+    REQUIRE(d.n >= 0 && d.h >= 1 && d.w >= 1 && d.c >= 1, "bad tensor shape");
+    REQUIRE(code_bits(d.bits_a) || d.bits_a == 32, "bits_a must be 2, 4, 8 or 32");
+    REQUIRE(code_bits(d.bits_b) || d.bits_b == 32, "bits_b must be 2, 4, 8 or 32");
+    REQUIRE(code_bits(d.bits_out), "bits_out must be 2, 4 or 8");
+    REQUIRE((d.c * d.bits_a) % 8 == 0 && (d.c * d.bits_b) % 8 == 0 && (d.c * d.bits_out) % 8 == 0,
+            "c * bits must be a multiple of 8");
+    if (d.up2)
+        REQUIRE(d.up2 == 1 && (d.h - 1) / 2 < d.hb && (d.w - 1) / 2 < d.wb && d.hb >= 1 && d.wb >= 1,
+                "upsampled operand too small");
+    else
+        REQUIRE(d.hb == d.h && d.wb == d.w, "operand sizes differ");
+    REQUIRE((long long)d.n * d.h * d.w < (1LL << 31), "too many pixels for one call");
+    if (d.n == 0)
+        return AQD_OK;
+    REQUIRE(a && b && y, "null tensor");
+    REQUIRE(aligned16(a) && aligned16(b) && aligned16(y), "tensors must be 16-byte aligned");
+    REQUIRE(p->skip_c && p->skip_d && p->skip_side && p->mult && p->shift, "null parameter array");
+    const size_t ab = (size_t)d.n * d.h * d.w * d.c * d.bits_a / 8;
+    const size_t bb = (size_t)d.n * d.hb * d.wb * d.c * d.bits_b / 8;
+    const size_t yb = (size_t)d.n * d.h * d.w * d.c * d.bits_out / 8;
+    REQUIRE(!overlap(y, yb, a, ab) && !overlap(y, yb, b, bb), "output overlaps an input");
+    QaddArgs q{};
+    q.a = a;
+    q.b = b;
+    q.y = (uint8_t *)y;
+    q.skip_c = p->skip_c;
+    q.skip_d = p->skip_d;
+    q.skip_side = p->skip_side;
+    q.mult = p->mult;
+    q.shift = p->shift;
+    q.n = d.n;
+    q.h = d.h;
+    q.w = d.w;
+    q.c = d.c;
+    q.hb = d.hb;
+    q.wb = d.wb;
+    q.bits_a = d.bits_a;
+    q.bits_b = d.bits_b;
+    q.bits_out = d.bits_out;
+    q.up2 = d.up2;
+    if (launch_qadd(q, (hipStream_t)stream) != hipSuccess)
+        return fail(AQD_ERR_DEVICE, "qadd launch failed");
+    return AQD_OK;
+}
+
+aqd_status_t aqd_channel_sums(const int32_t *v, int64_t rows, int c, int64_t *sums,
+                              aqd_stream_t stream)
+{
+    REQUIRE(rows >= 0 && c >= 1, "bad shape");
+    if (rows == 0)
+        return AQD_OK;
+    REQUIRE(v && sums, "null pointer");
+    if (launch_channel_sums(v, rows, c, (long long *)sums, (hipStream_t)stream) != hipSuccess)
+        return fail(AQD_ERR_DEVICE, "channel sums launch failed");
+    return AQD_OK;
+}
+
+// ------------------------------------------------------------------ host helpers
+aqd_status_t aqd_pack_codes(const uint8_t *codes, int64_t rows, int c, int bits, uint8_t *out)
+{
+    REQUIRE(codes && out && rows >= 0 && c >= 1 && code_bits(bits) && (c * bits) % 8 == 0,
+            "bad arguments");
+    const int rb = c * bits / 8;
+    const int mask = (1 << bits) - 1;
+    for (int64_t r = 0; r < rows; ++r) {
+        uint8_t *o = out + r * rb;
+        std::memset(o, 0, rb);
+        for (int ch = 0; ch < c; ++ch) {
+            const int v = codes[r * c + ch];
+            REQUIRE(v <= mask, "code out of range for the bitwidth");
+            const int bit = ch * bits;
+            o[bit >> 3] |= (uint8_t)(v << (bit & 7));
+        }
+    }
+    return AQD_OK;
+}
+
+aqd_status_t aqd_unpack_codes(const uint8_t *packed, int64_t rows, int c, int bits, uint8_t *out)
+{
+    REQUIRE(packed && out && rows >= 0 && c >= 1 && code_bits(bits) && (c * bits) % 8 == 0,
+            "bad arguments");
+    const int rb = c * bits / 8;
+    for (int64_t r = 0; r < rows; ++r)
+        for (int ch = 0; ch < c; ++ch) {
+            const int bit = ch * bits;
+            out[r * c + ch] = (packed[r * rb + (bit >> 3)] >> (bit & 7)) & ((1 << bits) - 1);
+        }
+    return AQD_OK;
+}
+
+aqd_status_t aqd_approx_ratio(double r, int32_t *c_out, int32_t *d_out)
+{
+    REQUIRE(c_out && d_out, "null argument");
+    REQUIRE(std::isfinite(r) && r >= 1.0 && r < 1073741824.0, "ratio must be in [1, 2^30)");
+    bool have = false;
+    double best_err = 0.0;
+    int32_t bc = 0, bd = 0;
+    for (int d = 1; d <= 31; ++d) {
+        const double x = std::ldexp(r, d);
+        if (x + 0.5 >= 2147483648.0)
+            break;
+        const double c = std::floor(x + 0.5);
+        const double err = std::fabs(r - std::ldexp(c, -d));
+        if (!have || err < best_err) {
+            have = true;
+            best_err = err;
+            bc = (int32_t)c;
+            bd = d;
+        }
+    }
+    *c_out = bc;
+    *d_out = bd;
+    return AQD_OK;
+}
+
+aqd_status_t aqd_normalize_multiplier(double r, int32_t *mult, int32_t *shift)
+{
+    REQUIRE(mult && shift, "null argument");
+    REQUIRE(std::isfinite(r) && r != 0.0, "scale must be finite and non-zero");
+    const double a = std::fabs(r);
+    int e = 0;
+    (void)std::frexp(a, &e);  // a = m * 2^e, m in [0.5, 1)
+    int d = 31 - e;           // a * 2^d in [2^30, 2^31)
+    double c = std::floor(std::ldexp(a, d) + 0.5);
+    if (c == 2147483648.0) {
+        c = 1073741824.0;
+        d -= 1;
+    }
+    const int sh = d - 31;
+    REQUIRE(sh >= -31 && sh <= 31, "scale out of range for the dyadic form");
+    *mult = r < 0 ? -(int32_t)c : (int32_t)c;
+    *shift = sh;
+    return AQD_OK;
+}
+
+aqd_status_t aqd_bn_stats_from_sums(int cout, const int64_t *s1, const int64_t *s2, int64_t count,
+                                    double alpha_conv, double *mean, double *var)
+{
+    REQUIRE(cout >= 1 && s1 && s2 && mean && var && count >= 1, "bad arguments");
+    for (int i = 0; i < cout; ++i) {
+        const double m = (double)s1[i] / (double)count;
+        const double va = (double)s2[i] / (double)count - m * m;
+        mean[i] = alpha_conv * m;
+        var[i] = (alpha_conv * alpha_conv) * va;
+    }
+    return AQD_OK;
+}
+
+aqd_status_t aqd_fold_bn(int cout, const double *gamma, const double *beta, const double *mean,
+                         const double *var, double eps, double alpha_conv, int32_t *bias,
+                         double *alpha_z)
+{
+    REQUIRE(cout >= 1 && gamma && beta && mean && var && bias && alpha_z, "bad arguments");
+    REQUIRE(std::isfinite(alpha_conv) && alpha_conv > 0.0, "alpha_conv must be positive");
+    for (int i = 0; i < cout; ++i) {
+        REQUIRE(gamma[i] != 0.0 && var[i] + eps > 0.0, "gamma must be non-zero and var + eps > 0");
+        const double sd = std::sqrt(var[i] + eps);
+        const double s = (beta[i] * sd / gamma[i] - mean[i]) / alpha_conv;
+        const double rb = std::floor(s + 0.5);
+        REQUIRE(rb > -2147483648.0 && rb < 2147483648.0, "folded bias outside int32");
+        bias[i] = (int32_t)rb;
+        alpha_z[i] = alpha_conv * gamma[i] / sd;
+    }
+    return AQD_OK;
+}
+
+aqd_status_t aqd_skip_params(int cout, const double *alpha_z, const double *alpha_k,
+                             int alpha_k_per_channel, int32_t *c, int32_t *d, int32_t *side,
+                             double *scale)
+{
+    REQUIRE(cout >= 1 && alpha_z && alpha_k && c && d && side && scale, "bad arguments");
+    for (int i = 0; i < cout; ++i) {
+        const double az = alpha_z[i];
+        const double ak = alpha_k_per_channel ? alpha_k[i] : alpha_k[0];
+        REQUIRE(az > 0.0 && ak > 0.0, "scales must be positive");
+        aqd_status_t st;
+        if (ak >= az) {
+            st = aqd_approx_ratio(ak / az, &c[i], &d[i]);
+            side[i] = 0;
+            scale[i] = az;
+        } else {
+            st = aqd_approx_ratio(az / ak, &c[i], &d[i]);
+            side[i] = 1;
+            scale[i] = ak;
+        }
+        if (st != AQD_OK)
+            return st;
+    }
+    return AQD_OK;
+}
+
+aqd_status_t aqd_requant_params(int cout, const double *scale, double alpha_out, int32_t *mult,
+                                int32_t *shift)
+{
+    REQUIRE(cout >= 1 && scale && mult && shift, "bad arguments");
+    REQUIRE(std::isfinite(alpha_out) && alpha_out > 0.0, "alpha_out must be positive");
+    for (int i = 0; i < cout; ++i) {
+        aqd_status_t st = aqd_normalize_multiplier(scale[i] / alpha_out, &mult[i], &shift[i]);
+        if (st != AQD_OK)
+            return st;
+    }
+    return AQD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,206 @@
+"""Stream-ordered whole-network runner on the C ABI.
+
+A network description (``workloads.NetSpec``) becomes a list of grouped
+``qconv_run_group`` launches on one HIP stream:
+
+* every tensor gets one device buffer (packed codes, or int32), so a forward
+  pass allocates nothing and can be captured in a HIP graph;
+* convolutions are ordered by dependency depth, and convolutions of the same
+  depth and configuration (same shapes, bitwidths and modes) share a launch:
+  the pyramid levels of a head layer (one epilogue table per level,
+  multi-level BN, Sec. 3.2.2) and the class and box towers at equal depth;
+* in calibrated mode the integer epilogue of every layer is derived here,
+  from the exact accumulator sums of the calibration images computed on the
+  GPU (int32 conv output + ``aqd_channel_sums``) and the library's host
+  helpers for Eq. 5-8; layers are calibrated in network order.
+
+PyTorch provides device memory and the stream; all arithmetic is in
+``libaqd.so``.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Tuple
+
+import numpy as np
+
+from . import aqd
+from .workloads import NetParams, NetSpec
+
+
+def _conv_key(net: NetSpec, conv) -> tuple:
+    x, skip, y = conv.segs[0]
+    ty = net.tensors[y]
+    return (conv.cin, conv.cout, conv.k, conv.stride, net.tensors[x].bits, conv.bits_w, conv.wenc,
+            ty.bits, net.tensors[skip].bits if skip else 0, conv.skip_up2)
+
+
+class Net:
+    def __init__(self, net: NetSpec, params: NetParams, device="cuda:0", stream=None):
+        import torch
+
+        self.torch = torch
+        self.net, self.params = net, params
+        self.device = torch.device(device)
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        self.bufs: Dict[str, "torch.Tensor"] = {}
+        for name, t in net.tensors.items():
+            if t.bits == 32:
+                self.bufs[name] = torch.empty(t.shape, dtype=torch.int32, device=self.device)
+            else:
+                self.bufs[name] = torch.empty((t.n, t.h, t.w, t.c * t.bits // 8), dtype=torch.uint8,
+                                              device=self.device)
+        for name in net.inputs:
+            t = net.tensors[name]
+            packed = aqd.pack_codes(params.inputs[name], t.bits)
+            self.bufs[name].copy_(torch.from_numpy(packed))
+        self.handles: Dict[str, int] = {}
+        self.tables: Dict[str, List[dict]] = {}
+        self._alpha_t: Dict[str, np.ndarray] = {}
+        self.schedule = self._make_schedule()
+        self._build()
+
+    # ---------------------------------------------------------------- setup
+    def _make_schedule(self) -> List[List[Tuple[object, int]]]:
+        producer = {}
+        for conv in self.net.convs:
+            for si, (_, _, y) in enumerate(conv.segs):
+                producer[y] = conv.name
+        depth = {}
+        for conv in self.net.convs:
+            d = 0
+            for x, skip, _ in conv.segs:
+                for src in (x, skip):
+                    if src is not None and src in producer:
+                        d = max(d, depth[producer[src]] + 1)
+            depth[conv.name] = d
+        groups: Dict[tuple, List[Tuple[object, int]]] = {}
+        order = []
+        for conv in self.net.convs:
+            key = (depth[conv.name], _conv_key(self.net, conv))
+            if key not in groups:
+                groups[key] = []
+                order.append(key)
+            groups[key].extend((conv, si) for si in range(len(conv.segs)))
+        sched = []
+        for key in sorted(order, key=lambda k: (k[0], order.index(k))):
+            segs = groups[key]
+            for i in range(0, len(segs), aqd.MAX_SEGS):
+                sched.append(segs[i:i + aqd.MAX_SEGS])
+        return sched
+
+    def _create(self, conv, levels, out_mode, bits_out, skip_bits, skip_up2):
+        x = conv.segs[0][0]
+        return aqd.qconv_create(conv.cin, conv.cout, conv.k, conv.stride, conv.pad,
+                                self.net.tensors[x].bits, conv.bits_w,
+                                self._packed_weights(conv), levels, wenc=conv.wenc,
+                                out_mode=out_mode, bits_out=bits_out, skip_bits=skip_bits,
+                                skip_up2=skip_up2)
+
+    def _packed_weights(self, conv):
+        return aqd.pack_codes(self.params.weights[conv.name], conv.bits_w)
+
+    def _seg_args(self, conv, si, level=None, images=None):
+        x, skip, y = conv.segs[si]
+        tx, ty = self.net.tensors[x], self.net.tensors[y]
+        xb, yb = self.bufs[x], self.bufs[y]
+        sb, hs, ws = None, 0, 0
+        if skip is not None:
+            ts = self.net.tensors[skip]
+            sb, hs, ws = self.bufs[skip], ts.h, ts.w
+        return (self.handles[conv.name], si if level is None else level, tx.n, tx.h, tx.w, xb, sb,
+                hs, ws, yb)
+
+    def _calibrate(self, conv, si, stats_handle) -> dict:
+        """Integer epilogue of one segment from the statistics of its
+        accumulator on the calibration images."""
+        torch = self.torch
+        p = self.params
+        x, skip, y = conv.segs[si]
+        tx, ty = self.net.tensors[x], self.net.tensors[y]
+        ho, wo = ty.h, ty.w
+        imgs = list(p.calib_images)
+        assert imgs == list(range(imgs[0], imgs[0] + len(imgs))), "calibration images must be contiguous"
+        img_bytes = self.bufs[x][0].numel() * self.bufs[x].element_size()
+        xptr = self.bufs[x].data_ptr() + imgs[0] * img_bytes
+        acc = torch.empty((len(imgs), ho, wo, conv.cout), dtype=torch.int32, device=self.device)
+        sums = torch.zeros(2 * conv.cout, dtype=torch.int64, device=self.device)
+        aqd.qconv_run(stats_handle, 0, len(imgs), tx.h, tx.w, xptr, None, 0, 0, acc,
+                      self.stream)
+        aqd.channel_sums(acc, len(imgs) * ho * wo, conv.cout, sums, self.stream)
+        self.stream.synchronize()
+        s = sums.cpu().numpy()
+        alpha_conv = p.alpha[x] * p.alpha_w[conv.name]
+        mean, var = aqd.bn_stats_from_sums(s[:conv.cout], s[conv.cout:], len(imgs) * ho * wo,
+                                           alpha_conv)
+        sp = p.segs[conv.name][si]
+        bias, alpha_z = aqd.fold_bn(sp["gamma"], sp["beta"], mean, var, p.bn_eps, alpha_conv)
+        t = {"bias": bias}
+        if ty.bits == 32:
+            self._alpha_t[y] = alpha_z
+            return t
+        scale = alpha_z
+        if skip is not None:
+            ak = self._alpha_t[skip] if self.net.tensors[skip].bits == 32 else p.alpha[skip]
+            c, d, side, scale = aqd.skip_params(alpha_z, ak)
+            t.update(skip_c=c, skip_d=d, skip_side=side)
+        t["mult"], t["shift"] = aqd.requant_params(scale, p.alpha[y])
+        return t
+
+    def _build(self):
+        """Derive every epilogue, create the handles, and run each layer once
+        (later layers calibrate on the outputs of earlier ones)."""
+        for conv in self.net.convs:
+            x, skip, y = conv.segs[0]
+            ty = self.net.tensors[y]
+            out_mode = aqd.OUT_INT32 if ty.bits == 32 else aqd.OUT_CODES
+            bits_out = 0 if ty.bits == 32 else ty.bits
+            skip_bits = self.net.tensors[skip].bits if skip else 0
+            if self.params.mode == "literal":
+                levels = [dict(s) for s in self.params.segs[conv.name]]
+            else:
+                zero = {"bias": np.zeros(conv.cout, np.int32)}
+                stats = self._create(conv, [zero], aqd.OUT_INT32, 0, 0, 0)
+                try:
+                    levels = [self._calibrate(conv, si, stats) for si in range(len(conv.segs))]
+                finally:
+                    aqd.qconv_destroy(stats)
+            self.tables[conv.name] = levels
+            self.handles[conv.name] = self._create(conv, levels, out_mode, bits_out, skip_bits,
+                                                   conv.skip_up2)
+            aqd.qconv_run_group([self._seg_args(conv, si) for si in range(len(conv.segs))],
+                                self.stream)
+        self.stream.synchronize()
+
+    # -------------------------------------------------------------- running
+    def forward(self, stream=None, launch_hook=None):
+        """Enqueue the whole network on the stream. launch_hook(group_index,
+        'before'|'after') is called around each grouped launch (for timing)."""
+        s = self.stream if stream is None else stream
+        for gi, group in enumerate(self.schedule):
+            if launch_hook:
+                launch_hook(gi, "before")
+            aqd.qconv_run_group([self._seg_args(conv, si) for conv, si in group], s)
+            if launch_hook:
+                launch_hook(gi, "after")
+
+    def group_macs(self, group) -> int:
+        tot = 0
+        for conv, si in group:
+            t = self.net.tensors[conv.segs[si][2]]
+            tot += t.n * t.h * t.w * conv.cout * conv.k * conv.k * conv.cin
+        return tot
+
+    def raw(self, name) -> np.ndarray:
+        """Host copy of a tensor's device bytes (packed codes or int32)."""
+        return self.bufs[name].cpu().numpy()
+
+    def close(self):
+        for h in self.handles.values():
+            aqd.qconv_destroy(h)
+        self.handles = {}
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

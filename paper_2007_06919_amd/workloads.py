@@ -385,3 +385,75 @@ def scaled_config(idx: int, n: int, h: int, w: int, seed: Optional[int] = None):
     else:
         raise ValueError(idx)
     return net, make_params(net, seed, "calibrated")
+
+
+# --------------------------------------------------------------------------
+# random single-conv cases (parity fuzzing)
+# --------------------------------------------------------------------------
+@dataclass
+class ConvCase:
+    n: int
+    h: int
+    w: int
+    cin: int
+    cout: int
+    k: int
+    stride: int
+    pad: int
+    bits_in: int
+    bits_w: int
+    wenc: int
+    bits_out: int        # 32: int32 output
+    skip_bits: int       # 0: none
+    skip_up2: bool
+    x: np.ndarray        # [n][h][w][cin] codes
+    w_fields: np.ndarray  # [cout][k][k][cin]
+    skip: Optional[np.ndarray]   # [n][hs][ws][cout] codes or int32 values
+    levels: List[dict]   # integer epilogue tables
+
+    @property
+    def out_hw(self):
+        return (out_size(self.h, self.k, self.stride, self.pad),
+                out_size(self.w, self.k, self.stride, self.pad))
+
+
+def random_conv_case(seed, n, h, w, cin, cout, k=3, stride=1, bits_in=4, bits_w=4,
+                     wenc=WENC_TWOS, bits_out=4, skip_bits=0, skip_up2=False, num_levels=1):
+    """Random codes and an integer epilogue whose scale keeps the output codes
+    spread over their range (multiplier U[2^30, 2^31), exponent chosen from
+    the accumulator's standard deviation under the drawn distributions)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    pad = k // 2
+    x = draw_codes(rng, (n, h, w, cin), bits_in)
+    w_fields, wv = draw_weights(rng, cout, k, cin, bits_w, wenc)
+    ho, wo = out_size(h, k, stride, pad), out_size(w, k, stride, pad)
+    qx = qmax(bits_in)
+    ex2 = (qx * (2 * qx + 1)) / 6.0                 # E[x^2], x uniform on 0..qx
+    ew2 = float(np.mean(wv.astype(np.float64) ** 2)) + 1e-9
+    acc_sd = np.sqrt(k * k * cin * ex2 * ew2)
+    # expected accumulator per channel (interior pixels): E[x] * sum of the channel's weights
+    acc_mean = (qx / 2.0) * wv.reshape(cout, -1).sum(axis=1).astype(np.float64)
+    skip = None
+    if skip_bits:
+        hs, ws = ((ho + 1) // 2, (wo + 1) // 2) if skip_up2 else (ho, wo)
+        if skip_bits == 32:
+            lim = int(4 * acc_sd) + 1
+            skip = rng.integers(-lim, lim, size=(n, hs, ws, cout)).astype(np.int32)
+        else:
+            skip = draw_codes(rng, (n, hs, ws, cout), skip_bits)
+    levels = []
+    for _ in range(num_levels):
+        noise = rng.integers(-int(acc_sd / 2), int(acc_sd / 2) + 1, size=cout)
+        lv = {"bias": (np.round(-acc_mean) + noise).astype(np.int32)}
+        if bits_out != 32:
+            target = qmax(bits_out) / (2.0 * acc_sd)   # scale mapping ~2 sd onto the code range
+            lv["mult"] = rng.integers(1 << 30, 1 << 31, size=cout).astype(np.int32)
+            base = int(np.floor(-np.log2(target)))     # M / 2^(31 + shift) ~ target
+            lv["shift"] = (base + rng.integers(-1, 2, size=cout)).clip(-31, 31).astype(np.int32)
+        if skip_bits:
+            lv["skip_c"] = rng.integers(1, 1 << 12, size=cout).astype(np.int32)
+            lv["skip_d"] = rng.integers(9, 14, size=cout).astype(np.int32)
+            lv["skip_side"] = rng.integers(0, 2, size=cout).astype(np.int32)
+        levels.append(lv)
+    return ConvCase(n, h, w, cin, cout, k, stride, pad, bits_in, bits_w, wenc, bits_out,
+                    skip_bits, skip_up2, x, w_fields, skip, levels)

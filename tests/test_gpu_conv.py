@@ -1,0 +1,178 @@
+"""GPU parity of single convolutions, grouped launches, the standalone add and
+the channel sums: the C ABI on the MI355X against the CPU oracle, bit for bit.
+
+Shapes span several 128 x 256 workgroup tiles with ragged pixel and channel
+tails, every bitwidth and output mode, both weight grids, skip operands of
+every width (with and without the nearest 2x upsample), strides 1 and 2, and
+both kernels (the MFMA kernel and the direct kernel for shapes it does not
+take).
+"""
+import numpy as np
+import pytest
+
+from gpu_helpers import assert_same, check_case, gpu_conv, oracle_conv
+from oracle import ref
+from paper_2007_06919_amd import aqd, workloads
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available()
+    return t
+
+
+MFMA_CASES = [
+    # (n, h, w, cin, cout, k, stride, bits_in, bits_w, wenc, bits_out, skip_bits, up2)
+    (1, 32, 32, 64, 64, 3, 1, 4, 4, 0, 4, 0, False),
+    (2, 17, 23, 128, 144, 3, 1, 4, 4, 0, 4, 0, False),      # ragged pixels and channels
+    (1, 19, 30, 64, 128, 3, 2, 2, 2, 0, 2, 0, False),       # stride 2, 2-bit
+    (2, 13, 11, 192, 256, 1, 1, 4, 4, 1, 4, 0, False),      # 1x1, odd grid
+    (1, 25, 21, 64, 256, 1, 2, 2, 2, 1, 2, 0, False),       # 1x1 stride 2
+    (1, 21, 19, 128, 96, 3, 1, 4, 8, 0, 8, 0, False),       # 8-bit weights and output codes
+    (2, 15, 17, 64, 64, 3, 1, 2, 4, 1, 4, 4, False),        # mixed widths, code skip
+    (1, 20, 22, 64, 128, 3, 1, 4, 4, 0, 2, 2, False),       # 2-bit skip, 2-bit out
+    (1, 16, 18, 128, 64, 1, 1, 4, 4, 0, 4, 4, True),        # FPN top-down: upsampled skip
+    (1, 17, 19, 64, 64, 1, 1, 2, 2, 0, 2, 2, True),         # odd output size, upsampled skip
+    (2, 9, 14, 64, 256, 1, 1, 4, 4, 1, 4, 32, False),       # int32 skip (normalised branch)
+    (1, 12, 12, 64, 64, 3, 1, 4, 4, 0, 8, 8, False),        # 8-bit skip
+    (1, 23, 29, 256, 720, 3, 1, 4, 4, 1, 32, 0, False),     # class prediction: int32 out
+    (2, 11, 13, 256, 36, 3, 1, 4, 4, 1, 32, 0, False),      # box prediction: 36 channels
+    (1, 7, 11, 64, 64, 3, 1, 4, 4, 0, 4, 0, False),         # one partial tile
+    (3, 1, 1, 64, 32, 3, 1, 4, 4, 0, 4, 0, False),          # 1x1 image, all taps but one padded
+]
+
+
+@pytest.mark.parametrize("case", MFMA_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_conv_mfma_parity(torch, case):
+    n, h, w, cin, cout, k, s, bi, bw, wenc, bo, sb, up2 = case
+    check_case(torch, seed=hash(case) % 1000, n=n, h=h, w=w, cin=cin, cout=cout, k=k, stride=s,
+               bits_in=bi, bits_w=bw, wenc=wenc, bits_out=bo, skip_bits=sb, skip_up2=up2)
+
+
+DIRECT_CASES = [
+    (1, 9, 10, 32, 16, 3, 1, 4, 4, 0, 4, 0, False),         # cin not a multiple of 64
+    (2, 8, 7, 16, 12, 3, 2, 8, 4, 0, 8, 0, False),          # 8-bit activations
+    (1, 6, 9, 24, 20, 1, 1, 2, 2, 1, 2, 2, False),          # 20 channels (not 16k)
+    (1, 7, 8, 64, 24, 3, 1, 4, 8, 1, 4, 4, True),           # 8-bit odd-grid weights
+    (1, 5, 6, 8, 10, 3, 1, 8, 8, 0, 32, 0, False),          # int32 out, 10 channels
+    (1, 11, 9, 40, 8, 5, 2, 4, 2, 0, 4, 32, False),         # 5x5, int32 skip
+]
+
+
+@pytest.mark.parametrize("case", DIRECT_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_conv_direct_parity(torch, case):
+    n, h, w, cin, cout, k, s, bi, bw, wenc, bo, sb, up2 = case
+    check_case(torch, seed=hash(case) % 1000 + 7, n=n, h=h, w=w, cin=cin, cout=cout, k=k,
+               stride=s, bits_in=bi, bits_w=bw, wenc=wenc, bits_out=bo, skip_bits=sb,
+               skip_up2=up2)
+
+
+def test_multi_level_tables(torch):
+    """One handle, three epilogue tables (multi-level BN): each level's output
+    uses its own table."""
+    check_case(torch, seed=5, n=1, h=20, w=26, cin=128, cout=128, k=3, bits_in=4, bits_w=4,
+               wenc=1, bits_out=4, num_levels=3)
+
+
+def test_grouped_launch_matches_separate_runs(torch):
+    """Two handles (class and box towers), five pyramid levels each, one launch."""
+    dev = torch.device("cuda:0")
+    sizes = [(20, 33), (10, 17), (5, 9), (3, 5), (2, 3)]
+    cases = [workloads.random_conv_case(seed=40 + t, n=2, h=20, w=33, cin=128, cout=128, k=3,
+                                        bits_in=4, bits_w=4, wenc=1, bits_out=4, num_levels=5)
+             for t in range(2)]
+    handles = [aqd.qconv_create(128, 128, 3, 1, 1, 4, 4, aqd.pack_codes(c.w_fields, 4), c.levels,
+                                wenc=1, bits_out=4) for c in cases]
+    rng = np.random.Generator(np.random.PCG64(9))
+    try:
+        segs, expect, outs = [], [], []
+        for t, c in enumerate(cases):
+            for lv, (h, w) in enumerate(sizes):
+                x = rng.integers(0, 16, size=(2, h, w, 128))
+                xd = torch.from_numpy(aqd.pack_codes(x, 4)).to(dev)
+                yd = torch.zeros((2, h, w, 64), dtype=torch.uint8, device=dev)
+                segs.append((handles[t], lv, 2, h, w, xd, None, 0, 0, yd))
+                outs.append(yd)
+                L = c.levels[lv]
+                want = ref.qconv(x, c.w_fields, 4, 1, 1, L["bias"], wenc=1, mult=L["mult"],
+                                 shift=L["shift"], bits_out=4)
+                expect.append(ref.pack_codes(want, 4))
+        aqd.qconv_run_group(segs)
+        torch.cuda.synchronize()
+        for i, (yd, want) in enumerate(zip(outs, expect)):
+            assert_same(yd.cpu().numpy(), want, f"segment {i}")
+    finally:
+        for h in handles:
+            aqd.qconv_destroy(h)
+
+
+def test_run_is_deterministic_and_leaves_guard_bytes(torch):
+    case = workloads.random_conv_case(seed=77, n=1, h=30, w=31, cin=64, cout=128, k=3,
+                                      bits_in=4, bits_w=4, bits_out=4)
+    a = gpu_conv(case, torch)[0]
+    b = gpu_conv(case, torch)[0]
+    assert np.array_equal(a, b)
+    dev = torch.device("cuda:0")
+    h = aqd.qconv_create(64, 128, 3, 1, 1, 4, 4, aqd.pack_codes(case.w_fields, 4), case.levels)
+    try:
+        x = torch.from_numpy(aqd.pack_codes(case.x, 4)).to(dev)
+        nbytes = 30 * 31 * 64
+        buf = torch.full((nbytes + 4096,), 0x5A, dtype=torch.uint8, device=dev)
+        y = buf[2048:2048 + nbytes]
+        aqd.qconv_run(h, 0, 1, 30, 31, x, None, 0, 0, y)
+        torch.cuda.synchronize()
+        host = buf.cpu().numpy()
+        assert np.all(host[:2048] == 0x5A) and np.all(host[2048 + nbytes:] == 0x5A)
+        assert np.array_equal(host[2048:2048 + nbytes].reshape(a.shape), a)
+    finally:
+        aqd.qconv_destroy(h)
+
+
+@pytest.mark.parametrize("bits_a,bits_b,bits_out,up2", [(4, 4, 4, True), (2, 2, 2, False),
+                                                        (32, 4, 4, False), (4, 32, 8, True),
+                                                        (8, 2, 4, True)])
+def test_qadd_parity(torch, bits_a, bits_b, bits_out, up2):
+    dev = torch.device("cuda:0")
+    rng = np.random.Generator(np.random.PCG64(bits_a * 100 + bits_b))
+    n, h, w, c = 2, 21, 34, 64
+    hb, wb = ((h + 1) // 2, (w + 1) // 2) if up2 else (h, w)
+
+    def draw(bits, shape):
+        if bits == 32:
+            return rng.integers(-5000, 5000, size=shape)
+        return rng.integers(0, 1 << bits, size=shape)
+
+    a, b = draw(bits_a, (n, h, w, c)), draw(bits_b, (n, hb, wb, c))
+    p = {"skip_c": rng.integers(1, 1 << 12, c), "skip_d": rng.integers(9, 14, c),
+         "skip_side": rng.integers(0, 2, c), "mult": rng.integers(1 << 30, 1 << 31, c),
+         "shift": rng.integers(-3, 6, c)}
+    want = ref.pack_codes(ref.qadd(a, b, up2, p["skip_c"], p["skip_d"], p["skip_side"], p["mult"],
+                                   p["shift"], bits_out), bits_out)
+
+    def dev_t(v, bits):
+        if bits == 32:
+            return torch.from_numpy(v.astype(np.int32)).to(dev)
+        return torch.from_numpy(aqd.pack_codes(v, bits)).to(dev)
+
+    pd = {k: torch.from_numpy(v.astype(np.int32)).to(dev) for k, v in p.items()}
+    y = torch.zeros((n, h, w, c * bits_out // 8), dtype=torch.uint8, device=dev)
+    aqd.qadd_run(n, h, w, c, bits_a, bits_b, bits_out, up2, hb, wb, dev_t(a, bits_a),
+                 dev_t(b, bits_b), y, pd)
+    torch.cuda.synchronize()
+    assert_same(y.cpu().numpy(), want, "qadd")
+
+
+def test_channel_sums(torch):
+    dev = torch.device("cuda:0")
+    rng = np.random.Generator(np.random.PCG64(3))
+    v = rng.integers(-40000, 40000, size=(3001, 300)).astype(np.int32)
+    sums = torch.zeros(600, dtype=torch.int64, device=dev)
+    aqd.channel_sums(torch.from_numpy(v).to(dev), 3001, 300, sums)
+    torch.cuda.synchronize()
+    s = sums.cpu().numpy()
+    s1, s2, cnt = ref.channel_sums(v)
+    assert cnt == 3001
+    assert s[:300].tolist() == s1 and s[300:].tolist() == s2

@@ -1,0 +1,62 @@
+"""GPU parity of whole networks: the runner (grouped launches, multi-level
+tables, fused skip adds, GPU-side calibration) against the oracle's own
+layer-by-layer evaluation, for every tensor of the network and for every
+derived integer epilogue table."""
+import numpy as np
+import pytest
+
+from gpu_helpers import assert_same
+from oracle import network, ref
+from paper_2007_06919_amd import runner, workloads
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available()
+    return t
+
+
+def compare_network(torch, net, params, images=None, check_tables=True):
+    gpu = runner.Net(net, params, device="cuda:0")
+    try:
+        gpu.forward()          # a second pass through the grouped schedule
+        torch.cuda.synchronize()
+        vals, tables = network.run(net, params, images=images)
+        sel = slice(None) if images is None else list(images)
+        if check_tables:
+            for conv in net.convs:
+                for si, (t_gpu, t_ref) in enumerate(zip(gpu.tables[conv.name], tables[conv.name])):
+                    for k, v in t_ref.items():
+                        assert np.array_equal(np.asarray(t_gpu[k], np.int64), np.asarray(v, np.int64)), \
+                            (conv.name, si, k)
+        for name, t in net.tensors.items():
+            if name not in vals:
+                continue
+            got = gpu.raw(name)[sel]
+            want = vals[name].astype(np.int32) if t.bits == 32 else ref.pack_codes(vals[name], t.bits)
+            assert_same(got, want, name)
+        return gpu, vals
+    finally:
+        gpu.close()
+
+
+def test_config0_full(torch):
+    net, params = workloads.config(0)
+    compare_network(torch, net, params)
+
+
+def test_config1_full(torch):
+    """ResNet-18 basic block, N=2, 100x168x128, 2-bit, literal epilogue with skip."""
+    net, params = workloads.config(1)
+    compare_network(torch, net, params)
+
+
+@pytest.mark.parametrize("cfg,n,h,w", [(2, 1, 320, 448), (3, 1, 256, 384), (4, 2, 192, 256)])
+def test_scaled_networks(torch, cfg, n, h, w):
+    """Workloads 2-4 at reduced image size: same wiring, calibration and
+    grouping; every layer's output and every epilogue table."""
+    net, params = workloads.scaled_config(cfg, n, h, w)
+    compare_network(torch, net, params)
