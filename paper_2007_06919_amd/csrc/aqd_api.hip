@@ -8,6 +8,7 @@
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -52,13 +53,47 @@ int widened_channel(int bits_in, int p)
     return 16 * (p / 16) + 4 * (p % 4) + ((p / 4) % 4);  // bits_in == 2
 }
 
-// Weight row of MFMA row rho (0..127) of a channel tile: lane group g of
-// accumulator tile i of wave slice wc ends up holding channel 16g + 4i + e.
-int tile_row_channel(int rho)
+// Channel (within a workgroup tile) of MFMA row rho: a wave slice has
+// 4 * cpl_rows = 16 * MI rows; lane group g of accumulator tile i of slice w
+// holds channel w * 16 * MI + cpl * g + 4i + e, where cpl = 4 * MI is the
+// number of consecutive channels a lane owns per pixel.
+int tile_row_channel(int rho, int cpl)
 {
-    int wc = rho / 64, rr = rho % 64;
+    const int slice = 4 * cpl;  // rows per wave slice
+    int w = rho / slice, rr = rho % slice;
     int i = rr / 16, g = (rr % 16) / 4, e = rr % 4;
-    return wc * 64 + 16 * g + 4 * i + e;
+    return w * slice + cpl * g + 4 * i + e;
+}
+
+int pick_tile(int cout, bool codes, int bits_in)
+{
+    if (bits_in == 4 && cout >= 256 && (!codes || cout % 32 == 0))
+        return TILE_256x128;
+    return cout > 64 ? TILE_128x256 : TILE_64x512;
+}
+
+// 256 zero bytes per device: the source of the kernel's copies for padding taps.
+std::mutex g_zero_mu;
+void *g_zero[64] = {};
+
+const uint8_t *device_zero_page()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return nullptr;
+    std::lock_guard<std::mutex> lock(g_zero_mu);
+    if (!g_zero[dev]) {
+        static const uint8_t zeros[256] = {};
+        void *p = nullptr;
+        if (hipMalloc(&p, sizeof zeros) != hipSuccess)
+            return nullptr;
+        if (hipMemcpy(p, zeros, sizeof zeros, hipMemcpyHostToDevice) != hipSuccess) {
+            (void)hipFree(p);
+            return nullptr;
+        }
+        g_zero[dev] = p;
+    }
+    return (const uint8_t *)g_zero[dev];
 }
 
 int weight_value(int field, int bits, int wenc)
@@ -73,9 +108,12 @@ int weight_value(int field, int bits, int wenc)
 struct qconv_s {
     qconv_desc_t d;
     bool mfma;
+    int tile_cfg, blk_co, blk_px;
     int co_tiles, ksteps, cout_pad;
     void *w_dev;
-    int32_t *epi_dev;  // [num_levels][6][cout_pad]
+    int32_t *epi_dev;  // [num_levels][EPI_FIELDS][cout_pad]
+    std::vector<int> fast;  // per level: every shift >= 2
+    const uint8_t *zero;    // the device's zero page
 };
 
 extern "C" {
@@ -157,15 +195,31 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
             }
         }
 
+    // MFMA kernel: 2/4-bit activations, weights that fit int8, 64-channel K
+    // steps, output and skip codes of the input's width; the direct kernel
+    // takes everything else
     const bool w_fits_i8 = d.bits_w <= 4 || d.wenc == AQD_WENC_TWOS;
     const bool mfma = (d.bits_in == 2 || d.bits_in == 4) && d.cin % KC == 0 && w_fits_i8 &&
-                      (codes ? d.cout % 16 == 0 : d.cout % 4 == 0);
+                      (codes ? (d.cout % 16 == 0 && d.bits_out == d.bits_in &&
+                                (d.skip_bits == 0 || d.skip_bits == d.bits_in || d.skip_bits == 32))
+                             : d.cout % 4 == 0);
     qconv_s h{};
     h.d = d;
     h.mfma = mfma;
+    int cpl = 0;
+    h.tile_cfg = pick_tile(d.cout, codes, d.bits_in);
+    mfma_tile_shape(h.tile_cfg, &h.blk_co, &h.blk_px, &cpl);
+    const int BLK_CO = h.blk_co;
     h.co_tiles = mfma ? (d.cout + BLK_CO - 1) / BLK_CO : 1;
     h.cout_pad = mfma ? h.co_tiles * BLK_CO : d.cout;
     h.ksteps = mfma ? taps * (d.cin / KC) : 0;
+    h.fast.assign(d.num_levels, 0);
+    for (int l = 0; l < d.num_levels && codes; ++l) {
+        int ok = 1;
+        for (int c = 0; c < d.cout; ++c)
+            ok &= levels[l].shift[c] >= 2;
+        h.fast[l] = ok;
+    }
 
     std::vector<uint8_t> wbuf;
     if (mfma) {
@@ -177,7 +231,7 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
             for (int ks = 0; ks < h.ksteps; ++ks) {
                 const int tap = ks / kpt, cc = ks % kpt;
                 for (int rho = 0; rho < BLK_CO; ++rho) {
-                    const int co = ct * BLK_CO + tile_row_channel(rho);
+                    const int co = ct * BLK_CO + tile_row_channel(rho, cpl);
                     if (co >= d.cout)
                         continue;
                     int8_t *dst = (int8_t *)wbuf.data() + (((size_t)ct * h.ksteps + ks) * BLK_CO + rho) * KC;
@@ -190,20 +244,23 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
         wbuf.resize(wv.size() * sizeof(int16_t));
         std::memcpy(wbuf.data(), wv.data(), wbuf.size());
     }
-    std::vector<int32_t> epi((size_t)d.num_levels * 6 * h.cout_pad, 0);
+    std::vector<int32_t> epi((size_t)d.num_levels * EPI_FIELDS * h.cout_pad, 0);
     for (int l = 0; l < d.num_levels; ++l) {
         const qconv_epilogue_t &e = levels[l];
-        int32_t *t = epi.data() + (size_t)l * 6 * h.cout_pad;
+        int32_t *t = epi.data() + (size_t)l * EPI_FIELDS * h.cout_pad;
         for (int c = 0; c < d.cout; ++c) {
-            t[c] = e.bias[c];
+            t[EPI_BIAS * h.cout_pad + c] = e.bias[c];
             if (codes) {
-                t[h.cout_pad + c] = e.mult[c];
-                t[2 * h.cout_pad + c] = e.shift[c];
+                const int sh = e.shift[c];
+                t[EPI_MULT * h.cout_pad + c] = e.mult[c];
+                t[EPI_SHIFT * h.cout_pad + c] = sh;
+                t[EPI_SHR * h.cout_pad + c] = sh - 1;
+                t[EPI_RND * h.cout_pad + c] = sh >= 2 ? (1 << (sh - 2)) : 0;
             }
             if (d.skip_bits) {
-                t[3 * h.cout_pad + c] = e.skip_c[c];
-                t[4 * h.cout_pad + c] = e.skip_d[c];
-                t[5 * h.cout_pad + c] = e.skip_side[c];
+                t[EPI_SKIP_C * h.cout_pad + c] = e.skip_c[c];
+                t[EPI_SKIP_D * h.cout_pad + c] = e.skip_d[c];
+                t[EPI_SKIP_SIDE * h.cout_pad + c] = e.skip_side[c];
             }
         }
     }
@@ -212,6 +269,9 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
     if (inject && std::strcmp(inject, "alloc") == 0)
         return fail(AQD_ERR_NOMEM, "device allocation failed (injected)");
 
+    h.zero = device_zero_page();
+    if (!h.zero)
+        return fail(AQD_ERR_NOMEM, "could not allocate the device zero page");
     qconv_s *hp = new (std::nothrow) qconv_s(h);
     if (!hp)
         return fail(AQD_ERR_NOMEM, "host allocation failed");
@@ -320,7 +380,7 @@ aqd_status_t launch_direct(const qconv_seg_t &s, const SegCheck &c, hipStream_t 
     a.skip = s.skip;
     a.y = s.y;
     a.wt = (const int16_t *)h.w_dev;
-    a.epi = h.epi_dev + (size_t)s.level * 6 * h.cout_pad;
+    a.epi = h.epi_dev + (size_t)s.level * EPI_FIELDS * h.cout_pad;
     a.n = s.n;
     a.h = s.h;
     a.w = s.w;
@@ -389,7 +449,7 @@ aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t st
         m.skip = s.skip;
         m.y = s.y;
         m.wt = (const int8_t *)s.conv->w_dev;
-        m.epi = s.conv->epi_dev + (size_t)s.level * 6 * s.conv->cout_pad;
+        m.epi = s.conv->epi_dev + (size_t)s.level * EPI_FIELDS * s.conv->cout_pad;
         m.P = (long long)s.n * chk[i].ho * chk[i].wo;
         m.n = s.n;
         m.h = s.h;
@@ -399,7 +459,8 @@ aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t st
         m.hs = s.hs;
         m.ws = s.ws;
         m.tile_begin = tiles;
-        const long long px_tiles = (m.P + BLK_PX - 1) / BLK_PX;
+        m.fast = s.conv->fast[s.level];
+        const long long px_tiles = (m.P + h0.blk_px - 1) / h0.blk_px;
         REQUIRE(tiles + px_tiles * h0.co_tiles < (1LL << 30), "too many tiles for one launch");
         tiles += (int)(px_tiles * h0.co_tiles);
     }
@@ -417,8 +478,11 @@ aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t st
     a.co_tiles = h0.co_tiles;
     a.ksteps = h0.ksteps;
     a.up2 = h0.d.skip_up2;
-    const int out_bits = h0.d.out_mode == AQD_OUT_INT32 ? 32 : h0.d.bits_out;
-    if (launch_qconv_mfma(h0.d.bits_in, out_bits, h0.d.skip_bits, a, stream) != hipSuccess)
+    a.tile_cfg = h0.tile_cfg;
+    a.bits_out = h0.d.out_mode == AQD_OUT_INT32 ? 32 : h0.d.bits_out;
+    a.skip_bits = h0.d.skip_bits;
+    a.zero = h0.zero;
+    if (launch_qconv_mfma(h0.d.bits_in, a, stream) != hipSuccess)
         return fail(AQD_ERR_DEVICE, "MFMA conv launch failed");
     return AQD_OK;
 }

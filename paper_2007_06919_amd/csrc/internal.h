@@ -9,21 +9,32 @@
 namespace aqd {
 
 // ---- implicit-GEMM MFMA kernel (qconv_mfma.hip) ----------------------------
-// Output tile of one workgroup: BLK_CO output channels x BLK_PX output pixels;
-// one K step is KC input channels of one filter tap.
-constexpr int BLK_CO = 128;
-constexpr int BLK_PX = 256;
+// One K step is KC input channels of one filter tap. Workgroup tile shapes
+// (output channels x output pixels), chosen per handle from cout:
+enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2 };
 constexpr int KC = 64;
+
+// tile shape of a configuration, and the channels one lane holds per pixel
+void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane);
+
+// Epilogue table of one level: EPI_FIELDS arrays of cout_pad int32.
+enum {
+    EPI_BIAS = 0, EPI_MULT = 1, EPI_SHIFT = 2,            // v = acc + bias; requant M / 2^(31+shift)
+    EPI_SKIP_C = 3, EPI_SKIP_D = 4, EPI_SKIP_SIDE = 5,    // Eq. 7-8 alignment
+    EPI_SHR = 6, EPI_RND = 7,                             // shift - 1 and 2^(shift-2) (shift >= 2)
+    EPI_FIELDS = 8
+};
 
 struct MfmaSeg {
     const uint8_t *x;    // [n][h][w][cin] codes
     const void *skip;    // [n][hs][ws][cout] or null
     void *y;             // [n][ho][wo][cout]
-    const int8_t *wt;    // weight tiles [co_tiles][ksteps][BLK_CO][KC]
-    const int32_t *epi;  // epilogue table [6][cout_pad] of this segment's level
+    const int8_t *wt;    // weight tiles [co_tiles][ksteps][blk_co][KC]
+    const int32_t *epi;  // epilogue table [EPI_FIELDS][cout_pad] of this segment's level
     long long P;         // n * ho * wo
     int n, h, w, ho, wo, hs, ws;
     int tile_begin;      // first workgroup tile of this segment
+    int fast;            // every shift of the level >= 2: 32-bit requantisation
 };
 
 struct MfmaArgs {
@@ -31,15 +42,18 @@ struct MfmaArgs {
     int nseg;
     int total_tiles;
     int tiles_per_xcd;   // grid = 8 * tiles_per_xcd workgroups
+    int tile_cfg;
     int cin, cout, cout_pad;
     int kh, kw, stride, pad;
     int co_tiles, ksteps;
+    int bits_out;        // 2, 4, 8 or 32 (int32 output)
+    int skip_bits;       // 0, 2, 4, 8 or 32
     int up2;
+    const uint8_t *zero; // >= 16 zero bytes in device memory (source of padding taps)
 };
 
-// bits_in in {2, 4}; out_bits in {2, 4, 8} or 32 (int32 output); skip_bits in {0, 2, 4, 8, 32}
-hipError_t launch_qconv_mfma(int bits_in, int out_bits, int skip_bits, const MfmaArgs &a,
-                             hipStream_t stream);
+// bits_in in {2, 4}
+hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream);
 
 // ---- direct kernel (qconv_direct.hip): any shape the ABI allows -------------
 struct DirectArgs {

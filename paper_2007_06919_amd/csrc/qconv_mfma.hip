@@ -3,35 +3,45 @@
 //
 // GEMM view of a convolution (Sec. 3.2.1, Eq. 4): rows = output channels
 // (weights, operand A), columns = output pixels n*ho*wo (operand B, gathered
-// from the NHWC input per filter tap), K = taps x input channels.
+// from the NHWC input per filter tap), K = taps x input channels; one K step
+// is 64 input channels of one tap.
 //
-// Workgroup: 256 threads = 4 waves in a 2 x 2 arrangement; tile 128 channels
-// x 256 pixels; each wave owns 64 channels x 128 pixels = 4 x 8 MFMA tiles of
-// 16 x 16 (128 int32 accumulators per lane). One K step = 64 input channels
-// of one tap, double-buffered in LDS.
+// Workgroup: 256 threads = 4 waves in a WC x WP grid. A wave owns MI x NJ
+// accumulator tiles of 16 x 16 (128 int32 accumulators per lane), i.e.
+// 16*MI channels x 16*NJ pixels; the workgroup tile is WC*16*MI x WP*16*NJ.
+// Two workgroups share a CU.
 //
-// Operand staging:
-//  * activations: each thread loads one pixel's 64 packed b-bit codes
-//    (32 B at 4 bit, 16 B at 2 bit) with 16-byte loads, widens them to int8
-//    with mask/shift word operations and writes one 64-byte LDS row. The
-//    widening leaves the codes in a fixed permutation sigma of the 64
-//    channels; the weights were stored in the same permutation at create,
-//    so every MFMA dot product is unchanged.
-//  * weights: int8 tiles prepared at create ([co_tile][k step][128][64]);
-//    each thread copies 32 B into LDS.
-//  LDS rows are 80 B apart (64 B + 16 B pad), which spreads the 16-byte
-//  reads of 16 consecutive rows over distinct banks.
+// Operand path: every K step is copied from global memory straight into LDS
+// (global_load_lds_dwordx4, no VGPR staging) into a ring of NSTAGE stages,
+// NSTAGE-1 steps ahead of the MFMAs:
+//  * weights: int8, decoded and tiled at create ([co_tile][k step][rows][64]),
+//    64-byte rows whose 16-byte columns are XOR-swizzled;
+//  * activations: the packed b-bit codes as stored in HBM (32 B per pixel and
+//    K step at 4 bit, 16 B at 2 bit), 4-bit rows with swizzled 16-byte halves;
+//    padding taps copy zeros from a zero page.
+// Each wave reads its fragments for step k+1 from LDS into a second register
+// set while the MFMAs of step k run, and widens the packed codes to int8 with
+// mask/shift word operations. The widening leaves a fixed permutation of the
+// 16 channels of a fragment; the weights were stored at create in the same
+// permutation, so every dot product is unchanged.
 //
-// Epilogue: the weight rows of each 64-channel wave slice were permuted at
-// create so that lane group g (lanes 16g..16g+15) of a 16 x 16 accumulator
-// tile i holds channels 16g + 4i + e (e = 0..3): each lane ends with 16
-// consecutive channels of one pixel per column tile and packs their b-bit
-// codes into one 4/8/16-byte store without cross-lane traffic.
+// Epilogue: weight rows were permuted at create so that lane group g (lanes
+// 16g..16g+15) of accumulator tile i holds channels 4*MI*g + 4i + e
+// (e = 0..3): each lane owns 4*MI consecutive channels of one pixel per
+// column tile and packs their codes into one store without cross-lane
+// traffic. Output codes and skip codes have the input's bitwidth. The
+// requantisation uses 32-bit operations when every shift is >= 2: with
+// d = 31 + shift, floor((u*M + 2^(d-1)) / 2^d) = (mulhi(u, M) + 2^(d-33)) >>
+// (d-32) exactly (u*M = hi*2^32 + lo with 0 <= lo < 2^32 cannot carry into
+// the quotient); other levels take the 64-bit path.
 //
 // Workgroup order: consecutive workgroup ids are dispatched round-robin over
 // the 8 XCDs; ids are remapped so that each XCD receives a contiguous range
 // of tiles (neighbouring pixel tiles of all channel tiles), which keeps the
 // gathered input rows and the weights in that XCD's L2.
+
+#include <type_traits>
+#include <utility>
 
 #include "epilogue.h"
 #include "internal.h"
@@ -39,26 +49,137 @@
 namespace aqd {
 namespace {
 
+// f(integral_constant<int, 0>) ... f(integral_constant<int, N-1>): compile-time
+// indices, so register arrays indexed by them stay in registers.
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, I...>)
+{
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f)
+{
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 constexpr int NT = 256;
-constexpr int LDS_ROW = 80;
-constexpr int A_STAGE = BLK_CO * LDS_ROW;            // 10 KiB
-constexpr int B_STAGE = BLK_PX * LDS_ROW;            // 20 KiB
-constexpr int PRM_OFF = 2 * (A_STAGE + B_STAGE);     // parameter table after both stages
-constexpr int LDS_BYTES = PRM_OFF + 6 * BLK_CO * 4;  // 64512 B
 
-template <int BI, int BO, int SK>
+// round(a * c / 2^d), ties up, d in [0, 31], result assumed to fit in int32
+__device__ __forceinline__ int rsm32(int a, int c, int d)
+{
+    const unsigned lo = (unsigned)a * (unsigned)c;
+    const int hi = __mulhi(a, c);
+    const unsigned r = d > 0 ? (1u << (d - 1)) : 0u;
+    const unsigned lo2 = lo + r;
+    const unsigned hi2 = (unsigned)hi + (lo2 < lo ? 1u : 0u);
+    return (int)__builtin_amdgcn_alignbit(hi2, lo2, (unsigned)d);
+}
+
+
+template <int BI, int MI, int NJ, int WC>
+struct Cfg {
+    static constexpr int WP = 4 / WC;
+    static constexpr int TM = 16 * MI;            // channels per wave
+    static constexpr int TN = 16 * NJ;            // pixels per wave
+    static constexpr int BCO = WC * TM;           // channels per workgroup
+    static constexpr int BPX = WP * TN;           // pixels per workgroup
+    static constexpr int PB = KC * BI / 8;        // packed bytes per pixel and K step (32 / 16)
+    static constexpr int A_STAGE = BCO * KC;      // int8 weight rows of 64 B
+    static constexpr int B_STAGE = BPX * PB;      // packed code rows of PB bytes
+    static constexpr int STAGE = A_STAGE + B_STAGE;
+    static constexpr int NSTAGE = STAGE <= 16384 ? 4 : 3;  // ring depth: two workgroups per CU
+    static constexpr int A_PER = A_STAGE / 1024 / 4;       // 1 KiB copies per wave and K step
+    static constexpr int B_PER = B_STAGE / 1024 / 4;
+    static constexpr int NOPS = A_PER + B_PER;             // copy instructions per lane and K step
+    static constexpr int BPC = 1024 / PB;                  // pixels per 1 KiB chunk (32 / 64)
+    static constexpr int LPP = 64 / BPC;                   // lanes per pixel row (2 / 1)
+    static constexpr int CPL = 4 * MI;                     // channels per lane and pixel (epilogue)
+    static constexpr int OW = CPL * BI / 32;               // packed output dwords per lane and pixel
+    static_assert(A_STAGE % 4096 == 0 && B_STAGE % 4096 == 0, "a stage splits into 4 waves x 1 KiB");
+    static_assert(2 * (NSTAGE * STAGE + 8 * BCO * 4) <= 163840, "two workgroups per CU");
+};
+
+// XOR swizzle of the 16-byte columns of weight row r (64-byte rows): the
+// 16-byte reads of 16 consecutive rows at one logical column hit distinct
+// banks whether 8 or 16 lanes are served per cycle.
+__device__ __forceinline__ int swz_a(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
+// XOR swizzle of the 16-byte halves of a 32-byte packed 4-bit code row.
+__device__ __forceinline__ int swz_b4(int p) { return (p >> 3) & 1; }
+
+// 16 bytes per lane from global memory straight into LDS at l + 16 * lane
+// (l wave-uniform, in M0). Issued as inline assembly so that the compiler does
+// not track it: every wait for these copies is an explicit wait_vmcnt (the
+// counter retires in issue order, so the compiler's own waits for later loads
+// stay correct, only stricter).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void *g, uint8_t *l)
+{
+    const uint32_t la = __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)l);
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 ::"s"(la), "v"(g) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt()
+{
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <int W>
+__device__ __forceinline__ void load_words(const uint8_t *p, uint32_t *w)
+{
+    if constexpr (W == 1) {
+        w[0] = *(const uint32_t *)p;
+    } else if constexpr (W == 2) {
+        const uint2 t = *(const uint2 *)p;
+        w[0] = t.x;
+        w[1] = t.y;
+    } else {
+#pragma unroll
+        for (int u = 0; u < W; u += 4) {
+            const uint4 t = *(const uint4 *)(p + 4 * u);
+            w[u] = t.x;
+            w[u + 1] = t.y;
+            w[u + 2] = t.z;
+            w[u + 3] = t.w;
+        }
+    }
+}
+
+template <int W>
+__device__ __forceinline__ void store_words(uint8_t *p, const uint32_t *w)
+{
+    if constexpr (W == 1) {
+        *(uint32_t *)p = w[0];
+    } else if constexpr (W == 2) {
+        *(uint2 *)p = make_uint2(w[0], w[1]);
+    } else {
+#pragma unroll
+        for (int u = 0; u < W; u += 4)
+            *(uint4 *)(p + 4 * u) = make_uint4(w[u], w[u + 1], w[u + 2], w[u + 3]);
+    }
+}
+
+// OUTK: 0 = codes of width BI, 1 = int32.
+// SKK: 0 = none, 1 = codes of width BI, 2 = int32.
+// FAST: every segment's shifts are >= 2 (32-bit requantisation).
+template <int BI, int MI, int NJ, int WC, int OUTK, int SKK, int FAST>
 __global__ void __launch_bounds__(NT, 2) qconv_mfma_kernel(MfmaArgs A)
 {
-    __shared__ __attribute__((aligned(16))) uint8_t lds[LDS_BYTES];
+    using C = Cfg<BI, MI, NJ, WC>;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_stages[C::NSTAGE * C::STAGE];
+    __shared__ __attribute__((aligned(16))) int32_t prm[EPI_FIELDS * C::BCO];
 
     const int bid = blockIdx.x;
     const int logical = (bid & 7) * A.tiles_per_xcd + (bid >> 3);
     if (logical >= A.total_tiles)
         return;
 
-    // segment of this tile (uniform over the workgroup)
     int s = 0;
 #pragma unroll
     for (int i = 1; i < AQD_MAX_SEGS; ++i)
@@ -72,286 +193,332 @@ __global__ void __launch_bounds__(NT, 2) qconv_mfma_kernel(MfmaArgs A)
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wc = wave >> 1;  // channel half of the tile
-    const int wp = wave & 1;   // pixel half of the tile
+    const int wc = wave / C::WP;
+    const int wp = wave % C::WP;
 
-    constexpr int CHUNK = KC * BI / 8;  // packed bytes of one K step per pixel
     const int row_bytes = A.cin * BI / 8;
-    const int kpt = A.cin / KC;         // K steps per tap
+    const int kpt = A.cin / KC;
     const int KS = A.ksteps;
-
-    // pixel gathered by this thread
-    const long long p = (long long)px_tile * BLK_PX + tid;
-    const bool pvalid = p < S.P;
     const int hw = S.ho * S.wo;
-    const int pn = pvalid ? (int)(p / hw) : 0;
-    const int prem = pvalid ? (int)(p - (long long)pn * hw) : 0;
-    const int poh = prem / S.wo;
-    const int pow_ = prem - poh * S.wo;
-    const int ih0 = poh * A.stride - A.pad;
-    const int iw0 = pow_ * A.stride - A.pad;
-    const uint8_t *xn = S.x + (long long)pn * S.h * S.w * row_bytes;
 
-    const int8_t *wtile = S.wt + (long long)co_tile * KS * (BLK_CO * KC);
-
-    // epilogue parameters of this channel tile -> LDS
-    {
-        int32_t *prm = (int32_t *)(lds + PRM_OFF);
-        constexpr int NP = (BO == 32) ? 1 : (SK ? 6 : 3);
-        for (int i = tid; i < NP * BLK_CO; i += NT) {
-            int which = i / BLK_CO, c = i - which * BLK_CO;
-            prm[which * BLK_CO + c] = S.epi[which * A.cout_pad + co_tile * BLK_CO + c];
-        }
+    // epilogue table of this channel tile -> LDS
+    for (int i = tid; i < EPI_FIELDS * C::BCO; i += NT) {
+        const int which = i / C::BCO, c = i - which * C::BCO;
+        prm[which * C::BCO + c] = S.epi[which * A.cout_pad + co_tile * C::BCO + c];
     }
 
-    uint4 breg[CHUNK / 16];
-    uint4 areg[2];
+    // Copies: chunk q of a stage (1 KiB) belongs to wave q % 4; which source
+    // bytes a lane fetches implements the LDS swizzle.
+    //  weights: chunk q = rows 16q .. 16q+15; lane L -> row 16q + L/4, LDS
+    //           column L%4 holding logical column (L%4) ^ swz_a(row)
+    //  codes:   chunk q = pixels BPC*q ..; lane L -> pixel BPC*q + L/LPP, LDS
+    //           16-byte part L%LPP holding logical part (L%LPP) ^ swz_b4(pixel)
+    int a_src[C::A_PER];
+#pragma unroll
+    for (int t = 0; t < C::A_PER; ++t) {
+        const int row = 16 * (4 * t + wave) + (lane >> 2);
+        a_src[t] = row * KC + 16 * ((lane & 3) ^ swz_a(row));
+    }
+    int ih0[C::B_PER], iw0[C::B_PER];
+    const uint8_t *xb[C::B_PER];
+    bool pv[C::B_PER];
+#pragma unroll
+    for (int t = 0; t < C::B_PER; ++t) {
+        const int ploc = C::BPC * (4 * t + wave) + lane / C::LPP;
+        const int part = lane % C::LPP;
+        const long long p = (long long)px_tile * C::BPX + ploc;
+        pv[t] = p < S.P;
+        const int pn = pv[t] ? (int)(p / hw) : 0;
+        const int prem = pv[t] ? (int)(p - (long long)pn * hw) : 0;
+        const int oh = prem / S.wo, ow = prem - oh * S.wo;
+        ih0[t] = oh * A.stride - A.pad;
+        iw0[t] = ow * A.stride - A.pad;
+        xb[t] = S.x + (long long)pn * S.h * S.w * row_bytes + 16 * (BI == 4 ? (part ^ swz_b4(ploc)) : part);
+    }
 
-    auto load_b = [&](int ks) {
-        int tap = ks / kpt;
-        int cc = ks - tap * kpt;
-        int r = tap / A.kw;
-        int q = tap - r * A.kw;
-        int ih = ih0 + r, iw = iw0 + q;
-        bool ok = pvalid && (unsigned)ih < (unsigned)S.h && (unsigned)iw < (unsigned)S.w;
-        if (ok) {
-            const uint4 *src = (const uint4 *)(xn + ((long long)ih * S.w + iw) * row_bytes + cc * CHUNK);
+    // Copy state: steps are issued in order, so the per-pixel source of the
+    // current tap is computed once per tap (bsrc; null for padding taps).
+    const int8_t *a_next = S.wt + (long long)co_tile * KS * C::A_STAGE;
+    int tap_next = 0, cc_next = 0, ks_next = 0;
+    const uint8_t *bsrc[C::B_PER];
+    auto issue = [&]() {
+        if (cc_next == 0) {
+            const int r = tap_next / A.kw;
+            const int q = tap_next - r * A.kw;
 #pragma unroll
-            for (int u = 0; u < CHUNK / 16; ++u)
-                breg[u] = src[u];
-        } else {
-#pragma unroll
-            for (int u = 0; u < CHUNK / 16; ++u)
-                breg[u] = make_uint4(0, 0, 0, 0);
-        }
-    };
-    auto store_b = [&](int stage) {
-        uint8_t *dst = lds + 2 * A_STAGE + stage * B_STAGE + tid * LDS_ROW;
-        uint32_t in[CHUNK / 4];
-#pragma unroll
-        for (int u = 0; u < CHUNK / 16; ++u) {
-            in[4 * u + 0] = breg[u].x;
-            in[4 * u + 1] = breg[u].y;
-            in[4 * u + 2] = breg[u].z;
-            in[4 * u + 3] = breg[u].w;
-        }
-        uint32_t o[16];
-        if constexpr (BI == 4) {
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                o[2 * i] = in[i] & 0x0F0F0F0Fu;
-                o[2 * i + 1] = (in[i] >> 4) & 0x0F0F0F0Fu;
+            for (int t = 0; t < C::B_PER; ++t) {
+                const int ih = ih0[t] + r, iw = iw0[t] + q;
+                const bool ok = pv[t] && (unsigned)ih < (unsigned)S.h && (unsigned)iw < (unsigned)S.w;
+                bsrc[t] = ok ? xb[t] + ((long long)ih * S.w + iw) * row_bytes : nullptr;
             }
-        } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    o[4 * i + j] = (in[i] >> (2 * j)) & 0x03030303u;
         }
+        uint8_t *st = lds_stages + (ks_next % C::NSTAGE) * C::STAGE;
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-            *(uint4 *)(dst + 16 * u) = make_uint4(o[4 * u], o[4 * u + 1], o[4 * u + 2], o[4 * u + 3]);
+        for (int t = 0; t < C::A_PER; ++t)
+            dma16(a_next + a_src[t], st + (4 * t + wave) * 1024);
+#pragma unroll
+        for (int t = 0; t < C::B_PER; ++t)
+            dma16(bsrc[t] ? bsrc[t] + cc_next * C::PB : A.zero, st + C::A_STAGE + (4 * t + wave) * 1024);
+        a_next += C::A_STAGE;
+        ++ks_next;
+        if (++cc_next == kpt) {
+            cc_next = 0;
+            ++tap_next;
+        }
     };
-    auto load_a = [&](int ks) {
-        const uint4 *src = (const uint4 *)(wtile + (long long)ks * (BLK_CO * KC)) + tid * 2;
-        areg[0] = src[0];
-        areg[1] = src[1];
-    };
-    auto store_a = [&](int stage) {
-        uint8_t *dst = lds + stage * A_STAGE + (tid >> 1) * LDS_ROW + (tid & 1) * 32;
-        *(uint4 *)dst = areg[0];
-        *(uint4 *)(dst + 16) = areg[1];
+    // wait until at most `steps` K steps of copies are outstanding
+    auto wait_steps = [&](int steps) {
+        switch (steps) {
+        case 0: wait_vmcnt<0>(); break;
+        case 1: wait_vmcnt<C::NOPS>(); break;
+        default: wait_vmcnt<2 * C::NOPS>(); break;
+        }
     };
 
-    v4i acc[4][8];
+    v4i acc[MI][NJ];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+        for (int j = 0; j < NJ; ++j)
             acc[i][j] = v4i{0, 0, 0, 0};
 
-    load_a(0);
-    load_b(0);
-    store_a(0);
-    store_b(0);
+    // fragment addresses inside a stage (swizzled as written above)
+    const int a_off = (wc * C::TM + (lane & 15)) * KC + 16 * ((lane >> 4) ^ swz_a(lane & 15));
+    int b_off;
+    if constexpr (BI == 4)
+        b_off = C::A_STAGE + (wp * C::TN + (lane & 15)) * C::PB + 8 * ((lane >> 4) ^ (swz_b4(lane & 15) << 1));
+    else
+        b_off = C::A_STAGE + (wp * C::TN + (lane & 15)) * C::PB + 4 * (lane >> 4);
+
+    using BW = typename std::conditional<BI == 4, uint2, uint32_t>::type;
+    v4i fa[2][MI];
+    BW fb[2][NJ];
+    auto read_a = [&](int stage, v4i *dst, int i) {
+        dst[i] = *(const v4i *)(lds_stages + stage * C::STAGE + a_off + i * 16 * KC);
+    };
+    auto read_b = [&](int stage, BW *dst, int j) {
+        dst[j] = *(const BW *)(lds_stages + stage * C::STAGE + b_off + j * 16 * C::PB);
+    };
+    auto widen = [&](const BW w) -> v4i {
+        if constexpr (BI == 4)
+            return v4i{(int)(w.x & 0x0F0F0F0Fu), (int)((w.x >> 4) & 0x0F0F0F0Fu),
+                       (int)(w.y & 0x0F0F0F0Fu), (int)((w.y >> 4) & 0x0F0F0F0Fu)};
+        else
+            return v4i{(int)(w & 0x03030303u), (int)((w >> 2) & 0x03030303u),
+                       (int)((w >> 4) & 0x03030303u), (int)((w >> 6) & 0x03030303u)};
+    };
+
+    // prologue: copies for steps 0 .. NSTAGE-2, fragments of step 0
+    const int pre = KS < C::NSTAGE - 1 ? KS : C::NSTAGE - 1;
+    for (int k = 0; k < pre; ++k)
+        issue();
+    wait_steps(pre - 1);
     __syncthreads();
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+        read_b(0, fb[0], j);
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+        read_a(0, fa[0], i);
 
-    const int a_off = (wc * 64 + (lane & 15)) * LDS_ROW + (lane >> 4) * 16;
-    const int b_off = 2 * A_STAGE + (wp * 128 + (lane & 15)) * LDS_ROW + (lane >> 4) * 16;
-
-    for (int ks = 0; ks < KS; ++ks) {
-        const int cur = ks & 1;
-        const bool more = ks + 1 < KS;
-        if (more) {
-            load_a(ks + 1);
-            load_b(ks + 1);
-        }
-        const uint8_t *ab = lds + cur * A_STAGE + a_off;
-        const uint8_t *bb = lds + cur * B_STAGE + b_off;
-        v4i af[4], bf[8];
+    // step ks: MFMAs on register set ks & 1 while the fragments of step ks + 1
+    // are read into the other set; copies run NSTAGE - 1 steps ahead.
+    for (int k0 = 0; k0 < KS; k0 += 2) {
+        static_for<2>([&](auto pc) {
+            constexpr int P = decltype(pc)::value;
+            const int ks = k0 + P;
+            if (ks >= KS)
+                return;
+            const bool next = ks + 1 < KS;
+            if (next) {
+                // step ks + 1 landed: copies up to step min(ks + NSTAGE - 2, KS - 1) were issued
+                const int last = ks + C::NSTAGE - 2 < KS - 1 ? ks + C::NSTAGE - 2 : KS - 1;
+                wait_steps(last - (ks + 1));
+                // stage ks + 1 visible to every wave; every wave is past step ks - 1, whose
+                // reads (of stage ks) ended the use of the stage the next copy refills
+                asm volatile("s_barrier" ::: "memory");
+                if (ks + C::NSTAGE - 1 < KS)
+                    issue();
+            }
+            const int nst = (ks + 1) % C::NSTAGE;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            af[i] = *(const v4i *)(ab + i * 16 * LDS_ROW);
+            for (int j = 0; j < NJ; ++j) {
+                const v4i bj = widen(fb[P][j]);
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-            bf[j] = *(const v4i *)(bb + j * 16 * LDS_ROW);
+                for (int i = 0; i < MI; ++i)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[P][i], bj, acc[i][j], 0, 0, 0);
+                if (next) {
+                    read_b(nst, fb[P ^ 1], j);
+                    if (j < MI)
+                        read_a(nst, fa[P ^ 1], j);
+                }
+            }
+            if (next) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
-        if (more) {
-            store_a(cur ^ 1);
-            store_b(cur ^ 1);
-        }
-        __syncthreads();
+                for (int i = NJ; i < MI; ++i)
+                    read_a(nst, fa[P ^ 1], i);
+            }
+        });
     }
 
     // ---------------------------------------------------------------- epilogue
+    constexpr int CPL = C::CPL;
+    constexpr int QMAX = (1 << BI) - 1;
     const int g = lane >> 4;
-    const int co_loc = wc * 64 + 16 * g;           // first of this lane's 16 channels
-    const int co_glob = co_tile * BLK_CO + co_loc;
-    const int32_t *prm = (const int32_t *)(lds + PRM_OFF);
-    constexpr int QMAX = (BO == 32) ? 0 : (1 << BO) - 1;
+    const int co_loc = wc * C::TM + CPL * g;
+    const int co_glob = co_tile * C::BCO + co_loc;
 
-    if (BO != 32 && co_glob >= A.cout)
+    if (!OUTK && co_glob >= A.cout)
         return;
 
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const long long px = (long long)px_tile * BLK_PX + wp * 128 + j * 16 + (lane & 15);
+    static_for<NJ>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        const long long px = (long long)px_tile * C::BPX + wp * C::TN + j * 16 + (lane & 15);
         if (px >= S.P)
-            continue;
-        // skip row of this pixel
-        long long spix = px;
-        if (SK && A.up2) {
-            int n_ = (int)(px / hw);
-            int rem = (int)(px - (long long)n_ * hw);
-            int oh = rem / S.wo, ow = rem - oh * S.wo;
-            spix = ((long long)n_ * S.hs + (oh >> 1)) * S.ws + (ow >> 1);
-        }
-        uint32_t skw[4] = {0, 0, 0, 0};  // packed skip codes of the 16 channels
-        if constexpr (SK == 2) {
-            skw[0] = *(const uint32_t *)((const uint8_t *)S.skip + spix * (A.cout / 4) + co_glob / 4);
-        } else if constexpr (SK == 4) {
-            uint2 t = *(const uint2 *)((const uint8_t *)S.skip + spix * (A.cout / 2) + co_glob / 2);
-            skw[0] = t.x;
-            skw[1] = t.y;
-        } else if constexpr (SK == 8) {
-            uint4 t = *(const uint4 *)((const uint8_t *)S.skip + spix * A.cout + co_glob);
-            skw[0] = t.x;
-            skw[1] = t.y;
-            skw[2] = t.z;
-            skw[3] = t.w;
-        }
-        uint32_t outw[(BO == 32) ? 1 : BO / 2];
+            return;
+        if constexpr (OUTK == 1) {
 #pragma unroll
-        for (int u = 0; u < ((BO == 32) ? 1 : BO / 2); ++u)
-            outw[u] = 0;
-
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int cl = co_loc + 4 * i;
-            const int4 bias4 = *(const int4 *)(prm + cl);
-            const int bias[4] = {bias4.x, bias4.y, bias4.z, bias4.w};
-            if constexpr (BO == 32) {
+            for (int i = 0; i < MI; ++i) {
                 if (co_glob + 4 * i < A.cout) {
+                    const int4 b4 = *(const int4 *)(prm + co_loc + 4 * i);
                     int4 o;
-                    o.x = acc[i][j][0] + bias[0];
-                    o.y = acc[i][j][1] + bias[1];
-                    o.z = acc[i][j][2] + bias[2];
-                    o.w = acc[i][j][3] + bias[3];
+                    o.x = acc[i][j][0] + b4.x;
+                    o.y = acc[i][j][1] + b4.y;
+                    o.z = acc[i][j][2] + b4.z;
+                    o.w = acc[i][j][3] + b4.w;
                     *(int4 *)((int32_t *)S.y + px * A.cout + co_glob + 4 * i) = o;
                 }
-            } else {
-                const int4 m4 = *(const int4 *)(prm + BLK_CO + cl);
-                const int4 s4 = *(const int4 *)(prm + 2 * BLK_CO + cl);
-                const int mult[4] = {m4.x, m4.y, m4.z, m4.w};
-                const int shf[4] = {s4.x, s4.y, s4.z, s4.w};
-                int kv[4] = {0, 0, 0, 0}, sc[4] = {0, 0, 0, 0}, sd[4] = {0, 0, 0, 0}, sside[4] = {0, 0, 0, 0};
-                if constexpr (SK != 0) {
-                    const int4 c4 = *(const int4 *)(prm + 3 * BLK_CO + cl);
-                    const int4 d4 = *(const int4 *)(prm + 4 * BLK_CO + cl);
-                    const int4 e4 = *(const int4 *)(prm + 5 * BLK_CO + cl);
-                    sc[0] = c4.x; sc[1] = c4.y; sc[2] = c4.z; sc[3] = c4.w;
-                    sd[0] = d4.x; sd[1] = d4.y; sd[2] = d4.z; sd[3] = d4.w;
-                    sside[0] = e4.x; sside[1] = e4.y; sside[2] = e4.z; sside[3] = e4.w;
-                    if constexpr (SK == 32) {
-                        const int4 k4 = *(const int4 *)((const int32_t *)S.skip + spix * A.cout + co_glob + 4 * i);
-                        kv[0] = k4.x; kv[1] = k4.y; kv[2] = k4.z; kv[3] = k4.w;
-                    } else {
+            }
+            return;
+        }
+        long long spix = px;
+        if (SKK && A.up2) {
+            const int n_ = (int)(px / hw);
+            const int rem = (int)(px - (long long)n_ * hw);
+            const int oh = rem / S.wo, ow = rem - oh * S.wo;
+            spix = ((long long)n_ * S.hs + (oh >> 1)) * S.ws + (ow >> 1);
+        }
+        uint32_t skw[C::OW];
+        if constexpr (SKK == 1)
+            load_words<C::OW>((const uint8_t *)S.skip + spix * (A.cout * BI / 8) + co_glob * BI / 8, skw);
+        uint32_t outw[C::OW];
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const int bit = (4 * i + e) * SK;
-                            kv[e] = (skw[bit >> 5] >> (bit & 31)) & ((1 << SK) - 1);
-                        }
+        for (int u = 0; u < C::OW; ++u)
+            outw[u] = 0;
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            const int cl = co_loc + 4 * i;
+            const int4 b4 = *(const int4 *)(prm + EPI_BIAS * C::BCO + cl);
+            const int4 m4 = *(const int4 *)(prm + EPI_MULT * C::BCO + cl);
+            const int4 s4 = *(const int4 *)(prm + (FAST ? EPI_SHR : EPI_SHIFT) * C::BCO + cl);
+            const int bias[4] = {b4.x, b4.y, b4.z, b4.w};
+            const int mult[4] = {m4.x, m4.y, m4.z, m4.w};
+            const int shf[4] = {s4.x, s4.y, s4.z, s4.w};
+            int rnd[4] = {0, 0, 0, 0};
+            if constexpr (FAST) {
+                const int4 r4 = *(const int4 *)(prm + EPI_RND * C::BCO + cl);
+                rnd[0] = r4.x; rnd[1] = r4.y; rnd[2] = r4.z; rnd[3] = r4.w;
+            }
+            int kv[4] = {0, 0, 0, 0}, sc[4] = {0, 0, 0, 0}, sd[4] = {0, 0, 0, 0}, sside[4] = {0, 0, 0, 0};
+            if constexpr (SKK != 0) {
+                const int4 c4 = *(const int4 *)(prm + EPI_SKIP_C * C::BCO + cl);
+                const int4 d4 = *(const int4 *)(prm + EPI_SKIP_D * C::BCO + cl);
+                const int4 e4 = *(const int4 *)(prm + EPI_SKIP_SIDE * C::BCO + cl);
+                sc[0] = c4.x; sc[1] = c4.y; sc[2] = c4.z; sc[3] = c4.w;
+                sd[0] = d4.x; sd[1] = d4.y; sd[2] = d4.z; sd[3] = d4.w;
+                sside[0] = e4.x; sside[1] = e4.y; sside[2] = e4.z; sside[3] = e4.w;
+                if constexpr (SKK == 2) {
+                    const int4 k4 = *(const int4 *)((const int32_t *)S.skip + spix * A.cout + co_glob + 4 * i);
+                    kv[0] = k4.x; kv[1] = k4.y; kv[2] = k4.z; kv[3] = k4.w;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int bit = (4 * i + e) * BI;
+                        kv[e] = (int)((skw[bit >> 5] >> (bit & 31)) & QMAX);
                     }
                 }
+            }
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int v = acc[i][j][e] + bias[e];
+            for (int e = 0; e < 4; ++e) {
+                const int v = acc[i][j][e] + bias[e];
+                int y;
+                if constexpr (FAST) {
+                    int u = v;
+                    if constexpr (SKK != 0) {
+                        const int scaled = rsm32(sside[e] ? v : kv[e], sc[e], sd[e]);
+                        u = scaled + (sside[e] ? kv[e] : v);
+                    }
+                    y = (__mulhi(u, mult[e]) + rnd[e]) >> shf[e];
+                    y = y < 0 ? 0 : (y > QMAX ? QMAX : y);
+                } else {
                     long long u = v;
-                    if constexpr (SK != 0)
+                    if constexpr (SKK != 0)
                         u = align_add(v, kv[e], sc[e], sd[e], sside[e]);
-                    const uint32_t code = requant_clamp(u, mult[e], shf[e], QMAX);
-                    const int bit = (4 * i + e) * BO;
-                    outw[bit >> 5] |= code << (bit & 31);
+                    y = (int)requant_clamp(u, mult[e], shf[e], QMAX);
                 }
+                const int bit = (4 * i + e) * BI;
+                outw[bit >> 5] |= (uint32_t)y << (bit & 31);
             }
         }
-        if constexpr (BO == 2) {
-            *(uint32_t *)((uint8_t *)S.y + px * (A.cout / 4) + co_glob / 4) = outw[0];
-        } else if constexpr (BO == 4) {
-            *(uint2 *)((uint8_t *)S.y + px * (A.cout / 2) + co_glob / 2) = make_uint2(outw[0], outw[1]);
-        } else if constexpr (BO == 8) {
-            *(uint4 *)((uint8_t *)S.y + px * A.cout + co_glob) = make_uint4(outw[0], outw[1], outw[2], outw[3]);
-        }
-    }
+        store_words<C::OW>((uint8_t *)S.y + px * (A.cout * BI / 8) + co_glob * BI / 8, outw);
+    });
 }
 
-template <int BI, int BO, int SK>
+template <int BI, int MI, int NJ, int WC, int OUTK, int SKK>
 hipError_t launch_t(const MfmaArgs &a, hipStream_t stream)
 {
     dim3 grid(8 * a.tiles_per_xcd), block(NT);
-    hipLaunchKernelGGL((qconv_mfma_kernel<BI, BO, SK>), grid, block, 0, stream, a);
+    bool fast = true;
+    for (int i = 0; i < a.nseg; ++i)
+        fast = fast && a.seg[i].fast;
+    if (OUTK == 1 || fast)
+        hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, OUTK, SKK, 1>), grid, block, 0, stream, a);
+    else
+        hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, OUTK, SKK, 0>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 
-template <int BI, int BO>
-hipError_t launch_skip(int skip_bits, const MfmaArgs &a, hipStream_t stream)
+template <int BI, int MI, int NJ, int WC>
+hipError_t launch_modes(const MfmaArgs &a, hipStream_t stream)
 {
-    switch (skip_bits) {
-    case 0: return launch_t<BI, BO, 0>(a, stream);
-    case 2: return launch_t<BI, BO, 2>(a, stream);
-    case 4: return launch_t<BI, BO, 4>(a, stream);
-    case 8: return launch_t<BI, BO, 8>(a, stream);
-    case 32: return launch_t<BI, BO, 32>(a, stream);
-    }
-    return hipErrorInvalidValue;
-}
-
-template <int BI>
-hipError_t launch_out(int out_bits, int skip_bits, const MfmaArgs &a, hipStream_t stream)
-{
-    switch (out_bits) {
-    case 2: return launch_skip<BI, 2>(skip_bits, a, stream);
-    case 4: return launch_skip<BI, 4>(skip_bits, a, stream);
-    case 8: return launch_skip<BI, 8>(skip_bits, a, stream);
-    case 32: return skip_bits ? hipErrorInvalidValue : launch_t<BI, 32, 0>(a, stream);
-    }
+    if (a.bits_out == 32)
+        return a.skip_bits ? hipErrorInvalidValue : launch_t<BI, MI, NJ, WC, 1, 0>(a, stream);
+    if (a.bits_out != BI)
+        return hipErrorInvalidValue;
+    if (a.skip_bits == 0)
+        return launch_t<BI, MI, NJ, WC, 0, 0>(a, stream);
+    if (a.skip_bits == 32)
+        return launch_t<BI, MI, NJ, WC, 0, 2>(a, stream);
+    if (a.skip_bits == BI)
+        return launch_t<BI, MI, NJ, WC, 0, 1>(a, stream);
     return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-hipError_t launch_qconv_mfma(int bits_in, int out_bits, int skip_bits, const MfmaArgs &a,
-                             hipStream_t stream)
+void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane)
 {
-    if (bits_in == 4)
-        return launch_out<4>(out_bits, skip_bits, a, stream);
-    if (bits_in == 2)
-        return launch_out<2>(out_bits, skip_bits, a, stream);
+    switch (tile_cfg) {
+    case TILE_256x128: *blk_co = 256; *blk_px = 128; *chan_per_lane = 32; return;
+    case TILE_128x256: *blk_co = 128; *blk_px = 256; *chan_per_lane = 16; return;
+    default: *blk_co = 64; *blk_px = 512; *chan_per_lane = 16; return;
+    }
+}
+
+hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
+{
+    if (bits_in == 4) {
+        switch (a.tile_cfg) {
+        case TILE_256x128: return launch_modes<4, 8, 4, 2>(a, stream);
+        case TILE_128x256: return launch_modes<4, 4, 8, 2>(a, stream);
+        case TILE_64x512: return launch_modes<4, 4, 8, 1>(a, stream);
+        }
+    } else if (bits_in == 2) {
+        switch (a.tile_cfg) {
+        case TILE_128x256: return launch_modes<2, 4, 8, 2>(a, stream);
+        case TILE_64x512: return launch_modes<2, 4, 8, 1>(a, stream);
+        }
+    }
     return hipErrorInvalidValue;
 }
 

@@ -42,7 +42,24 @@ MFMA_CASES = [
     (2, 11, 13, 256, 36, 3, 1, 4, 4, 1, 32, 0, False),      # box prediction: 36 channels
     (1, 7, 11, 64, 64, 3, 1, 4, 4, 0, 4, 0, False),         # one partial tile
     (3, 1, 1, 64, 32, 3, 1, 4, 4, 0, 4, 0, False),          # 1x1 image, all taps but one padded
+    (1, 30, 31, 128, 256, 1, 1, 4, 4, 0, 4, 0, False),      # 2 K steps
+    (1, 29, 33, 256, 128, 1, 1, 2, 2, 1, 2, 0, False),      # 4 K steps, 2-bit
+    (1, 31, 17, 320, 64, 1, 1, 4, 4, 0, 4, 4, False),       # 5 K steps
+    (2, 40, 37, 64, 512, 3, 2, 4, 4, 1, 4, 0, False),       # several 256x256 tiles, stride 2
 ]
+
+
+def test_conv_mfma_general_requant_path(torch):
+    """Levels with shift < 2 take the 64-bit requantisation path."""
+    for seed, skip in ((11, 0), (12, 4)):
+        case = workloads.random_conv_case(seed=seed, n=1, h=21, w=23, cin=64, cout=128, k=1,
+                                          bits_in=2, bits_w=2, bits_out=4, skip_bits=skip)
+        rng = np.random.Generator(np.random.PCG64(seed))
+        for lv in case.levels:
+            lv["shift"] = rng.integers(-2, 2, size=128).astype(np.int32)
+            lv["mult"] = rng.integers(1 << 26, 1 << 28, size=128).astype(np.int32)
+        for level, got in enumerate(gpu_conv(case, torch)):
+            assert_same(got, oracle_conv(case, level), f"general path, skip {skip}")
 
 
 @pytest.mark.parametrize("case", MFMA_CASES, ids=lambda c: "x".join(map(str, c)))
