@@ -113,6 +113,7 @@ struct qconv_s {
     void *w_dev;
     int32_t *epi_dev;  // [num_levels][EPI_FIELDS][cout_pad]
     std::vector<int> fast;  // per level: every shift >= 2
+    std::vector<int> side0; // per level: every skip side is 0
     const uint8_t *zero;    // the device's zero page
 };
 
@@ -214,6 +215,13 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
     h.cout_pad = mfma ? h.co_tiles * BLK_CO : d.cout;
     h.ksteps = mfma ? taps * (d.cin / KC) : 0;
     h.fast.assign(d.num_levels, 0);
+    h.side0.assign(d.num_levels, 0);
+    for (int l = 0; l < d.num_levels && d.skip_bits; ++l) {
+        int ok = 1;
+        for (int c = 0; c < d.cout; ++c)
+            ok &= levels[l].skip_side[c] == 0;
+        h.side0[l] = ok;
+    }
     for (int l = 0; l < d.num_levels && codes; ++l) {
         int ok = 1;
         for (int c = 0; c < d.cout; ++c)
@@ -460,6 +468,7 @@ aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t st
         m.ws = s.ws;
         m.tile_begin = tiles;
         m.fast = s.conv->fast[s.level];
+        m.side0 = s.conv->side0[s.level];
         const long long px_tiles = (m.P + h0.blk_px - 1) / h0.blk_px;
         REQUIRE(tiles + px_tiles * h0.co_tiles < (1LL << 30), "too many tiles for one launch");
         tiles += (int)(px_tiles * h0.co_tiles);

@@ -35,6 +35,7 @@ struct MfmaSeg {
     int n, h, w, ho, wo, hs, ws;
     int tile_begin;      // first workgroup tile of this segment
     int fast;            // every shift of the level >= 2: 32-bit requantisation
+    int side0;           // every skip side of the level is 0 (code skips use a table)
 };
 
 struct MfmaArgs {

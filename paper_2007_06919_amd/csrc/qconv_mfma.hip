@@ -64,7 +64,6 @@ __device__ __forceinline__ void static_for(F &&f)
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 
-constexpr int NT = 256;
 
 // round(a * c / 2^d), ties up, d in [0, 31], result assumed to fit in int32
 __device__ __forceinline__ int rsm32(int a, int c, int d)
@@ -78,9 +77,11 @@ __device__ __forceinline__ int rsm32(int a, int c, int d)
 }
 
 
-template <int BI, int MI, int NJ, int WC>
+template <int BI, int MI, int NJ, int WC, int WP>
 struct Cfg {
-    static constexpr int WP = 4 / WC;
+    static constexpr int WPC = WP;                // waves along pixels
+    static constexpr int NW = WC * WP;            // waves per workgroup
+    static constexpr int NTH = 64 * NW;           // threads per workgroup
     static constexpr int TM = 16 * MI;            // channels per wave
     static constexpr int TN = 16 * NJ;            // pixels per wave
     static constexpr int BCO = WC * TM;           // channels per workgroup
@@ -89,16 +90,21 @@ struct Cfg {
     static constexpr int A_STAGE = BCO * KC;      // int8 weight rows of 64 B
     static constexpr int B_STAGE = BPX * PB;      // packed code rows of PB bytes
     static constexpr int STAGE = A_STAGE + B_STAGE;
-    static constexpr int NSTAGE = STAGE <= 16384 ? 4 : 3;  // ring depth: two workgroups per CU
-    static constexpr int A_PER = A_STAGE / 1024 / 4;       // 1 KiB copies per wave and K step
-    static constexpr int B_PER = B_STAGE / 1024 / 4;
+    // ring depth: 8-wave workgroups own the CU's LDS, 4-wave ones share it with a
+    // second; the epilogue table reuses the ring after the last K step
+    static constexpr int LDS_BUDGET = NW == 8 ? 163840 : 81920;
+    static constexpr int NSTAGE = LDS_BUDGET / STAGE < 6 ? LDS_BUDGET / STAGE : 6;
+    static constexpr int A_PER = A_STAGE / 1024 / NW;      // 1 KiB copies per wave and K step
+    static constexpr int B_PER = B_STAGE / 1024 / NW;
     static constexpr int NOPS = A_PER + B_PER;             // copy instructions per lane and K step
     static constexpr int BPC = 1024 / PB;                  // pixels per 1 KiB chunk (32 / 64)
     static constexpr int LPP = 64 / BPC;                   // lanes per pixel row (2 / 1)
     static constexpr int CPL = 4 * MI;                     // channels per lane and pixel (epilogue)
     static constexpr int OW = CPL * BI / 32;               // packed output dwords per lane and pixel
-    static_assert(A_STAGE % 4096 == 0 && B_STAGE % 4096 == 0, "a stage splits into 4 waves x 1 KiB");
-    static_assert(2 * (NSTAGE * STAGE + 8 * BCO * 4) <= 163840, "two workgroups per CU");
+    static_assert(A_STAGE % (1024 * NW) == 0 && B_STAGE % (1024 * NW) == 0,
+                  "a stage splits into 1 KiB copies, the same number per wave");
+    static_assert(NSTAGE >= 3, "ring of at least three stages");
+    static_assert(NSTAGE * STAGE >= EPI_FIELDS * BCO * 4, "epilogue table fits in the ring");
 };
 
 // XOR swizzle of the 16-byte columns of weight row r (64-byte rows): the
@@ -168,12 +174,12 @@ __device__ __forceinline__ void store_words(uint8_t *p, const uint32_t *w)
 // OUTK: 0 = codes of width BI, 1 = int32.
 // SKK: 0 = none, 1 = codes of width BI, 2 = int32.
 // FAST: every segment's shifts are >= 2 (32-bit requantisation).
-template <int BI, int MI, int NJ, int WC, int OUTK, int SKK, int FAST>
-__global__ void __launch_bounds__(NT, 2) qconv_mfma_kernel(MfmaArgs A)
+template <int BI, int MI, int NJ, int WC, int WP, int OUTK, int SKK, int FAST>
+__global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel(MfmaArgs A)
 {
-    using C = Cfg<BI, MI, NJ, WC>;
+    using C = Cfg<BI, MI, NJ, WC, WP>;
+    constexpr int NT = C::NTH;
     __shared__ __attribute__((aligned(1024))) uint8_t lds_stages[C::NSTAGE * C::STAGE];
-    __shared__ __attribute__((aligned(16))) int32_t prm[EPI_FIELDS * C::BCO];
 
     const int bid = blockIdx.x;
     const int logical = (bid & 7) * A.tiles_per_xcd + (bid >> 3);
@@ -193,21 +199,15 @@ __global__ void __launch_bounds__(NT, 2) qconv_mfma_kernel(MfmaArgs A)
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wc = wave / C::WP;
-    const int wp = wave % C::WP;
+    const int wc = wave / C::WPC;
+    const int wp = wave % C::WPC;
 
     const int row_bytes = A.cin * BI / 8;
     const int kpt = A.cin / KC;
     const int KS = A.ksteps;
     const int hw = S.ho * S.wo;
 
-    // epilogue table of this channel tile -> LDS
-    for (int i = tid; i < EPI_FIELDS * C::BCO; i += NT) {
-        const int which = i / C::BCO, c = i - which * C::BCO;
-        prm[which * C::BCO + c] = S.epi[which * A.cout_pad + co_tile * C::BCO + c];
-    }
-
-    // Copies: chunk q of a stage (1 KiB) belongs to wave q % 4; which source
+    // Copies: chunk q of a stage (1 KiB) belongs to wave q % NW; which source
     // bytes a lane fetches implements the LDS swizzle.
     //  weights: chunk q = rows 16q .. 16q+15; lane L -> row 16q + L/4, LDS
     //           column L%4 holding logical column (L%4) ^ swz_a(row)
@@ -216,7 +216,7 @@ __global__ void __launch_bounds__(NT, 2) qconv_mfma_kernel(MfmaArgs A)
     int a_src[C::A_PER];
 #pragma unroll
     for (int t = 0; t < C::A_PER; ++t) {
-        const int row = 16 * (4 * t + wave) + (lane >> 2);
+        const int row = 16 * (C::NW * t + wave) + (lane >> 2);
         a_src[t] = row * KC + 16 * ((lane & 3) ^ swz_a(row));
     }
     int ih0[C::B_PER], iw0[C::B_PER];
@@ -224,7 +224,7 @@ __global__ void __launch_bounds__(NT, 2) qconv_mfma_kernel(MfmaArgs A)
     bool pv[C::B_PER];
 #pragma unroll
     for (int t = 0; t < C::B_PER; ++t) {
-        const int ploc = C::BPC * (4 * t + wave) + lane / C::LPP;
+        const int ploc = C::BPC * (C::NW * t + wave) + lane / C::LPP;
         const int part = lane % C::LPP;
         const long long p = (long long)px_tile * C::BPX + ploc;
         pv[t] = p < S.P;
@@ -239,7 +239,7 @@ __global__ void __launch_bounds__(NT, 2) qconv_mfma_kernel(MfmaArgs A)
     // Copy state: steps are issued in order, so the per-pixel source of the
     // current tap is computed once per tap (bsrc; null for padding taps).
     const int8_t *a_next = S.wt + (long long)co_tile * KS * C::A_STAGE;
-    int tap_next = 0, cc_next = 0, ks_next = 0;
+    int tap_next = 0, cc_next = 0, st_next = 0;
     const uint8_t *bsrc[C::B_PER];
     auto issue = [&]() {
         if (cc_next == 0) {
@@ -252,15 +252,16 @@ __global__ void __launch_bounds__(NT, 2) qconv_mfma_kernel(MfmaArgs A)
                 bsrc[t] = ok ? xb[t] + ((long long)ih * S.w + iw) * row_bytes : nullptr;
             }
         }
-        uint8_t *st = lds_stages + (ks_next % C::NSTAGE) * C::STAGE;
+        uint8_t *st = lds_stages + st_next * C::STAGE;
 #pragma unroll
         for (int t = 0; t < C::A_PER; ++t)
-            dma16(a_next + a_src[t], st + (4 * t + wave) * 1024);
+            dma16(a_next + a_src[t], st + (C::NW * t + wave) * 1024);
 #pragma unroll
         for (int t = 0; t < C::B_PER; ++t)
-            dma16(bsrc[t] ? bsrc[t] + cc_next * C::PB : A.zero, st + C::A_STAGE + (4 * t + wave) * 1024);
+            dma16(bsrc[t] ? bsrc[t] + cc_next * C::PB : A.zero, st + C::A_STAGE + (C::NW * t + wave) * 1024);
         a_next += C::A_STAGE;
-        ++ks_next;
+        if (++st_next == C::NSTAGE)
+            st_next = 0;
         if (++cc_next == kpt) {
             cc_next = 0;
             ++tap_next;
@@ -271,7 +272,8 @@ __global__ void __launch_bounds__(NT, 2) qconv_mfma_kernel(MfmaArgs A)
         switch (steps) {
         case 0: wait_vmcnt<0>(); break;
         case 1: wait_vmcnt<C::NOPS>(); break;
-        default: wait_vmcnt<2 * C::NOPS>(); break;
+        case 2: wait_vmcnt<2 * C::NOPS>(); break;
+        default: wait_vmcnt<3 * C::NOPS>(); break;
         }
     };
 
@@ -322,15 +324,16 @@ __global__ void __launch_bounds__(NT, 2) qconv_mfma_kernel(MfmaArgs A)
         read_a(0, fa[0], i);
 
     // step ks: MFMAs on register set ks & 1 while the fragments of step ks + 1
-    // are read into the other set; copies run NSTAGE - 1 steps ahead.
+    // are read into the other set (after the last step these reads fetch
+    // unused data); copies run NSTAGE - 1 steps ahead.
+    int st_read = 1 % C::NSTAGE;  // stage of step ks + 1
     for (int k0 = 0; k0 < KS; k0 += 2) {
         static_for<2>([&](auto pc) {
             constexpr int P = decltype(pc)::value;
             const int ks = k0 + P;
             if (ks >= KS)
                 return;
-            const bool next = ks + 1 < KS;
-            if (next) {
+            if (ks + 1 < KS) {
                 // step ks + 1 landed: copies up to step min(ks + NSTAGE - 2, KS - 1) were issued
                 const int last = ks + C::NSTAGE - 2 < KS - 1 ? ks + C::NSTAGE - 2 : KS - 1;
                 wait_steps(last - (ks + 1));
@@ -340,73 +343,130 @@ __global__ void __launch_bounds__(NT, 2) qconv_mfma_kernel(MfmaArgs A)
                 if (ks + C::NSTAGE - 1 < KS)
                     issue();
             }
-            const int nst = (ks + 1) % C::NSTAGE;
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
                 const v4i bj = widen(fb[P][j]);
 #pragma unroll
                 for (int i = 0; i < MI; ++i)
                     acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[P][i], bj, acc[i][j], 0, 0, 0);
-                if (next) {
-                    read_b(nst, fb[P ^ 1], j);
-                    if (j < MI)
-                        read_a(nst, fa[P ^ 1], j);
-                }
+                read_b(st_read, fb[P ^ 1], j);
+                if (j < MI)
+                    read_a(st_read, fa[P ^ 1], j);
             }
-            if (next) {
 #pragma unroll
-                for (int i = NJ; i < MI; ++i)
-                    read_a(nst, fa[P ^ 1], i);
-            }
+            for (int i = NJ; i < MI; ++i)
+                read_a(st_read, fa[P ^ 1], i);
+            if (++st_read == C::NSTAGE)
+                st_read = 0;
         });
     }
 
     // ---------------------------------------------------------------- epilogue
-    constexpr int CPL = C::CPL;
+    // The ring is idle after the last step; it now holds this channel tile's
+    // epilogue table, the side-0 skip table and the int32 output staging.
     constexpr int QMAX = (1 << BI) - 1;
+    constexpr int CPL = C::CPL;
+    int32_t *prm = (int32_t *)lds_stages;
+    int32_t *lut = prm + EPI_FIELDS * C::BCO;            // [BCO][2^BI]: RSM(k, c, d)
+    const bool use_lut = SKK == 1 && S.side0;            // uniform over the workgroup
+    __syncthreads();  // every wave is done with the ring
+    for (int i = tid; i < EPI_FIELDS * C::BCO; i += NT) {
+        const int which = i / C::BCO, c = i - which * C::BCO;
+        prm[which * C::BCO + c] = S.epi[which * A.cout_pad + co_tile * C::BCO + c];
+    }
+    if (use_lut) {
+        // every skip operand is a b-bit code scaled by c / 2^d (side 0): tabulate
+        for (int i = tid; i < C::BCO * (QMAX + 1); i += NT) {
+            const int ch = co_tile * C::BCO + (i >> BI);
+            lut[i] = rsm32(i & QMAX, S.epi[EPI_SKIP_C * A.cout_pad + ch], S.epi[EPI_SKIP_D * A.cout_pad + ch]);
+        }
+    }
+    __syncthreads();
+
     const int g = lane >> 4;
-    const int co_loc = wc * C::TM + CPL * g;
+    const int co_loc = wc * C::TM + CPL * g;      // first of this lane's CPL channels (in the tile)
     const int co_glob = co_tile * C::BCO + co_loc;
+    const long long px0 = (long long)px_tile * C::BPX + wp * C::TN + (lane & 15);
 
-    if (!OUTK && co_glob >= A.cout)
-        return;
+    // int32 tiles (outputs, int32 skips) move between HBM and registers through
+    // a per-wave LDS staging area, JP column tiles (16 JP pixel rows) at a time,
+    // so that global accesses cover whole contiguous channel runs of a pixel row
+    constexpr int ROWB = C::TM * 4 + 16;          // staged row: TM channels + pad (bank spread)
+    constexpr int JP = 2;                         // column tiles per pass
+    constexpr int LPR = C::TM / 4;                // lanes per staged row (16 B each)
+    constexpr int RPI = 64 / LPR;                 // rows per instruction
+    static_assert(EPI_FIELDS * C::BCO * 4 + C::NW * 16 * JP * ROWB <= C::NSTAGE * C::STAGE,
+                  "int32 staging fits in the ring");
+    uint8_t *stg = lds_stages + EPI_FIELDS * C::BCO * 4 + wave * (16 * JP * ROWB);
 
-    static_for<NJ>([&](auto jc) {
-        constexpr int j = decltype(jc)::value;
-        const long long px = (long long)px_tile * C::BPX + wp * C::TN + j * 16 + (lane & 15);
-        if (px >= S.P)
-            return;
-        if constexpr (OUTK == 1) {
+    if constexpr (OUTK == 1) {
+        static_for<NJ / JP>([&](auto pc) {
+            constexpr int pass = decltype(pc)::value;
+            static_for<JP>([&](auto jc) {
+                constexpr int jj = decltype(jc)::value;
+                constexpr int j = pass * JP + jj;
 #pragma unroll
-            for (int i = 0; i < MI; ++i) {
-                if (co_glob + 4 * i < A.cout) {
+                for (int i = 0; i < MI; ++i) {
                     const int4 b4 = *(const int4 *)(prm + co_loc + 4 * i);
                     int4 o;
                     o.x = acc[i][j][0] + b4.x;
                     o.y = acc[i][j][1] + b4.y;
                     o.z = acc[i][j][2] + b4.z;
                     o.w = acc[i][j][3] + b4.w;
-                    *(int4 *)((int32_t *)S.y + px * A.cout + co_glob + 4 * i) = o;
+                    *(int4 *)(stg + (jj * 16 + (lane & 15)) * ROWB + (CPL * g + 4 * i) * 4) = o;
                 }
+            });
+            __syncthreads();
+#pragma unroll
+            for (int r = 0; r < 16 * JP; r += RPI) {
+                const int row = r + lane / LPR;
+                const int cw = (lane % LPR) * 4;                       // channel within the wave
+                const long long px = (long long)px_tile * C::BPX + wp * C::TN + pass * JP * 16 + row;
+                const int ch = co_tile * C::BCO + wc * C::TM + cw;
+                const int4 v = *(const int4 *)(stg + row * ROWB + cw * 4);
+                if (px < S.P && ch < A.cout)
+                    *(int4 *)((int32_t *)S.y + px * A.cout + ch) = v;
             }
-            return;
-        }
-        long long spix = px;
-        if (SKK && A.up2) {
-            const int n_ = (int)(px / hw);
-            const int rem = (int)(px - (long long)n_ * hw);
-            const int oh = rem / S.wo, ow = rem - oh * S.wo;
-            spix = ((long long)n_ * S.hs + (oh >> 1)) * S.ws + (ow >> 1);
-        }
-        uint32_t skw[C::OW];
-        if constexpr (SKK == 1)
-            load_words<C::OW>((const uint8_t *)S.skip + spix * (A.cout * BI / 8) + co_glob * BI / 8, skw);
-        uint32_t outw[C::OW];
+            __syncthreads();  // staging is rewritten by the next pass
+        });
+        return;
+    }
+
+    const bool co_ok = co_glob < A.cout;  // CPL channels are all valid or all padding
+
+    // per pixel column: validity, skip codes, packed output codes
+    bool okj[NJ];
+    uint32_t skw[NJ][C::OW];
+    uint32_t outw[NJ][C::OW];
+    static_for<NJ>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        const long long px = px0 + j * 16;
+        okj[j] = co_ok && px < S.P;
 #pragma unroll
-        for (int u = 0; u < C::OW; ++u)
-            outw[u] = 0;
-#pragma unroll
-        for (int i = 0; i < MI; ++i) {
+        for (int u = 0; u < C::OW; ++u) {
+            skw[j][u] = 0;
+            outw[j][u] = 0;
+        }
+        if constexpr (SKK == 1) {
+            if (okj[j]) {
+                long long spix = px;
+                if (A.up2) {
+                    const int n_ = (int)(px / hw);
+                    const int rem = (int)(px - (long long)n_ * hw);
+                    const int oh = rem / S.wo, ow = rem - oh * S.wo;
+                    spix = ((long long)n_ * S.hs + (oh >> 1)) * S.ws + (ow >> 1);
+                }
+                load_words<C::OW>((const uint8_t *)S.skip + spix * (A.cout * BI / 8) + co_glob * BI / 8, skw[j]);
+            }
+        }
+    });
+
+    // columns [J0, J0 + JN): channel group outer (parameters read once), column inner
+    auto body = [&](auto lut_c, auto j0_c, auto jn_c) {
+        constexpr bool LUT = decltype(lut_c)::value;
+        constexpr int J0 = decltype(j0_c)::value, JN = decltype(jn_c)::value;
+        static_for<MI>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
             const int cl = co_loc + 4 * i;
             const int4 b4 = *(const int4 *)(prm + EPI_BIAS * C::BCO + cl);
             const int4 m4 = *(const int4 *)(prm + EPI_MULT * C::BCO + cl);
@@ -419,78 +479,132 @@ __global__ void __launch_bounds__(NT, 2) qconv_mfma_kernel(MfmaArgs A)
                 const int4 r4 = *(const int4 *)(prm + EPI_RND * C::BCO + cl);
                 rnd[0] = r4.x; rnd[1] = r4.y; rnd[2] = r4.z; rnd[3] = r4.w;
             }
-            int kv[4] = {0, 0, 0, 0}, sc[4] = {0, 0, 0, 0}, sd[4] = {0, 0, 0, 0}, sside[4] = {0, 0, 0, 0};
-            if constexpr (SKK != 0) {
+            int sc[4] = {0, 0, 0, 0}, sd[4] = {0, 0, 0, 0}, sside[4] = {0, 0, 0, 0};
+            if constexpr (SKK != 0 && !LUT) {
                 const int4 c4 = *(const int4 *)(prm + EPI_SKIP_C * C::BCO + cl);
                 const int4 d4 = *(const int4 *)(prm + EPI_SKIP_D * C::BCO + cl);
                 const int4 e4 = *(const int4 *)(prm + EPI_SKIP_SIDE * C::BCO + cl);
                 sc[0] = c4.x; sc[1] = c4.y; sc[2] = c4.z; sc[3] = c4.w;
                 sd[0] = d4.x; sd[1] = d4.y; sd[2] = d4.z; sd[3] = d4.w;
                 sside[0] = e4.x; sside[1] = e4.y; sside[2] = e4.z; sside[3] = e4.w;
+            }
+            static_for<JN>([&](auto jc) {
+                constexpr int j = J0 + decltype(jc)::value;
+                if (!okj[j])
+                    return;
+                int kv[4] = {0, 0, 0, 0};
                 if constexpr (SKK == 2) {
-                    const int4 k4 = *(const int4 *)((const int32_t *)S.skip + spix * A.cout + co_glob + 4 * i);
+                    const int4 k4 = *(const int4 *)(stg + ((j - J0) * 16 + (lane & 15)) * ROWB + (CPL * g + 4 * i) * 4);
                     kv[0] = k4.x; kv[1] = k4.y; kv[2] = k4.z; kv[3] = k4.w;
-                } else {
+                } else if constexpr (SKK == 1) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const int bit = (4 * i + e) * BI;
-                        kv[e] = (int)((skw[bit >> 5] >> (bit & 31)) & QMAX);
+                        kv[e] = (int)((skw[j][bit >> 5] >> (bit & 31)) & QMAX);
                     }
                 }
-            }
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int v = acc[i][j][e] + bias[e];
-                int y;
-                if constexpr (FAST) {
-                    int u = v;
-                    if constexpr (SKK != 0) {
-                        const int scaled = rsm32(sside[e] ? v : kv[e], sc[e], sd[e]);
-                        u = scaled + (sside[e] ? kv[e] : v);
+                for (int e = 0; e < 4; ++e) {
+                    const int v = acc[i][j][e] + bias[e];
+                    int y;
+                    if constexpr (FAST) {
+                        int u = v;
+                        // u fits in int32, so the sum modulo 2^32 is exact
+                        if constexpr (LUT) {
+                            u = (int)((unsigned)v + (unsigned)lut[((cl + e) << BI) | kv[e]]);
+                        } else if constexpr (SKK != 0) {
+                            const int scaled = rsm32(sside[e] ? v : kv[e], sc[e], sd[e]);
+                            u = (int)((unsigned)scaled + (unsigned)(sside[e] ? kv[e] : v));
+                        }
+                        y = (__mulhi(u, mult[e]) + rnd[e]) >> shf[e];
+                        y = y < 0 ? 0 : (y > QMAX ? QMAX : y);
+                    } else {
+                        long long u = v;
+                        if constexpr (LUT)
+                            u = (int)((unsigned)v + (unsigned)lut[((cl + e) << BI) | kv[e]]);
+                        else if constexpr (SKK != 0)
+                            u = align_add(v, kv[e], sc[e], sd[e], sside[e]);
+                        y = (int)requant_clamp(u, mult[e], shf[e], QMAX);
                     }
-                    y = (__mulhi(u, mult[e]) + rnd[e]) >> shf[e];
-                    y = y < 0 ? 0 : (y > QMAX ? QMAX : y);
-                } else {
-                    long long u = v;
-                    if constexpr (SKK != 0)
-                        u = align_add(v, kv[e], sc[e], sd[e], sside[e]);
-                    y = (int)requant_clamp(u, mult[e], shf[e], QMAX);
+                    const int bit = (4 * i + e) * BI;
+                    outw[j][bit >> 5] |= (uint32_t)y << (bit & 31);
                 }
-                const int bit = (4 * i + e) * BI;
-                outw[bit >> 5] |= (uint32_t)y << (bit & 31);
+            });
+        });
+    };
+    using I0 = std::integral_constant<int, 0>;
+    using INJ = std::integral_constant<int, NJ>;
+    if constexpr (SKK == 2) {
+        // int32 skip: JP column tiles per pass, staged with row-contiguous loads
+        static_for<NJ / JP>([&](auto pc) {
+            constexpr int pass = decltype(pc)::value;
+#pragma unroll
+            for (int r = 0; r < 16 * JP; r += RPI) {
+                const int row = r + lane / LPR;
+                const int cw = (lane % LPR) * 4;
+                const long long px = (long long)px_tile * C::BPX + wp * C::TN + pass * JP * 16 + row;
+                const int ch = co_tile * C::BCO + wc * C::TM + cw;
+                int4 v = make_int4(0, 0, 0, 0);
+                if (px < S.P && ch < A.cout) {
+                    long long spix = px;
+                    if (A.up2) {
+                        const int n_ = (int)(px / hw);
+                        const int rem = (int)(px - (long long)n_ * hw);
+                        const int oh = rem / S.wo, ow = rem - oh * S.wo;
+                        spix = ((long long)n_ * S.hs + (oh >> 1)) * S.ws + (ow >> 1);
+                    }
+                    v = *(const int4 *)((const int32_t *)S.skip + spix * A.cout + ch);
+                }
+                *(int4 *)(stg + row * ROWB + cw * 4) = v;
             }
-        }
-        store_words<C::OW>((uint8_t *)S.y + px * (A.cout * BI / 8) + co_glob * BI / 8, outw);
+            __syncthreads();
+            body(std::false_type{}, std::integral_constant<int, pass * JP>{},
+                 std::integral_constant<int, JP>{});
+            __syncthreads();  // staging is rewritten by the next pass
+        });
+    } else if constexpr (SKK == 1) {
+        if (use_lut)
+            body(std::true_type{}, I0{}, INJ{});
+        else
+            body(std::false_type{}, I0{}, INJ{});
+    } else {
+        body(std::false_type{}, I0{}, INJ{});
+    }
+
+    static_for<NJ>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        if (okj[j])
+            store_words<C::OW>((uint8_t *)S.y + (px0 + j * 16) * (A.cout * BI / 8) + co_glob * BI / 8, outw[j]);
     });
 }
 
-template <int BI, int MI, int NJ, int WC, int OUTK, int SKK>
+template <int BI, int MI, int NJ, int WC, int WP, int OUTK, int SKK>
 hipError_t launch_t(const MfmaArgs &a, hipStream_t stream)
 {
-    dim3 grid(8 * a.tiles_per_xcd), block(NT);
+    dim3 grid(8 * a.tiles_per_xcd), block(64 * WC * WP);
     bool fast = true;
     for (int i = 0; i < a.nseg; ++i)
         fast = fast && a.seg[i].fast;
     if (OUTK == 1 || fast)
-        hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, OUTK, SKK, 1>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, WP, OUTK, SKK, 1>), grid, block, 0, stream, a);
     else
-        hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, OUTK, SKK, 0>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, WP, OUTK, SKK, 0>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 
-template <int BI, int MI, int NJ, int WC>
+template <int BI, int MI, int NJ, int WC, int WP>
 hipError_t launch_modes(const MfmaArgs &a, hipStream_t stream)
 {
     if (a.bits_out == 32)
-        return a.skip_bits ? hipErrorInvalidValue : launch_t<BI, MI, NJ, WC, 1, 0>(a, stream);
+        return a.skip_bits ? hipErrorInvalidValue : launch_t<BI, MI, NJ, WC, WP, 1, 0>(a, stream);
     if (a.bits_out != BI)
         return hipErrorInvalidValue;
     if (a.skip_bits == 0)
-        return launch_t<BI, MI, NJ, WC, 0, 0>(a, stream);
+        return launch_t<BI, MI, NJ, WC, WP, 0, 0>(a, stream);
     if (a.skip_bits == 32)
-        return launch_t<BI, MI, NJ, WC, 0, 2>(a, stream);
+        return launch_t<BI, MI, NJ, WC, WP, 0, 2>(a, stream);
     if (a.skip_bits == BI)
-        return launch_t<BI, MI, NJ, WC, 0, 1>(a, stream);
+        return launch_t<BI, MI, NJ, WC, WP, 0, 1>(a, stream);
     return hipErrorInvalidValue;
 }
 
@@ -509,14 +623,14 @@ hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
 {
     if (bits_in == 4) {
         switch (a.tile_cfg) {
-        case TILE_256x128: return launch_modes<4, 8, 4, 2>(a, stream);
-        case TILE_128x256: return launch_modes<4, 4, 8, 2>(a, stream);
-        case TILE_64x512: return launch_modes<4, 4, 8, 1>(a, stream);
+        case TILE_256x128: return launch_modes<4, 8, 4, 2, 2>(a, stream);
+        case TILE_128x256: return launch_modes<4, 4, 8, 2, 2>(a, stream);
+        case TILE_64x512: return launch_modes<4, 4, 8, 1, 4>(a, stream);
         }
     } else if (bits_in == 2) {
         switch (a.tile_cfg) {
-        case TILE_128x256: return launch_modes<2, 4, 8, 2>(a, stream);
-        case TILE_64x512: return launch_modes<2, 4, 8, 1>(a, stream);
+        case TILE_128x256: return launch_modes<2, 4, 8, 2, 2>(a, stream);
+        case TILE_64x512: return launch_modes<2, 4, 8, 1, 4>(a, stream);
         }
     }
     return hipErrorInvalidValue;
