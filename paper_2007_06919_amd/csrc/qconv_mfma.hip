@@ -114,21 +114,25 @@ __device__ __forceinline__ int swz_a(int r) { return ((r >> 1) ^ (r >> 2)) & 3; 
 // XOR swizzle of the 16-byte halves of a 32-byte packed 4-bit code row.
 __device__ __forceinline__ int swz_b4(int p) { return (p >> 3) & 1; }
 
-// 16 bytes per lane from global memory straight into LDS at l + 16 * lane
-// (l wave-uniform, in M0). Issued as inline assembly so that the compiler does
-// not track it: every wait for these copies is an explicit wait_vmcnt (the
-// counter retires in issue order, so the compiler's own waits for later loads
-// stay correct, only stricter).
+// 16 bytes per lane from global memory straight into LDS at byte address
+// la + 16 * lane (la wave-uniform, kept in SGPRs, in M0). Issued as inline
+// assembly so that the compiler does not track it: every wait for these
+// copies is an explicit wait_vmcnt (the counter retires in issue order, so the
+// compiler's own waits for later loads stay correct, only stricter).
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void dma16(const void *g, uint8_t *l)
+__device__ __forceinline__ void dma16(const void *g, uint32_t la)
 {
-    const uint32_t la = __builtin_amdgcn_readfirstlane(
-        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)l);
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
                  ::"s"(la), "v"(g) : "memory", "m0");
 }
 #pragma clang diagnostic pop
+
+// LDS byte address of a shared-memory pointer
+__device__ __forceinline__ uint32_t lds_addr(const void *p)
+{
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t *)p;
+}
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt()
@@ -198,7 +202,7 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: SGPR arithmetic
     const int wc = wave / C::WPC;
     const int wp = wave % C::WPC;
 
@@ -239,9 +243,15 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
     // Copy state: steps are issued in order, so the per-pixel source of the
     // current tap is computed once per tap (bsrc; null for padding taps).
     const int8_t *a_next = S.wt + (long long)co_tile * KS * C::A_STAGE;
+    const uint32_t lds_base = lds_addr(lds_stages);
     int tap_next = 0, cc_next = 0, st_next = 0;
     const uint8_t *bsrc[C::B_PER];
-    auto issue = [&]() {
+    // A step's copies are issued in three parts so that the main loop can
+    // spread them between its MFMAs: issue_begin (the tap's sources, at a tap
+    // change), issue_copy<d> for d = 0 .. NOPS-1 (activation copies first),
+    // issue_end (advance to the next step).
+    uint32_t st_cur = 0;
+    auto issue_begin = [&]() {
         if (cc_next == 0) {
             const int r = tap_next / A.kw;
             const int q = tap_next - r * A.kw;
@@ -252,13 +262,16 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
                 bsrc[t] = ok ? xb[t] + ((long long)ih * S.w + iw) * row_bytes : nullptr;
             }
         }
-        uint8_t *st = lds_stages + st_next * C::STAGE;
-#pragma unroll
-        for (int t = 0; t < C::A_PER; ++t)
-            dma16(a_next + a_src[t], st + (C::NW * t + wave) * 1024);
-#pragma unroll
-        for (int t = 0; t < C::B_PER; ++t)
-            dma16(bsrc[t] ? bsrc[t] + cc_next * C::PB : A.zero, st + C::A_STAGE + (C::NW * t + wave) * 1024);
+        st_cur = lds_base + st_next * C::STAGE;
+    };
+    auto issue_copy = [&](auto d_c) {
+        constexpr int d = decltype(d_c)::value;
+        if constexpr (d < C::B_PER)
+            dma16(bsrc[d] ? bsrc[d] + cc_next * C::PB : A.zero, st_cur + C::A_STAGE + (C::NW * d + wave) * 1024);
+        else
+            dma16(a_next + a_src[d - C::B_PER], st_cur + (C::NW * (d - C::B_PER) + wave) * 1024);
+    };
+    auto issue_end = [&]() {
         a_next += C::A_STAGE;
         if (++st_next == C::NSTAGE)
             st_next = 0;
@@ -267,13 +280,19 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
             ++tap_next;
         }
     };
+    auto issue = [&]() {
+        issue_begin();
+        static_for<C::NOPS>([&](auto d_c) { issue_copy(d_c); });
+        issue_end();
+    };
     // wait until at most `steps` K steps of copies are outstanding
     auto wait_steps = [&](int steps) {
         switch (steps) {
         case 0: wait_vmcnt<0>(); break;
         case 1: wait_vmcnt<C::NOPS>(); break;
         case 2: wait_vmcnt<2 * C::NOPS>(); break;
-        default: wait_vmcnt<3 * C::NOPS>(); break;
+        case 3: wait_vmcnt<3 * C::NOPS>(); break;
+        default: wait_vmcnt<4 * C::NOPS>(); break;
         }
     };
 
@@ -310,10 +329,34 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
                        (int)((w >> 4) & 0x03030303u), (int)((w >> 6) & 0x03030303u)};
     };
 
-    // prologue: copies for steps 0 .. NSTAGE-2, fragments of step 0
-    const int pre = KS < C::NSTAGE - 1 ? KS : C::NSTAGE - 1;
+    // prologue: copies for steps 0 .. NSTAGE-1 (every stage), fragments of step 0
+    const int pre = KS < C::NSTAGE ? KS : C::NSTAGE;
     for (int k = 0; k < pre; ++k)
         issue();
+
+    // this channel tile's epilogue table does not depend on the accumulators:
+    // it is fetched now, so that its latency hides behind the K loop, and goes
+    // to LDS after the last step
+    constexpr int PRM_PER = EPI_FIELDS * C::BCO / NT;
+    static_assert(EPI_FIELDS * C::BCO % NT == 0, "epilogue table splits evenly over the threads");
+    int prm_r[PRM_PER];
+#pragma unroll
+    for (int t = 0; t < PRM_PER; ++t) {
+        const int i = tid + t * NT;
+        const int which = i / C::BCO, c = i - which * C::BCO;
+        prm_r[t] = S.epi[which * A.cout_pad + co_tile * C::BCO + c];
+    }
+    constexpr int CPL = C::CPL;
+    const int g = lane >> 4;
+    const int co_loc = wc * C::TM + CPL * g;      // first of this lane's CPL channels (in the tile)
+    const int co_glob = co_tile * C::BCO + co_loc;
+    const long long px0 = (long long)px_tile * C::BPX + wp * C::TN + (lane & 15);
+    const bool co_ok = co_glob < A.cout;          // CPL channels are all valid or all padding
+    bool okj[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+        okj[j] = co_ok && px0 + j * 16 < S.P;
+
     wait_steps(pre - 1);
     __syncthreads();
 #pragma unroll
@@ -325,7 +368,9 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
 
     // step ks: MFMAs on register set ks & 1 while the fragments of step ks + 1
     // are read into the other set (after the last step these reads fetch
-    // unused data); copies run NSTAGE - 1 steps ahead.
+    // unused data). The stage of step ks was read into registers during step
+    // ks - 1; once every wave has those reads back (lgkmcnt(0) + barrier) it is
+    // refilled with step ks + NSTAGE, so copies run NSTAGE steps ahead.
     int st_read = 1 % C::NSTAGE;  // stage of step ks + 1
     for (int k0 = 0; k0 < KS; k0 += 2) {
         static_for<2>([&](auto pc) {
@@ -334,13 +379,14 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
             if (ks >= KS)
                 return;
             if (ks + 1 < KS) {
-                // step ks + 1 landed: copies up to step min(ks + NSTAGE - 2, KS - 1) were issued
-                const int last = ks + C::NSTAGE - 2 < KS - 1 ? ks + C::NSTAGE - 2 : KS - 1;
+                // step ks + 1 landed: copies up to step min(ks + NSTAGE - 1, KS - 1) were issued
+                const int last = ks + C::NSTAGE - 1 < KS - 1 ? ks + C::NSTAGE - 1 : KS - 1;
                 wait_steps(last - (ks + 1));
-                // stage ks + 1 visible to every wave; every wave is past step ks - 1, whose
-                // reads (of stage ks) ended the use of the stage the next copy refills
+                // this wave's fragment reads of stage ks are back
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                // stage ks + 1 visible to every wave, and no wave reads stage ks any more
                 asm volatile("s_barrier" ::: "memory");
-                if (ks + C::NSTAGE - 1 < KS)
+                if (ks + C::NSTAGE < KS)
                     issue();
             }
 #pragma unroll
@@ -356,6 +402,21 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
 #pragma unroll
             for (int i = NJ; i < MI; ++i)
                 read_a(st_read, fa[P ^ 1], i);
+            // schedule: per column tile, its widening, then its MI MFMAs with
+            // the next step's fragment reads spread between them, so that the
+            // LDS latency hides under the matrix cores
+            static_for<NJ>([&](auto jc) {
+                constexpr int j = decltype(jc)::value;
+                constexpr int RD = MI + NJ;                       // fragment reads per step
+                constexpr int lo = RD * j / NJ, hi = RD * (j + 1) / NJ;
+                __builtin_amdgcn_sched_group_barrier(0x002, BI == 4 ? 6 : 7, 0);  // VALU
+                static_for<MI>([&](auto ic) {
+                    constexpr int i = decltype(ic)::value;
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // MFMA
+                    if constexpr (i < hi - lo)
+                        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);        // DS read
+                });
+            });
             if (++st_read == C::NSTAGE)
                 st_read = 0;
         });
@@ -365,28 +426,43 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
     // The ring is idle after the last step; it now holds this channel tile's
     // epilogue table, the side-0 skip table and the int32 output staging.
     constexpr int QMAX = (1 << BI) - 1;
-    constexpr int CPL = C::CPL;
     int32_t *prm = (int32_t *)lds_stages;
     int32_t *lut = prm + EPI_FIELDS * C::BCO;            // [BCO][2^BI]: RSM(k, c, d)
     const bool use_lut = SKK == 1 && S.side0;            // uniform over the workgroup
+    // skip codes: issued before the table goes to LDS, so that the two overlap
+    uint32_t skw[NJ][C::OW];
+    static_for<NJ>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+#pragma unroll
+        for (int u = 0; u < C::OW; ++u)
+            skw[j][u] = 0;
+        if constexpr (OUTK == 0 && SKK == 1) {
+            if (okj[j]) {
+                const long long px = px0 + j * 16;
+                long long spix = px;
+                if (A.up2) {
+                    const int n_ = (int)(px / hw);
+                    const int rem = (int)(px - (long long)n_ * hw);
+                    const int oh = rem / S.wo, ow = rem - oh * S.wo;
+                    spix = ((long long)n_ * S.hs + (oh >> 1)) * S.ws + (ow >> 1);
+                }
+                load_words<C::OW>((const uint8_t *)S.skip + spix * (A.cout * BI / 8) + co_glob * BI / 8, skw[j]);
+            }
+        }
+    });
     __syncthreads();  // every wave is done with the ring
-    for (int i = tid; i < EPI_FIELDS * C::BCO; i += NT) {
-        const int which = i / C::BCO, c = i - which * C::BCO;
-        prm[which * C::BCO + c] = S.epi[which * A.cout_pad + co_tile * C::BCO + c];
-    }
+#pragma unroll
+    for (int t = 0; t < PRM_PER; ++t)
+        prm[tid + t * NT] = prm_r[t];
+    __syncthreads();
     if (use_lut) {
         // every skip operand is a b-bit code scaled by c / 2^d (side 0): tabulate
         for (int i = tid; i < C::BCO * (QMAX + 1); i += NT) {
-            const int ch = co_tile * C::BCO + (i >> BI);
-            lut[i] = rsm32(i & QMAX, S.epi[EPI_SKIP_C * A.cout_pad + ch], S.epi[EPI_SKIP_D * A.cout_pad + ch]);
+            const int cl = i >> BI;
+            lut[i] = rsm32(i & QMAX, prm[EPI_SKIP_C * C::BCO + cl], prm[EPI_SKIP_D * C::BCO + cl]);
         }
+        __syncthreads();
     }
-    __syncthreads();
-
-    const int g = lane >> 4;
-    const int co_loc = wc * C::TM + CPL * g;      // first of this lane's CPL channels (in the tile)
-    const int co_glob = co_tile * C::BCO + co_loc;
-    const long long px0 = (long long)px_tile * C::BPX + wp * C::TN + (lane & 15);
 
     // int32 tiles (outputs, int32 skips) move between HBM and registers through
     // a per-wave LDS staging area, JP column tiles (16 JP pixel rows) at a time,
@@ -432,34 +508,13 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
         return;
     }
 
-    const bool co_ok = co_glob < A.cout;  // CPL channels are all valid or all padding
-
-    // per pixel column: validity, skip codes, packed output codes
-    bool okj[NJ];
-    uint32_t skw[NJ][C::OW];
+    // packed output codes per pixel column
     uint32_t outw[NJ][C::OW];
-    static_for<NJ>([&](auto jc) {
-        constexpr int j = decltype(jc)::value;
-        const long long px = px0 + j * 16;
-        okj[j] = co_ok && px < S.P;
 #pragma unroll
-        for (int u = 0; u < C::OW; ++u) {
-            skw[j][u] = 0;
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int u = 0; u < C::OW; ++u)
             outw[j][u] = 0;
-        }
-        if constexpr (SKK == 1) {
-            if (okj[j]) {
-                long long spix = px;
-                if (A.up2) {
-                    const int n_ = (int)(px / hw);
-                    const int rem = (int)(px - (long long)n_ * hw);
-                    const int oh = rem / S.wo, ow = rem - oh * S.wo;
-                    spix = ((long long)n_ * S.hs + (oh >> 1)) * S.ws + (ow >> 1);
-                }
-                load_words<C::OW>((const uint8_t *)S.skip + spix * (A.cout * BI / 8) + co_glob * BI / 8, skw[j]);
-            }
-        }
-    });
 
     // columns [J0, J0 + JN): channel group outer (parameters read once), column inner
     auto body = [&](auto lut_c, auto j0_c, auto jn_c) {
