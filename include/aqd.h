@@ -58,6 +58,7 @@
 #ifndef AQD_H
 #define AQD_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -162,6 +163,29 @@ typedef struct {
  * inputs or outputs. */
 #define AQD_MAX_SEGS 16
 aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t stream);
+
+/* Split reduction over K (Sec. 3.2.1, Eq. 4: acc is an integer sum over the
+ * taps and input channels, so summing it in parts, in any order, gives the
+ * same int32 value).
+ *
+ * qconv_group_workspace: *bytes receives the device workspace size with
+ * which qconv_run_group_ws may split this group's reduction over several
+ * workgroups; 0 when the group is not worth splitting (its launch already
+ * fills the GPU). The size depends on the handles' shapes and on n, h, w of
+ * every segment, not on the tensor pointers. Errors as qconv_run_group.
+ *
+ * qconv_run_group_ws: as qconv_run_group. With workspace non-NULL and
+ * ws_bytes at least the queried size (and the size non-zero), the K range of
+ * every output tile is cut into parts whose int32 partial sums go to the
+ * workspace, and a second kernel adds the parts and applies the epilogue;
+ * the outputs are identical to qconv_run_group's. Otherwise the call is
+ * exactly qconv_run_group. The workspace is scratch (device memory owned by
+ * the caller, 256-byte aligned, contents irrelevant on entry and undefined
+ * on return); calls that share a workspace must not overlap in time (use one
+ * stream, or one workspace per stream). */
+aqd_status_t qconv_group_workspace(int count, const qconv_seg_t *segs, size_t *bytes);
+aqd_status_t qconv_run_group_ws(int count, const qconv_seg_t *segs, void *workspace,
+                                size_t ws_bytes, aqd_stream_t stream);
 
 void qconv_destroy(qconv_t conv);
 

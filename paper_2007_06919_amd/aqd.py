@@ -72,6 +72,8 @@ def lib():
             "qconv_out_shape": ([vp, i, i, POINTER(c_int), POINTER(c_int)], st),
             "qconv_run": ([vp, i, i, i, i, vp, vp, i, i, vp, vp], st),
             "qconv_run_group": ([i, POINTER(QconvSeg), vp], st),
+            "qconv_group_workspace": ([i, POINTER(QconvSeg), POINTER(ctypes.c_size_t)], st),
+            "qconv_run_group_ws": ([i, POINTER(QconvSeg), vp, ctypes.c_size_t, vp], st),
             "qconv_destroy": ([vp], None),
             "qadd_run": ([POINTER(QaddDesc), vp, vp, vp, POINTER(QaddParams), vp], st),
             "aqd_channel_sums": ([vp, c_int64, i, vp, vp], st),
@@ -94,7 +96,8 @@ def lib():
 
 
 def exported_symbols():
-    return ["qconv_create", "qconv_out_shape", "qconv_run", "qconv_run_group", "qconv_destroy",
+    return ["qconv_create", "qconv_out_shape", "qconv_run", "qconv_run_group",
+            "qconv_group_workspace", "qconv_run_group_ws", "qconv_destroy",
             "qadd_run", "aqd_channel_sums", "aqd_last_error", "aqd_pack_codes",
             "aqd_unpack_codes", "aqd_approx_ratio", "aqd_normalize_multiplier",
             "aqd_bn_stats_from_sums", "aqd_fold_bn", "aqd_skip_params", "aqd_requant_params"]
@@ -164,12 +167,29 @@ def qconv_run(conv, level, n, h, w, x, skip, hs, ws, y, stream=None):
                            _stream(stream)))
 
 
-def qconv_run_group(segs, stream=None):
-    """segs: list of tuples (conv, level, n, h, w, x, skip, hs, ws, y)."""
+def _seg_array(segs):
     arr = (QconvSeg * len(segs))()
     for i, (conv, level, n, h, w, x, skip, hs, ws, y) in enumerate(segs):
         arr[i] = QconvSeg(conv, level, n, h, w, _addr(x), _addr(skip), hs, ws, _addr(y))
-    _check(lib().qconv_run_group(len(segs), arr, _stream(stream)))
+    return arr
+
+
+def qconv_run_group(segs, stream=None):
+    """segs: list of tuples (conv, level, n, h, w, x, skip, hs, ws, y)."""
+    _check(lib().qconv_run_group(len(segs), _seg_array(segs), _stream(stream)))
+
+
+def qconv_group_workspace(segs) -> int:
+    """Workspace bytes with which qconv_run_group_ws splits the K reduction
+    of this group (0: never split)."""
+    b = ctypes.c_size_t(0)
+    _check(lib().qconv_group_workspace(len(segs), _seg_array(segs), ctypes.byref(b)))
+    return b.value
+
+
+def qconv_run_group_ws(segs, workspace, ws_bytes, stream=None):
+    _check(lib().qconv_run_group_ws(len(segs), _seg_array(segs), _addr(workspace), ws_bytes,
+                                    _stream(stream)))
 
 
 def qconv_destroy(conv):

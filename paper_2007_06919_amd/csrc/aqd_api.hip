@@ -415,11 +415,17 @@ aqd_status_t launch_direct(const qconv_seg_t &s, const SegCheck &c, hipStream_t 
 
 extern "C" {
 
-aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t stream_)
+}  // extern "C"
+
+namespace {
+
+// Checks a group and fills the MFMA launch description (everything but the
+// split); *tiles receives the number of output tiles, *direct whether the
+// group runs on the direct kernel.
+aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, MfmaArgs *out,
+                           bool *direct)
 {
     REQUIRE(segs && count >= 1 && count <= AQD_MAX_SEGS, "count must be in 1..AQD_MAX_SEGS");
-    hipStream_t stream = (hipStream_t)stream_;
-    SegCheck chk[AQD_MAX_SEGS];
     for (int i = 0; i < count; ++i) {
         aqd_status_t st = check_seg(segs[i], &chk[i]);
         if (st != AQD_OK)
@@ -437,16 +443,11 @@ aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t st
                     "a segment output overlaps another segment's tensors");
         }
     const qconv_s &h0 = *segs[0].conv;
-    if (!h0.mfma) {
-        for (int i = 0; i < count; ++i)
-            if (segs[i].n > 0) {
-                aqd_status_t st = launch_direct(segs[i], chk[i], stream);
-                if (st != AQD_OK)
-                    return st;
-            }
+    *direct = !h0.mfma;
+    if (!h0.mfma)
         return AQD_OK;
-    }
-    MfmaArgs a{};
+    MfmaArgs &a = *out;
+    a = MfmaArgs{};
     int tiles = 0;
     for (int i = 0; i < count; ++i) {
         const qconv_seg_t &s = segs[i];
@@ -470,13 +471,14 @@ aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t st
         m.fast = s.conv->fast[s.level];
         m.side0 = s.conv->side0[s.level];
         const long long px_tiles = (m.P + h0.blk_px - 1) / h0.blk_px;
-        REQUIRE(tiles + px_tiles * h0.co_tiles < (1LL << 30), "too many tiles for one launch");
+        REQUIRE(tiles + px_tiles * h0.co_tiles < (1LL << 26), "too many tiles for one launch");
         tiles += (int)(px_tiles * h0.co_tiles);
     }
-    if (a.nseg == 0)
-        return AQD_OK;
     a.total_tiles = tiles;
     a.tiles_per_xcd = (tiles + 7) / 8;
+    a.ksplit = 1;
+    a.kchunk = h0.ksteps;
+    a.part = 0;
     a.cin = h0.d.cin;
     a.cout = h0.d.cout;
     a.cout_pad = h0.cout_pad;
@@ -491,9 +493,161 @@ aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t st
     a.bits_out = h0.d.out_mode == AQD_OUT_INT32 ? 32 : h0.d.bits_out;
     a.skip_bits = h0.d.skip_bits;
     a.zero = h0.zero;
+    return AQD_OK;
+}
+
+// Split of the K range: the number of parts minimising a simple model of the
+// MI355X (256 CUs, two workgroups per CU), fitted to measured launches: a
+// workgroup alone on its CU takes ~0.65 us per K step, two sharing a CU
+// ~0.84 us (0.42 each), plus ~3 us of prologue and epilogue per pair of
+// workgroups; the parts cost one write and one read of nparts x P x cout
+// int32 (~5 TB/s) and the combining launch (~5 us). A split is taken only
+// when the model gains 20%.
+void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
+{
+    long long P = 0;
+    for (int i = 0; i < a.nseg; ++i)
+        P += a.seg[i].P;
+    auto cost = [&](int parts, int chunk) {
+        const double units = (double)a.total_tiles * parts;
+        const double per_cu = std::ceil(units / 256.0);
+        double t = chunk * (per_cu <= 1 ? 0.65 : 0.42 * per_cu) + 3.0 * std::ceil(per_cu / 2.0);
+        if (parts > 1)
+            t += (double)parts * P * a.cout * 8.0 / 5e6 + 5.0;
+        return t;
+    };
+    *nparts = 1;
+    *kchunk = a.ksteps;
+    double best = cost(1, a.ksteps);
+    static const int cand[] = {2, 3, 4, 6, 8, 12, 16};
+    for (int c : cand) {
+        const int chunk = (a.ksteps + c - 1) / c;
+        if (chunk < 2)
+            break;
+        const int parts = (a.ksteps + chunk - 1) / chunk;  // every part non-empty
+        const double t = cost(parts, chunk);
+        if (t < 0.8 * best) {
+            best = t;
+            *nparts = parts;
+            *kchunk = chunk;
+        }
+    }
+}
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+size_t split_bytes(const MfmaArgs &a, int nparts)
+{
+    size_t b = 0;
+    for (int i = 0; i < a.nseg; ++i)
+        b += align256((size_t)nparts * a.seg[i].P * a.cout * 4);
+    return b;
+}
+
+}  // namespace
+
+extern "C" {
+
+aqd_status_t qconv_group_workspace(int count, const qconv_seg_t *segs, size_t *bytes)
+{
+    REQUIRE(bytes, "null bytes");
+    *bytes = 0;
+    SegCheck chk[AQD_MAX_SEGS];
+    MfmaArgs a;
+    bool direct = false;
+    aqd_status_t st = prepare_group(count, segs, chk, &a, &direct);
+    if (st != AQD_OK || direct || a.nseg == 0)
+        return st;
+    int nparts = 1, kchunk = 0;
+    plan_split(a, &nparts, &kchunk);
+    if (nparts > 1)
+        *bytes = split_bytes(a, nparts);
+    return AQD_OK;
+}
+
+aqd_status_t qconv_run_group_ws(int count, const qconv_seg_t *segs, void *workspace, size_t ws_bytes,
+                                aqd_stream_t stream_)
+{
+    hipStream_t stream = (hipStream_t)stream_;
+    SegCheck chk[AQD_MAX_SEGS];
+    MfmaArgs a;
+    bool direct = false;
+    aqd_status_t st = prepare_group(count, segs, chk, &a, &direct);
+    if (st != AQD_OK)
+        return st;
+    if (direct) {
+        for (int i = 0; i < count; ++i)
+            if (segs[i].n > 0) {
+                st = launch_direct(segs[i], chk[i], stream);
+                if (st != AQD_OK)
+                    return st;
+            }
+        return AQD_OK;
+    }
+    if (a.nseg == 0)
+        return AQD_OK;
+    const qconv_s &h0 = *segs[0].conv;
+    int nparts = 1, kchunk = a.ksteps;
+    if (workspace) {
+        REQUIRE(((uintptr_t)workspace & 255) == 0, "workspace must be 256-byte aligned");
+        plan_split(a, &nparts, &kchunk);
+        if (nparts > 1 && ws_bytes < split_bytes(a, nparts))
+            nparts = 1;
+    }
+    if (nparts == 1) {
+        if (launch_qconv_mfma(h0.d.bits_in, a, stream) != hipSuccess)
+            return fail(AQD_ERR_DEVICE, "MFMA conv launch failed");
+        return AQD_OK;
+    }
+    // part sums of every segment into its workspace slice, then the combining epilogue
+    SplitArgs e{};
+    e.nseg = a.nseg;
+    e.nparts = nparts;
+    e.cout = a.cout;
+    e.cout_pad = a.cout_pad;
+    e.bits_out = a.bits_out;
+    e.skip_bits = a.skip_bits;
+    e.up2 = a.up2;
+    const int cpt = a.bits_out == 32 ? 4 : 32 / a.bits_out;
+    uint8_t *ws = (uint8_t *)workspace;
+    long long items = 0;
+    for (int i = 0; i < a.nseg; ++i) {
+        MfmaSeg &m = a.seg[i];
+        SplitSeg &q = e.seg[i];
+        q.part = (const int32_t *)ws;
+        q.skip = m.skip;
+        q.y = m.y;
+        q.epi = m.epi;
+        q.P = m.P;
+        q.ho = m.ho;
+        q.wo = m.wo;
+        q.hs = m.hs;
+        q.ws = m.ws;
+        q.item_begin = items;
+        items += m.P * (a.cout / cpt);
+        m.y = ws;
+        m.skip = nullptr;
+        ws += align256((size_t)nparts * m.P * a.cout * 4);
+    }
+    e.total_items = items;
+    a.part = 1;
+    a.ksplit = nparts;
+    a.kchunk = kchunk;
+    a.total_tiles *= nparts;
+    a.tiles_per_xcd = (a.total_tiles + 7) / 8;
+    a.bits_out = 32;
+    a.skip_bits = 0;
+    a.up2 = 0;
     if (launch_qconv_mfma(h0.d.bits_in, a, stream) != hipSuccess)
         return fail(AQD_ERR_DEVICE, "MFMA conv launch failed");
+    if (launch_splitk_epilogue(e, stream) != hipSuccess)
+        return fail(AQD_ERR_DEVICE, "split-K epilogue launch failed");
     return AQD_OK;
+}
+
+aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t stream)
+{
+    return qconv_run_group_ws(count, segs, nullptr, 0, stream);
 }
 
 aqd_status_t qconv_run(qconv_t conv, int level, int n, int h, int w, const void *x, const void *skip,

@@ -41,8 +41,11 @@ struct MfmaSeg {
 struct MfmaArgs {
     MfmaSeg seg[AQD_MAX_SEGS];
     int nseg;
-    int total_tiles;
+    int total_tiles;     // work units: output tiles x ksplit
     int tiles_per_xcd;   // grid = 8 * tiles_per_xcd workgroups
+    int ksplit;          // parts of the K range per output tile (1: no split)
+    int kchunk;          // K steps per part (the last part may have fewer)
+    int part;            // 1: write raw int32 partial sums (no bias) to y + part * P * cout
     int tile_cfg;
     int cin, cout, cout_pad;
     int kh, kw, stride, pad;
@@ -55,6 +58,25 @@ struct MfmaArgs {
 
 // bits_in in {2, 4}
 hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream);
+
+// ---- split-K combine + epilogue (qconv_splitk.hip) ---------------------------
+struct SplitSeg {
+    const int32_t *part;  // [nparts][P][cout] int32 partial sums
+    const void *skip;     // as MfmaSeg
+    void *y;
+    const int32_t *epi;   // [EPI_FIELDS][cout_pad]
+    long long P;
+    int ho, wo, hs, ws;
+    long long item_begin; // first work item (pixel x channel group) of this segment
+};
+struct SplitArgs {
+    SplitSeg seg[AQD_MAX_SEGS];
+    int nseg;
+    long long total_items;
+    int nparts, cout, cout_pad;
+    int bits_out, skip_bits, up2;  // bits_out 32: int32 output
+};
+hipError_t launch_splitk_epilogue(const SplitArgs &a, hipStream_t stream);
 
 // ---- direct kernel (qconv_direct.hip): any shape the ABI allows -------------
 struct DirectArgs {

@@ -189,14 +189,18 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
     const int logical = (bid & 7) * A.tiles_per_xcd + (bid >> 3);
     if (logical >= A.total_tiles)
         return;
+    // work unit -> output tile and part of its K range (the parts of a tile are
+    // consecutive units, hence on one XCD)
+    const int tile = logical / A.ksplit;
+    const int kpart = logical - tile * A.ksplit;
 
     int s = 0;
 #pragma unroll
     for (int i = 1; i < AQD_MAX_SEGS; ++i)
-        if (i < A.nseg && logical >= A.seg[i].tile_begin)
+        if (i < A.nseg && tile >= A.seg[i].tile_begin)
             s = i;
     const MfmaSeg &S = A.seg[s];
-    const int t_in_seg = logical - S.tile_begin;
+    const int t_in_seg = tile - S.tile_begin;
     const int co_tile = t_in_seg % A.co_tiles;
     const int px_tile = t_in_seg / A.co_tiles;
 
@@ -208,7 +212,8 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
 
     const int row_bytes = A.cin * BI / 8;
     const int kpt = A.cin / KC;
-    const int KS = A.ksteps;
+    const int kb = kpart * A.kchunk;                   // first K step of this part
+    const int KS = A.ksteps - kb < A.kchunk ? A.ksteps - kb : A.kchunk;  // >= 1 (host)
     const int hw = S.ho * S.wo;
 
     // Copies: chunk q of a stage (1 KiB) belongs to wave q % NW; which source
@@ -242,26 +247,30 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
 
     // Copy state: steps are issued in order, so the per-pixel source of the
     // current tap is computed once per tap (bsrc; null for padding taps).
-    const int8_t *a_next = S.wt + (long long)co_tile * KS * C::A_STAGE;
+    const int8_t *a_next = S.wt + ((long long)co_tile * A.ksteps + kb) * C::A_STAGE;
     const uint32_t lds_base = lds_addr(lds_stages);
-    int tap_next = 0, cc_next = 0, st_next = 0;
+    int tap_next = kb / kpt, cc_next = kb - (kb / kpt) * kpt, st_next = 0;
     const uint8_t *bsrc[C::B_PER];
-    // A step's copies are issued in three parts so that the main loop can
-    // spread them between its MFMAs: issue_begin (the tap's sources, at a tap
-    // change), issue_copy<d> for d = 0 .. NOPS-1 (activation copies first),
-    // issue_end (advance to the next step).
+    // per-pixel sources of tap tap_next (null: the tap falls in the padding)
+    auto tap_sources = [&]() {
+        const int r = tap_next / A.kw;
+        const int q = tap_next - r * A.kw;
+#pragma unroll
+        for (int t = 0; t < C::B_PER; ++t) {
+            const int ih = ih0[t] + r, iw = iw0[t] + q;
+            const bool ok = pv[t] && (unsigned)ih < (unsigned)S.h && (unsigned)iw < (unsigned)S.w;
+            bsrc[t] = ok ? xb[t] + ((long long)ih * S.w + iw) * row_bytes : nullptr;
+        }
+    };
+    // a part of a split K range may start inside a tap: its sources are set here
+    tap_sources();
+    // A step's copies are issued in three parts: issue_begin (the tap's
+    // sources, at a tap change), issue_copy<d> for d = 0 .. NOPS-1
+    // (activation copies first), issue_end (advance to the next step).
     uint32_t st_cur = 0;
     auto issue_begin = [&]() {
-        if (cc_next == 0) {
-            const int r = tap_next / A.kw;
-            const int q = tap_next - r * A.kw;
-#pragma unroll
-            for (int t = 0; t < C::B_PER; ++t) {
-                const int ih = ih0[t] + r, iw = iw0[t] + q;
-                const bool ok = pv[t] && (unsigned)ih < (unsigned)S.h && (unsigned)iw < (unsigned)S.w;
-                bsrc[t] = ok ? xb[t] + ((long long)ih * S.w + iw) * row_bytes : nullptr;
-            }
-        }
+        if (cc_next == 0)
+            tap_sources();
         st_cur = lds_base + st_next * C::STAGE;
     };
     auto issue_copy = [&](auto d_c) {
@@ -483,7 +492,9 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
                 constexpr int j = pass * JP + jj;
 #pragma unroll
                 for (int i = 0; i < MI; ++i) {
-                    const int4 b4 = *(const int4 *)(prm + co_loc + 4 * i);
+                    int4 b4 = *(const int4 *)(prm + co_loc + 4 * i);
+                    if (A.part)
+                        b4 = make_int4(0, 0, 0, 0);   // partial sums: the bias is added once, later
                     int4 o;
                     o.x = acc[i][j][0] + b4.x;
                     o.y = acc[i][j][1] + b4.y;
@@ -501,7 +512,7 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
                 const int ch = co_tile * C::BCO + wc * C::TM + cw;
                 const int4 v = *(const int4 *)(stg + row * ROWB + cw * 4);
                 if (px < S.P && ch < A.cout)
-                    *(int4 *)((int32_t *)S.y + px * A.cout + ch) = v;
+                    *(int4 *)((int32_t *)S.y + (kpart * S.P + px) * A.cout + ch) = v;
             }
             __syncthreads();  // staging is rewritten by the next pass
         });

@@ -9,6 +9,9 @@ A network description (``workloads.NetSpec``) becomes a list of grouped
   depth and configuration (same shapes, bitwidths and modes) share a launch:
   the pyramid levels of a head layer (one epilogue table per level,
   multi-level BN, Sec. 3.2.2) and the class and box towers at equal depth;
+* one workspace, sized for the largest group's split-K need
+  (``qconv_group_workspace``), lets small launches split their K reduction
+  over more workgroups (``qconv_run_group_ws``);
 * in calibrated mode the integer epilogue of every layer is derived here,
   from the exact accumulator sums of the calibration images computed on the
   GPU (int32 conv output + ``aqd_channel_sums``) and the library's host
@@ -35,7 +38,8 @@ def _conv_key(net: NetSpec, conv) -> tuple:
 
 
 class Net:
-    def __init__(self, net: NetSpec, params: NetParams, device="cuda:0", stream=None):
+    def __init__(self, net: NetSpec, params: NetParams, device="cuda:0", stream=None,
+                 split_k: bool = True):
         import torch
 
         self.torch = torch
@@ -58,6 +62,12 @@ class Net:
         self._alpha_t: Dict[str, np.ndarray] = {}
         self.schedule = self._make_schedule()
         self._build()
+        self.ws_bytes = 0
+        if split_k:
+            self.ws_bytes = max(aqd.qconv_group_workspace([self._seg_args(c, si) for c, si in g])
+                                for g in self.schedule)
+        self.ws = (torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+                   if self.ws_bytes else None)
 
     # ---------------------------------------------------------------- setup
     def _make_schedule(self) -> List[List[Tuple[object, int]]]:
@@ -179,7 +189,11 @@ class Net:
         for gi, group in enumerate(self.schedule):
             if launch_hook:
                 launch_hook(gi, "before")
-            aqd.qconv_run_group([self._seg_args(conv, si) for conv, si in group], s)
+            segs = [self._seg_args(conv, si) for conv, si in group]
+            if self.ws is not None:
+                aqd.qconv_run_group_ws(segs, self.ws, self.ws_bytes, s)
+            else:
+                aqd.qconv_run_group(segs, s)
             if launch_hook:
                 launch_hook(gi, "after")
 

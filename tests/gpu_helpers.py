@@ -6,8 +6,10 @@ from oracle import ref
 from paper_2007_06919_amd import aqd, workloads
 
 
-def gpu_conv(case, torch, stream=None):
-    """Run a ConvCase through qconv_create/qconv_run; returns (bytes, handle-kernel)."""
+def gpu_conv(case, torch, stream=None, split=False):
+    """Run a ConvCase through qconv_create/qconv_run (split: through
+    qconv_run_group_ws with the queried workspace, filled with junk first);
+    returns the output bytes of every level."""
     dev = torch.device("cuda:0")
     skip_bits = case.skip_bits
     out_mode = aqd.OUT_INT32 if case.bits_out == 32 else aqd.OUT_CODES
@@ -33,7 +35,14 @@ def gpu_conv(case, torch, stream=None):
                            dtype=torch.uint8, device=dev)
         outs = []
         for level in range(len(case.levels)):
-            aqd.qconv_run(h, level, case.n, case.h, case.w, x, skip, hs, ws, y, stream)
+            if split:
+                segs = [(h, level, case.n, case.h, case.w, x, skip, hs, ws, y)]
+                nbytes = aqd.qconv_group_workspace(segs)
+                assert nbytes > 0, "this case is expected to split"
+                wsbuf = torch.full((nbytes,), 0x77, dtype=torch.uint8, device=dev)
+                aqd.qconv_run_group_ws(segs, wsbuf, nbytes, stream)
+            else:
+                aqd.qconv_run(h, level, case.n, case.h, case.w, x, skip, hs, ws, y, stream)
             torch.cuda.synchronize()
             outs.append(y.cpu().numpy().copy())
         return outs

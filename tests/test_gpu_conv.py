@@ -69,6 +69,47 @@ def test_conv_mfma_parity(torch, case):
                bits_in=bi, bits_w=bw, wenc=wenc, bits_out=bo, skip_bits=sb, skip_up2=up2)
 
 
+SPLIT_CASES = [
+    # few output tiles and a long K range: the K reduction is split over workgroups
+    (1, 13, 21, 512, 256, 3, 2, 4, 4, 1, 4, 0, False),      # P6-like: 3x3 stride 2, 72 K steps
+    (2, 9, 11, 1024, 256, 1, 1, 4, 4, 1, 4, 4, True),       # lateral 1x1 + upsampled code skip
+    (1, 7, 9, 1024, 256, 1, 1, 4, 4, 0, 4, 32, False),      # int32 skip
+    (1, 10, 12, 256, 720, 3, 1, 4, 4, 1, 32, 0, False),     # int32 out, 720 channels
+    (1, 9, 9, 256, 128, 3, 1, 2, 2, 0, 2, 2, False),        # 2-bit, code skip
+    (1, 6, 7, 448, 64, 3, 1, 4, 4, 0, 4, 0, False),         # 63 K steps: a shorter last part
+]
+
+
+@pytest.mark.parametrize("case", SPLIT_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_conv_split_k_parity(torch, case):
+    """qconv_run_group_ws with a workspace: the split reduction and the
+    combining epilogue give the oracle's outputs bit for bit, and the same
+    bytes as the unsplit launch."""
+    n, h, w, cin, cout, k, s, bi, bw, wenc, bo, sb, up2 = case
+    c = workloads.random_conv_case(seed=hash(case) % 1000 + 3, n=n, h=h, w=w, cin=cin, cout=cout,
+                                   k=k, stride=s, bits_in=bi, bits_w=bw, wenc=wenc, bits_out=bo,
+                                   skip_bits=sb, skip_up2=up2)
+    got = gpu_conv(c, torch, split=True)
+    plain = gpu_conv(c, torch)
+    for level, g in enumerate(got):
+        assert_same(g, oracle_conv(c, level), f"split {case} level {level}")
+        assert_same(g, plain[level], f"split vs unsplit {case}")
+
+
+def test_split_k_not_used_for_full_launches(torch):
+    """A launch that already fills the GPU asks for no workspace."""
+    case = workloads.random_conv_case(seed=4, n=4, h=64, w=96, cin=256, cout=256, k=3,
+                                      bits_in=4, bits_w=4, bits_out=4)
+    h = aqd.qconv_create(256, 256, 3, 1, 1, 4, 4, aqd.pack_codes(case.w_fields, 4), case.levels)
+    try:
+        dev = torch.device("cuda:0")
+        x = torch.zeros((4, 64, 96, 128), dtype=torch.uint8, device=dev)
+        y = torch.zeros((4, 64, 96, 128), dtype=torch.uint8, device=dev)
+        assert aqd.qconv_group_workspace([(h, 0, 4, 64, 96, x, None, 0, 0, y)]) == 0
+    finally:
+        aqd.qconv_destroy(h)
+
+
 DIRECT_CASES = [
     (1, 9, 10, 32, 16, 3, 1, 4, 4, 0, 4, 0, False),         # cin not a multiple of 64
     (2, 8, 7, 16, 12, 3, 2, 8, 4, 0, 8, 0, False),          # 8-bit activations
