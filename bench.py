@@ -88,7 +88,7 @@ def main():
     with torch.cuda.stream(stream):
         gpu = runner.Net(net, params, device="cuda:0", stream=stream)
     log(f"[bench] handles created and calibrated in {time.time() - t0:.1f} s; "
-        f"{len(gpu.schedule)} launches per step")
+        f"{gpu.launches_per_forward()} launches per step, {len(gpu.fused)} projection shortcuts fused")
 
     n_img = net.tensors[net.inputs[0]].n
     total_ops = 2 * net.total_macs()
@@ -142,7 +142,7 @@ def main():
         "dtype": "i8", "data": "synthetic",
         "config": {"workload": workloads.CONFIG_NAMES[4], "batch": n_img, "image": [800, 1333],
                    "bits": 4, "conv_segments": sum(len(c.segs) for c in net.convs),
-                   "launches_per_step": len(gpu.schedule), "int_ops_per_step": total_ops},
+                   "launches_per_step": gpu.launches_per_forward(), "int_ops_per_step": total_ops},
         "ms_per_image": round(ms_step / n_img, 4),
         "roofline": {"bound": "mfma", "kernel": "qconv_mfma_kernel<4,4,0> (head tower 3x3 256->256, "
                                                 "10 segments)",

@@ -187,6 +187,26 @@ aqd_status_t qconv_group_workspace(int count, const qconv_seg_t *segs, size_t *b
 aqd_status_t qconv_run_group_ws(int count, const qconv_seg_t *segs, void *workspace,
                                 size_t ws_bytes, aqd_stream_t stream);
 
+/* Tail of a residual block with a projection shortcut, in one launch
+ * (Sec. 3.2.3, Eq. 7-8: the skip operand is the shortcut convolution's int32
+ * output v_p = acc_p + bias_p, one of the paper's 32-bit integer operands;
+ * here it stays in registers instead of making a round trip through memory).
+ * The outputs are exactly those of
+ *     qconv_run(proj, level, n, hp, wp, xp, NULL, 0, 0, t)    (t: int32)
+ *     qconv_run(conv, level, n, h, w, x, t, ho, wo, y)
+ * without the tensor t.
+ * x:  device, [n][h][w][conv cin] codes; xp: device, [n][hp][wp][proj cin]
+ *     codes; y: device, [n][ho][wo][cout] codes (bits_out of conv).
+ * Requirements, else AQD_ERR_UNSUPPORTED (nothing launched; run the two
+ * calls above instead): conv has AQD_OUT_CODES, skip_bits 32 and no
+ * upsample; proj has AQD_OUT_INT32, no skip, a 1x1 kernel and pad 0; both
+ * take 4-bit activations, have the same cout, a multiple of 256, and cin a
+ * multiple of 64; proj's output size for hp x wp equals conv's for h x w.
+ * level must be valid for both handles. Other errors as qconv_run. */
+aqd_status_t qconv_run_proj(qconv_t conv, qconv_t proj, int level, int n, int h, int w,
+                            const void *x, int hp, int wp, const void *xp, void *y,
+                            aqd_stream_t stream);
+
 void qconv_destroy(qconv_t conv);
 
 /* Standalone integer skip connection (Sec. 3.2.3, Eq. 7) with

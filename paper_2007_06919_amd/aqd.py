@@ -74,6 +74,7 @@ def lib():
             "qconv_run_group": ([i, POINTER(QconvSeg), vp], st),
             "qconv_group_workspace": ([i, POINTER(QconvSeg), POINTER(ctypes.c_size_t)], st),
             "qconv_run_group_ws": ([i, POINTER(QconvSeg), vp, ctypes.c_size_t, vp], st),
+            "qconv_run_proj": ([vp, vp, i, i, i, i, vp, i, i, vp, vp, vp], st),
             "qconv_destroy": ([vp], None),
             "qadd_run": ([POINTER(QaddDesc), vp, vp, vp, POINTER(QaddParams), vp], st),
             "aqd_channel_sums": ([vp, c_int64, i, vp, vp], st),
@@ -97,7 +98,7 @@ def lib():
 
 def exported_symbols():
     return ["qconv_create", "qconv_out_shape", "qconv_run", "qconv_run_group",
-            "qconv_group_workspace", "qconv_run_group_ws", "qconv_destroy",
+            "qconv_group_workspace", "qconv_run_group_ws", "qconv_run_proj", "qconv_destroy",
             "qadd_run", "aqd_channel_sums", "aqd_last_error", "aqd_pack_codes",
             "aqd_unpack_codes", "aqd_approx_ratio", "aqd_normalize_multiplier",
             "aqd_bn_stats_from_sums", "aqd_fold_bn", "aqd_skip_params", "aqd_requant_params"]
@@ -190,6 +191,12 @@ def qconv_group_workspace(segs) -> int:
 def qconv_run_group_ws(segs, workspace, ws_bytes, stream=None):
     _check(lib().qconv_run_group_ws(len(segs), _seg_array(segs), _addr(workspace), ws_bytes,
                                     _stream(stream)))
+
+
+def qconv_run_proj(conv, proj, level, n, h, w, x, hp, wp, xp, y, stream=None):
+    """Residual tail with the projection shortcut fused (see aqd.h)."""
+    _check(lib().qconv_run_proj(conv, proj, level, n, h, w, _addr(x), hp, wp, _addr(xp), _addr(y),
+                                _stream(stream)))
 
 
 def qconv_destroy(conv):

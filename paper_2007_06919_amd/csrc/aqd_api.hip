@@ -650,6 +650,92 @@ aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t st
     return qconv_run_group_ws(count, segs, nullptr, 0, stream);
 }
 
+aqd_status_t qconv_run_proj(qconv_t conv, qconv_t proj, int level, int n, int h, int w,
+                            const void *x, int hp, int wp, const void *xp, void *y,
+                            aqd_stream_t stream_)
+{
+    REQUIRE(conv && proj, "null handle");
+    const qconv_desc_t &d = conv->d, &e = proj->d;
+    REQUIRE(level >= 0 && level < d.num_levels && level < e.num_levels, "level out of range");
+    REQUIRE(n >= 0, "n must be >= 0");
+    int ho = 0, wo = 0, hpo = 0, wpo = 0;
+    aqd_status_t st = qconv_out_shape(conv, h, w, &ho, &wo);
+    if (st != AQD_OK)
+        return st;
+    st = qconv_out_shape(proj, hp, wp, &hpo, &wpo);
+    if (st != AQD_OK)
+        return st;
+    REQUIRE(hpo == ho && wpo == wo, "the projection's output size differs from the convolution's");
+    REQUIRE((long long)n * ho * wo < (1LL << 31) && (long long)n * h * w < (1LL << 31) &&
+                (long long)n * hp * wp < (1LL << 31),
+            "too many pixels for one call");
+    if (!(conv->mfma && proj->mfma && d.out_mode == AQD_OUT_CODES && d.skip_bits == 32 && !d.skip_up2 &&
+          e.out_mode == AQD_OUT_INT32 && e.skip_bits == 0 && e.kh == 1 && e.kw == 1 && e.pad == 0 &&
+          d.bits_in == 4 && e.bits_in == 4 && d.bits_out == 4 && d.cout == e.cout &&
+          conv->tile_cfg == TILE_256x128 && proj->tile_cfg == TILE_256x128))
+        return fail(AQD_ERR_UNSUPPORTED, "this pair of handles has no fused launch; run them separately");
+    if (n == 0)
+        return AQD_OK;
+    REQUIRE(x && xp && y, "null tensor");
+    REQUIRE(aligned16(x) && aligned16(xp) && aligned16(y), "tensors must be 16-byte aligned");
+    const size_t xbytes = (size_t)n * h * w * d.cin * d.bits_in / 8;
+    const size_t pbytes = (size_t)n * hp * wp * e.cin * e.bits_in / 8;
+    const size_t ybytes = (size_t)n * ho * wo * d.cout * d.bits_out / 8;
+    REQUIRE(!overlap(y, ybytes, x, xbytes) && !overlap(y, ybytes, xp, pbytes),
+            "output overlaps an input");
+    MfmaArgs a{};
+    a.nseg = 1;
+    MfmaSeg &m = a.seg[0];
+    m.x = (const uint8_t *)x;
+    m.skip = nullptr;
+    m.y = y;
+    m.wt = (const int8_t *)conv->w_dev;
+    m.epi = conv->epi_dev + (size_t)level * EPI_FIELDS * conv->cout_pad;
+    m.P = (long long)n * ho * wo;
+    m.n = n;
+    m.h = h;
+    m.w = w;
+    m.ho = ho;
+    m.wo = wo;
+    m.hs = ho;
+    m.ws = wo;
+    m.tile_begin = 0;
+    m.fast = conv->fast[level];
+    m.side0 = 0;
+    m.x2 = (const uint8_t *)xp;
+    m.wt2 = (const int8_t *)proj->w_dev;
+    m.epi2 = proj->epi_dev + (size_t)level * EPI_FIELDS * proj->cout_pad;
+    m.h2 = hp;
+    m.w2 = wp;
+    const long long tiles = (m.P + PROJ_BLK_PX - 1) / PROJ_BLK_PX * conv->co_tiles;
+    REQUIRE(tiles < (1LL << 26), "too many tiles for one launch");
+    a.total_tiles = (int)tiles;
+    a.tiles_per_xcd = (a.total_tiles + 7) / 8;
+    a.ksplit = 1;
+    a.kchunk = conv->ksteps;
+    a.part = 0;
+    a.cin = d.cin;
+    a.cout = d.cout;
+    a.cout_pad = conv->cout_pad;
+    a.kh = d.kh;
+    a.kw = d.kw;
+    a.stride = d.stride;
+    a.pad = d.pad;
+    a.co_tiles = conv->co_tiles;
+    a.ksteps = conv->ksteps;
+    a.up2 = 0;
+    a.tile_cfg = conv->tile_cfg;
+    a.bits_out = d.bits_out;
+    a.skip_bits = 32;
+    a.zero = conv->zero;
+    a.cin2 = e.cin;
+    a.stride2 = e.stride;
+    a.ksteps2 = proj->ksteps;
+    if (launch_qconv_proj(a, (hipStream_t)stream_) != hipSuccess)
+        return fail(AQD_ERR_DEVICE, "fused projection launch failed");
+    return AQD_OK;
+}
+
 aqd_status_t qconv_run(qconv_t conv, int level, int n, int h, int w, const void *x, const void *skip,
                        int hs, int ws, void *y, aqd_stream_t stream)
 {

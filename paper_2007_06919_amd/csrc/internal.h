@@ -36,6 +36,11 @@ struct MfmaSeg {
     int tile_begin;      // first workgroup tile of this segment
     int fast;            // every shift of the level >= 2: 32-bit requantisation
     int side0;           // every skip side of the level is 0 (code skips use a table)
+    // projection shortcut (fused launch only): 1x1 conv of x2 whose int32 output is the skip
+    const uint8_t *x2;   // [n][h2][w2][cin2] codes
+    const int8_t *wt2;   // its weight tiles (same tile layout)
+    const int32_t *epi2; // its epilogue table (bias)
+    int h2, w2;
 };
 
 struct MfmaArgs {
@@ -54,10 +59,14 @@ struct MfmaArgs {
     int skip_bits;       // 0, 2, 4, 8 or 32
     int up2;
     const uint8_t *zero; // >= 16 zero bytes in device memory (source of padding taps)
+    int cin2, stride2, ksteps2;  // projection shortcut (fused launch only)
 };
 
 // bits_in in {2, 4}
 hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream);
+// fused projection shortcut (4-bit, 256 x 64 tiles): tile counts use blk_px = 64
+constexpr int PROJ_BLK_PX = 64;
+hipError_t launch_qconv_proj(const MfmaArgs &a, hipStream_t stream);
 
 // ---- split-K combine + epilogue (qconv_splitk.hip) ---------------------------
 struct SplitSeg {

@@ -95,14 +95,18 @@ struct Cfg {
     static constexpr int LDS_BUDGET = NW == 8 ? 163840 : 81920;
     static constexpr int NSTAGE = LDS_BUDGET / STAGE < 6 ? LDS_BUDGET / STAGE : 6;
     static constexpr int A_PER = A_STAGE / 1024 / NW;      // 1 KiB copies per wave and K step
-    static constexpr int B_PER = B_STAGE / 1024 / NW;
+    // activation copies: 1 KiB each, or one copy per wave with only BLANES
+    // lanes active when the stage is smaller than 1 KiB per wave
+    static constexpr int BCH = B_STAGE / NW < 1024 ? B_STAGE / NW : 1024;
+    static constexpr int BLANES = BCH / 16;
+    static constexpr int B_PER = B_STAGE / BCH / NW;
     static constexpr int NOPS = A_PER + B_PER;             // copy instructions per lane and K step
-    static constexpr int BPC = 1024 / PB;                  // pixels per 1 KiB chunk (32 / 64)
-    static constexpr int LPP = 64 / BPC;                   // lanes per pixel row (2 / 1)
+    static constexpr int BPC = BCH / PB;                   // pixels per copy
+    static constexpr int LPP = PB / 16;                    // lanes per pixel row (2 / 1)
     static constexpr int CPL = 4 * MI;                     // channels per lane and pixel (epilogue)
     static constexpr int OW = CPL * BI / 32;               // packed output dwords per lane and pixel
-    static_assert(A_STAGE % (1024 * NW) == 0 && B_STAGE % (1024 * NW) == 0,
-                  "a stage splits into 1 KiB copies, the same number per wave");
+    static_assert(A_STAGE % (1024 * NW) == 0 && B_STAGE % (BCH * NW) == 0 && BCH % PB == 0,
+                  "a stage splits into copies, the same number per wave");
     static_assert(NSTAGE >= 3, "ring of at least three stages");
     static_assert(NSTAGE * STAGE >= EPI_FIELDS * BCO * 4, "epilogue table fits in the ring");
 };
@@ -178,9 +182,15 @@ __device__ __forceinline__ void store_words(uint8_t *p, const uint32_t *w)
 // OUTK: 0 = codes of width BI, 1 = int32.
 // SKK: 0 = none, 1 = codes of width BI, 2 = int32.
 // FAST: every segment's shifts are >= 2 (32-bit requantisation).
-template <int BI, int MI, int NJ, int WC, int WP, int OUTK, int SKK, int FAST>
+// DUAL: the int32 skip is a second convolution computed in the same
+//   workgroup (a residual block's projection shortcut, 1x1 with stride
+//   A.stride2 on the block input x2): its K steps run first into a second
+//   accumulator set, then the main convolution's; the epilogue aligns
+//   v = acc + bias with v2 = acc2 + bias2 (Eq. 7-8) from registers.
+template <int BI, int MI, int NJ, int WC, int WP, int OUTK, int SKK, int FAST, int DUAL = 0>
 __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel(MfmaArgs A)
 {
+    static_assert(!DUAL || (OUTK == 0 && SKK == 2), "the projection is an int32 skip of a codes output");
     using C = Cfg<BI, MI, NJ, WC, WP>;
     constexpr int NT = C::NTH;
     __shared__ __attribute__((aligned(1024))) uint8_t lds_stages[C::NSTAGE * C::STAGE];
@@ -213,7 +223,9 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
     const int row_bytes = A.cin * BI / 8;
     const int kpt = A.cin / KC;
     const int kb = kpart * A.kchunk;                   // first K step of this part
-    const int KS = A.ksteps - kb < A.kchunk ? A.ksteps - kb : A.kchunk;  // >= 1 (host)
+    const int KSM = A.ksteps - kb < A.kchunk ? A.ksteps - kb : A.kchunk;  // >= 1 (host)
+    const int KS1 = DUAL ? A.ksteps2 : 0;              // projection steps (first)
+    const int KS = KS1 + KSM;
     const int hw = S.ho * S.wo;
 
     // Copies: chunk q of a stage (1 KiB) belongs to wave q % NW; which source
@@ -230,24 +242,32 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
     }
     int ih0[C::B_PER], iw0[C::B_PER];
     const uint8_t *xb[C::B_PER];
+    const uint8_t *xb2[DUAL ? C::B_PER : 1];
     bool pv[C::B_PER];
 #pragma unroll
     for (int t = 0; t < C::B_PER; ++t) {
         const int ploc = C::BPC * (C::NW * t + wave) + lane / C::LPP;
         const int part = lane % C::LPP;
         const long long p = (long long)px_tile * C::BPX + ploc;
-        pv[t] = p < S.P;
+        pv[t] = p < S.P && lane < C::BLANES;
         const int pn = pv[t] ? (int)(p / hw) : 0;
         const int prem = pv[t] ? (int)(p - (long long)pn * hw) : 0;
         const int oh = prem / S.wo, ow = prem - oh * S.wo;
+        const int sw = 16 * (BI == 4 ? (part ^ swz_b4(ploc)) : part);
         ih0[t] = oh * A.stride - A.pad;
         iw0[t] = ow * A.stride - A.pad;
-        xb[t] = S.x + (long long)pn * S.h * S.w * row_bytes + 16 * (BI == 4 ? (part ^ swz_b4(ploc)) : part);
+        xb[t] = S.x + (long long)pn * S.h * S.w * row_bytes + sw;
+        if constexpr (DUAL)  // 1x1 projection, no padding: always inside its input
+            xb2[t] = pv[t] ? S.x2 + (((long long)pn * S.h2 + oh * A.stride2) * S.w2 + ow * A.stride2) *
+                                        (A.cin2 * BI / 8) + sw
+                           : nullptr;
     }
 
     // Copy state: steps are issued in order, so the per-pixel source of the
     // current tap is computed once per tap (bsrc; null for padding taps).
     const int8_t *a_next = S.wt + ((long long)co_tile * A.ksteps + kb) * C::A_STAGE;
+    const int8_t *a2_next = DUAL ? S.wt2 + (long long)co_tile * KS1 * C::A_STAGE : nullptr;
+    int issued = 0;  // steps issued (the first KS1 are the projection's)
     const uint32_t lds_base = lds_addr(lds_stages);
     int tap_next = kb / kpt, cc_next = kb - (kb / kpt) * kpt, st_next = 0;
     const uint8_t *bsrc[C::B_PER];
@@ -269,25 +289,36 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
     // (activation copies first), issue_end (advance to the next step).
     uint32_t st_cur = 0;
     auto issue_begin = [&]() {
-        if (cc_next == 0)
+        if (!(DUAL && issued < KS1) && cc_next == 0)
             tap_sources();
         st_cur = lds_base + st_next * C::STAGE;
     };
     auto issue_copy = [&](auto d_c) {
         constexpr int d = decltype(d_c)::value;
-        if constexpr (d < C::B_PER)
-            dma16(bsrc[d] ? bsrc[d] + cc_next * C::PB : A.zero, st_cur + C::A_STAGE + (C::NW * d + wave) * 1024);
-        else
-            dma16(a_next + a_src[d - C::B_PER], st_cur + (C::NW * (d - C::B_PER) + wave) * 1024);
+        const bool proj = DUAL && issued < KS1;
+        if constexpr (d < C::B_PER) {
+            const uint8_t *src = proj ? (xb2[DUAL ? d : 0] ? xb2[DUAL ? d : 0] + issued * C::PB : A.zero)
+                                      : (bsrc[d] ? bsrc[d] + cc_next * C::PB : A.zero);
+            if (C::BLANES == 64 || lane < C::BLANES)
+                dma16(src, st_cur + C::A_STAGE + (C::NW * d + wave) * C::BCH);
+        } else {
+            dma16((proj ? a2_next : a_next) + a_src[d - C::B_PER], st_cur + (C::NW * (d - C::B_PER) + wave) * 1024);
+        }
     };
     auto issue_end = [&]() {
-        a_next += C::A_STAGE;
         if (++st_next == C::NSTAGE)
             st_next = 0;
-        if (++cc_next == kpt) {
-            cc_next = 0;
-            ++tap_next;
+        if (DUAL && issued < KS1) {
+            a2_next += C::A_STAGE;
+        } else {
+            a_next += C::A_STAGE;
+            if (++cc_next == kpt) {
+                cc_next = 0;
+                ++tap_next;
+            }
         }
+        if constexpr (DUAL)
+            ++issued;
     };
     auto issue = [&]() {
         issue_begin();
@@ -306,11 +337,15 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
     };
 
     v4i acc[MI][NJ];
+    v4i acc2[DUAL ? MI : 1][DUAL ? NJ : 1];  // projection accumulators (DUAL)
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < NJ; ++j)
+        for (int j = 0; j < NJ; ++j) {
             acc[i][j] = v4i{0, 0, 0, 0};
+            if constexpr (DUAL)
+                acc2[i][j] = v4i{0, 0, 0, 0};
+        }
 
     // fragment addresses inside a stage (swizzled as written above)
     const int a_off = (wc * C::TM + (lane & 15)) * KC + 16 * ((lane >> 4) ^ swz_a(lane & 15));
@@ -355,6 +390,8 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
         const int which = i / C::BCO, c = i - which * C::BCO;
         prm_r[t] = S.epi[which * A.cout_pad + co_tile * C::BCO + c];
     }
+    static_assert(!DUAL || C::BCO <= NT, "one projection bias per thread");
+    const int prm2_r = DUAL && tid < C::BCO ? S.epi2[EPI_BIAS * A.cout_pad + co_tile * C::BCO + tid] : 0;
     constexpr int CPL = C::CPL;
     const int g = lane >> 4;
     const int co_loc = wc * C::TM + CPL * g;      // first of this lane's CPL channels (in the tile)
@@ -381,12 +418,10 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
     // ks - 1; once every wave has those reads back (lgkmcnt(0) + barrier) it is
     // refilled with step ks + NSTAGE, so copies run NSTAGE steps ahead.
     int st_read = 1 % C::NSTAGE;  // stage of step ks + 1
-    for (int k0 = 0; k0 < KS; k0 += 2) {
-        static_for<2>([&](auto pc) {
+    // steps [kbeg, kend) into the accumulator set ac; register set P = ks & 1
+    auto steps = [&](auto &ac, int kbeg, int kend) {
+        auto one = [&](auto pc, int ks) {
             constexpr int P = decltype(pc)::value;
-            const int ks = k0 + P;
-            if (ks >= KS)
-                return;
             if (ks + 1 < KS) {
                 // step ks + 1 landed: copies up to step min(ks + NSTAGE - 1, KS - 1) were issued
                 const int last = ks + C::NSTAGE - 1 < KS - 1 ? ks + C::NSTAGE - 1 : KS - 1;
@@ -403,7 +438,7 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
                 const v4i bj = widen(fb[P][j]);
 #pragma unroll
                 for (int i = 0; i < MI; ++i)
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[P][i], bj, acc[i][j], 0, 0, 0);
+                    ac[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[P][i], bj, ac[i][j], 0, 0, 0);
                 read_b(st_read, fb[P ^ 1], j);
                 if (j < MI)
                     read_a(st_read, fa[P ^ 1], j);
@@ -428,8 +463,21 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
             });
             if (++st_read == C::NSTAGE)
                 st_read = 0;
-        });
-    }
+        };
+        using P0 = std::integral_constant<int, 0>;
+        using P1 = std::integral_constant<int, 1>;
+        int ks = kbeg;
+        if ((ks & 1) && ks < kend)
+            one(P1{}, ks++);
+        for (; ks < kend; ks += 2) {
+            one(P0{}, ks);
+            if (ks + 1 < kend)
+                one(P1{}, ks + 1);
+        }
+    };
+    if constexpr (DUAL)
+        steps(acc2, 0, KS1);
+    steps(acc, KS1, KS);
 
     // ---------------------------------------------------------------- epilogue
     // The ring is idle after the last step; it now holds this channel tile's
@@ -463,6 +511,8 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
 #pragma unroll
     for (int t = 0; t < PRM_PER; ++t)
         prm[tid + t * NT] = prm_r[t];
+    if (DUAL && tid < C::BCO)
+        prm[EPI_FIELDS * C::BCO + tid] = prm2_r;  // projection bias (no table follows)
     __syncthreads();
     if (use_lut) {
         // every skip operand is a b-bit code scaled by c / 2^d (side 0): tabulate
@@ -480,8 +530,10 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
     constexpr int JP = 2;                         // column tiles per pass
     constexpr int LPR = C::TM / 4;                // lanes per staged row (16 B each)
     constexpr int RPI = 64 / LPR;                 // rows per instruction
-    static_assert(EPI_FIELDS * C::BCO * 4 + C::NW * 16 * JP * ROWB <= C::NSTAGE * C::STAGE,
+    static_assert((OUTK == 0 && (SKK != 2 || DUAL)) ||
+                      EPI_FIELDS * C::BCO * 4 + C::NW * 16 * JP * ROWB <= C::NSTAGE * C::STAGE,
                   "int32 staging fits in the ring");
+    static_assert((EPI_FIELDS + 1) * C::BCO * 4 <= C::NSTAGE * C::STAGE, "epilogue tables fit in the ring");
     uint8_t *stg = lds_stages + EPI_FIELDS * C::BCO * 4 + wave * (16 * JP * ROWB);
 
     if constexpr (OUTK == 1) {
@@ -559,7 +611,14 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
                 if (!okj[j])
                     return;
                 int kv[4] = {0, 0, 0, 0};
-                if constexpr (SKK == 2) {
+                if constexpr (DUAL) {
+                    // v2 = acc2 + bias2, the projection's int32 output (wraps like the stored tensor)
+                    const int4 p4 = *(const int4 *)(prm + EPI_FIELDS * C::BCO + cl);
+                    kv[0] = (int)((unsigned)acc2[i][j][0] + (unsigned)p4.x);
+                    kv[1] = (int)((unsigned)acc2[i][j][1] + (unsigned)p4.y);
+                    kv[2] = (int)((unsigned)acc2[i][j][2] + (unsigned)p4.z);
+                    kv[3] = (int)((unsigned)acc2[i][j][3] + (unsigned)p4.w);
+                } else if constexpr (SKK == 2) {
                     const int4 k4 = *(const int4 *)(stg + ((j - J0) * 16 + (lane & 15)) * ROWB + (CPL * g + 4 * i) * 4);
                     kv[0] = k4.x; kv[1] = k4.y; kv[2] = k4.z; kv[3] = k4.w;
                 } else if constexpr (SKK == 1) {
@@ -600,7 +659,9 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
     };
     using I0 = std::integral_constant<int, 0>;
     using INJ = std::integral_constant<int, NJ>;
-    if constexpr (SKK == 2) {
+    if constexpr (DUAL) {
+        body(std::false_type{}, I0{}, INJ{});
+    } else if constexpr (SKK == 2) {
         // int32 skip: JP column tiles per pass, staged with row-contiguous loads
         static_for<NJ / JP>([&](auto pc) {
             constexpr int pass = decltype(pc)::value;
@@ -683,6 +744,23 @@ void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane)
     case TILE_128x256: *blk_co = 128; *blk_px = 256; *chan_per_lane = 16; return;
     default: *blk_co = 64; *blk_px = 512; *chan_per_lane = 16; return;
     }
+}
+
+hipError_t launch_qconv_proj(const MfmaArgs &a, hipStream_t stream)
+{
+    // 256 x 64 tiles (two accumulator sets per wave), the 256-channel weight layout
+    constexpr int BI = 4, MI = 8, NJ = 2, WC = 2, WP = 2;
+    if (a.bits_out != BI || a.skip_bits != 32)
+        return hipErrorInvalidValue;
+    dim3 grid(8 * a.tiles_per_xcd), block(64 * WC * WP);
+    bool fast = true;
+    for (int i = 0; i < a.nseg; ++i)
+        fast = fast && a.seg[i].fast;
+    if (fast)
+        hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, WP, 0, 2, 1, 1>), grid, block, 0, stream, a);
+    else
+        hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, WP, 0, 2, 0, 1>), grid, block, 0, stream, a);
+    return hipGetLastError();
 }
 
 hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)

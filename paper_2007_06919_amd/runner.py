@@ -9,6 +9,10 @@ A network description (``workloads.NetSpec``) becomes a list of grouped
   depth and configuration (same shapes, bitwidths and modes) share a launch:
   the pyramid levels of a head layer (one epilogue table per level,
   multi-level BN, Sec. 3.2.2) and the class and box towers at equal depth;
+* a residual block's projection shortcut (1x1 conv with int32 output read
+  only by the block's last conv) runs fused into that conv
+  (``qconv_run_proj``): its int32 tensor is not written during a forward
+  pass (it is written once, at set-up, by the calibration pass);
 * one workspace, sized for the largest group's split-K need
   (``qconv_group_workspace``), lets small launches split their K reduction
   over more workgroups (``qconv_run_group_ws``);
@@ -39,7 +43,7 @@ def _conv_key(net: NetSpec, conv) -> tuple:
 
 class Net:
     def __init__(self, net: NetSpec, params: NetParams, device="cuda:0", stream=None,
-                 split_k: bool = True):
+                 split_k: bool = True, fuse_proj: bool = True):
         import torch
 
         self.torch = torch
@@ -61,6 +65,8 @@ class Net:
         self.tables: Dict[str, List[dict]] = {}
         self._alpha_t: Dict[str, np.ndarray] = {}
         self.schedule = self._make_schedule()
+        self.fused = self._fusable() if fuse_proj else {}
+        self._fused_away = {d.name for d in self.fused.values()}
         self._build()
         self.ws_bytes = 0
         if split_k:
@@ -70,6 +76,39 @@ class Net:
                    if self.ws_bytes else None)
 
     # ---------------------------------------------------------------- setup
+    def _fusable(self) -> dict:
+        """conv name -> projection conv, for the pairs qconv_run_proj covers."""
+        net = self.net
+        producer, consumers = {}, {}
+        for conv in net.convs:
+            for x, skip, y in conv.segs:
+                producer[y] = conv
+                for src in (x, skip):
+                    if src is not None:
+                        consumers[src] = consumers.get(src, 0) + 1
+        out = {}
+        for conv in net.convs:
+            if len(conv.segs) != 1:
+                continue
+            x, skip, y = conv.segs[0]
+            if skip is None or net.tensors[skip].bits != 32 or conv.skip_up2:
+                continue
+            d = producer.get(skip)
+            if d is None or len(d.segs) != 1 or d.k != 1 or consumers.get(skip) != 1:
+                continue
+            if (net.tensors[x].bits != 4 or net.tensors[y].bits != 4 or conv.cout % 256 or
+                    net.tensors[d.segs[0][0]].bits != 4 or d.cin % 64 or conv.cin % 64):
+                continue
+            out[conv.name] = d
+        return out
+
+    def launches_per_forward(self) -> int:
+        n = 0
+        for group in self.schedule:
+            plain = [c for c, _ in group if c.name not in self._fused_away and c.name not in self.fused]
+            n += (1 if plain else 0) + sum(1 for c, _ in group if c.name in self.fused)
+        return n
+
     def _make_schedule(self) -> List[List[Tuple[object, int]]]:
         producer = {}
         for conv in self.net.convs:
@@ -189,13 +228,26 @@ class Net:
         for gi, group in enumerate(self.schedule):
             if launch_hook:
                 launch_hook(gi, "before")
-            segs = [self._seg_args(conv, si) for conv, si in group]
-            if self.ws is not None:
-                aqd.qconv_run_group_ws(segs, self.ws, self.ws_bytes, s)
-            else:
-                aqd.qconv_run_group(segs, s)
+            plain = [(c, si) for c, si in group
+                     if c.name not in self._fused_away and c.name not in self.fused]
+            if plain:
+                segs = [self._seg_args(conv, si) for conv, si in plain]
+                if self.ws is not None:
+                    aqd.qconv_run_group_ws(segs, self.ws, self.ws_bytes, s)
+                else:
+                    aqd.qconv_run_group(segs, s)
+            for conv, si in group:
+                if conv.name in self.fused:
+                    self._run_fused(conv, self.fused[conv.name], s)
             if launch_hook:
                 launch_hook(gi, "after")
+
+    def _run_fused(self, conv, proj, stream):
+        x, _, y = conv.segs[0]
+        xp = proj.segs[0][0]
+        tx, tp = self.net.tensors[x], self.net.tensors[xp]
+        aqd.qconv_run_proj(self.handles[conv.name], self.handles[proj.name], 0, tx.n, tx.h, tx.w,
+                           self.bufs[x], tp.h, tp.w, self.bufs[xp], self.bufs[y], stream)
 
     def group_macs(self, group) -> int:
         tot = 0

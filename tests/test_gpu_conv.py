@@ -234,3 +234,92 @@ def test_channel_sums(torch):
     s1, s2, cnt = ref.channel_sums(v)
     assert cnt == 3001
     assert s[:300].tolist() == s1 and s[300:].tolist() == s2
+
+
+PROJ_CASES = [
+    # (n, h, w, cin, hp, wp, cin_p, stride_p, cout, k, wenc)
+    (1, 20, 23, 64, 20, 23, 64, 1, 256, 1, 1),       # first bottleneck block: stride 1 shortcut
+    (2, 13, 17, 128, 26, 33, 256, 2, 512, 1, 1),     # later stages: stride 2 shortcut, 2 channel tiles
+    (1, 9, 11, 256, 17, 21, 512, 2, 1024, 1, 0),     # ragged pixels, two's-complement weights
+    (1, 12, 10, 64, 12, 10, 128, 1, 256, 3, 1),      # 3x3 main convolution
+]
+
+
+def _proj_case(case, seed, general=False):
+    n, h, w, cin, hp, wp, cin_p, sp, cout, k, wenc = case
+    main = workloads.random_conv_case(seed=seed, n=n, h=h, w=w, cin=cin, cout=cout, k=k, bits_in=4,
+                                      bits_w=4, wenc=wenc, bits_out=4, skip_bits=32)
+    proj = workloads.random_conv_case(seed=seed + 1, n=n, h=hp, w=wp, cin=cin_p, cout=cout, k=1,
+                                      stride=sp, bits_in=4, bits_w=4, wenc=wenc, bits_out=32)
+    # the skip operand of the main convolution is the projection's int32 output
+    t = oracle_conv(proj)
+    assert t.shape == (n, main.skip.shape[1], main.skip.shape[2], cout)
+    main.skip = t
+    if general:
+        rng = np.random.Generator(np.random.PCG64(seed))
+        main.levels[0]["shift"] = rng.integers(-2, 2, size=cout).astype(np.int32)
+        main.levels[0]["mult"] = rng.integers(1 << 24, 1 << 26, size=cout).astype(np.int32)
+    return main, proj
+
+
+def _run_proj(torch, main, proj, fused=True):
+    dev = torch.device("cuda:0")
+    L = main.levels
+    hm = aqd.qconv_create(main.cin, main.cout, main.k, 1, main.pad, 4, 4,
+                          aqd.pack_codes(main.w_fields, 4), L, wenc=main.wenc, bits_out=4,
+                          skip_bits=32)
+    hp_ = aqd.qconv_create(proj.cin, proj.cout, 1, proj.stride, 0, 4, 4,
+                           aqd.pack_codes(proj.w_fields, 4), proj.levels, wenc=proj.wenc,
+                           out_mode=aqd.OUT_INT32, bits_out=0)
+    try:
+        ho, wo = aqd.qconv_out_shape(hm, main.h, main.w)
+        x = torch.from_numpy(aqd.pack_codes(main.x, 4)).to(dev)
+        xp = torch.from_numpy(aqd.pack_codes(proj.x, 4)).to(dev)
+        y = torch.full((main.n, ho, wo, main.cout // 2), 0xA5, dtype=torch.uint8, device=dev)
+        if fused:
+            aqd.qconv_run_proj(hm, hp_, 0, main.n, main.h, main.w, x, proj.h, proj.w, xp, y)
+        else:
+            t = torch.empty((main.n, ho, wo, main.cout), dtype=torch.int32, device=dev)
+            aqd.qconv_run(hp_, 0, proj.n, proj.h, proj.w, xp, None, 0, 0, t)
+            aqd.qconv_run(hm, 0, main.n, main.h, main.w, x, t, ho, wo, y)
+        torch.cuda.synchronize()
+        return y.cpu().numpy()
+    finally:
+        aqd.qconv_destroy(hm)
+        aqd.qconv_destroy(hp_)
+
+
+@pytest.mark.parametrize("case", PROJ_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_fused_projection_parity(torch, case):
+    """qconv_run_proj: bit-exact against the oracle's two convolutions, and
+    the same bytes as the two separate launches."""
+    main, proj = _proj_case(case, seed=hash(case) % 1000 + 11)
+    got = _run_proj(torch, main, proj)
+    assert_same(got, oracle_conv(main), f"fused projection {case}")
+    assert_same(got, _run_proj(torch, main, proj, fused=False), f"fused vs separate {case}")
+
+
+def test_fused_projection_general_requant(torch):
+    """Levels with shift < 2 take the 64-bit requantisation in the fused launch."""
+    main, proj = _proj_case(PROJ_CASES[1], seed=23, general=True)
+    assert_same(_run_proj(torch, main, proj), oracle_conv(main), "fused projection, shift < 2")
+
+
+def test_fused_projection_unsupported_pairs(torch):
+    """A pair the fused kernel does not cover is refused without a launch."""
+    case = workloads.random_conv_case(seed=2, n=1, h=8, w=8, cin=64, cout=128, k=1, bits_in=2,
+                                      bits_w=2, bits_out=2, skip_bits=32)
+    hm = aqd.qconv_create(64, 128, 1, 1, 0, 2, 2, aqd.pack_codes(case.w_fields, 2), case.levels,
+                          bits_out=2, skip_bits=32)
+    hp_ = aqd.qconv_create(64, 128, 1, 1, 0, 2, 2, aqd.pack_codes(case.w_fields, 2), case.levels,
+                           out_mode=aqd.OUT_INT32, bits_out=0)
+    try:
+        dev = torch.device("cuda:0")
+        x = torch.zeros((1, 8, 8, 16), dtype=torch.uint8, device=dev)
+        y = torch.zeros((1, 8, 8, 32), dtype=torch.uint8, device=dev)
+        with pytest.raises(aqd.AqdError) as e:
+            aqd.qconv_run_proj(hm, hp_, 0, 1, 8, 8, x, 8, 8, x, y)
+        assert e.value.status == aqd.AQD_ERR_UNSUPPORTED
+    finally:
+        aqd.qconv_destroy(hm)
+        aqd.qconv_destroy(hp_)
