@@ -60,3 +60,30 @@ def test_scaled_networks(torch, cfg, n, h, w):
     grouping; every layer's output and every epilogue table."""
     net, params = workloads.scaled_config(cfg, n, h, w)
     compare_network(torch, net, params)
+
+
+# ---------------------------------------------------------------- full sizes
+# The workloads at their real sizes: workloads 2 and 3 (one 800 x 1333 image)
+# in full, and workload 4 (batch 8) in the launch configuration the benchmark
+# times (split K, fused projection shortcuts), checked on images 0 (the
+# calibration image: every table) and 7 (the last image of the batch); the
+# oracle evaluates those images from the seeded inputs.
+
+
+def test_config2_full(torch):
+    """Detection heads on the five pyramid levels of one 800x1333 image."""
+    net, params = workloads.config(2)
+    compare_network(torch, net, params)
+
+
+def test_config3_full(torch):
+    """2-bit ResNet-50 + FPN on one 800x1333 image."""
+    net, params = workloads.config(3)
+    compare_network(torch, net, params)
+
+
+def test_config4_bench_configuration(torch):
+    """The benchmarked network, built as the benchmark builds it."""
+    net, params = workloads.config(4)
+    gpu, _ = compare_network(torch, net, params, images=[0, 7])
+    assert gpu.fused and gpu.ws_bytes > 0
