@@ -23,6 +23,19 @@ sys.path.insert(0, ROOT)
 
 METRIC = "int TOPS per qconv layer + ms/image quantized RetinaNet-R50 800x1333, 1 GPU"
 MFMA_I8_PEAK_TOPS = 5000.0  # MI355X dense int8 MFMA
+COPY_PROBE_BYTES = 256 << 20
+
+# HBM traffic of one head-tower launch, from two rocprofv3 counter runs
+# (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain copy of
+# COPY_PROBE_BYTES; valid only for the kernel source it was measured on.
+HEAD_TRAFFIC = {"kernel_sha256": "5f6b01288300aca000871399807a554e91aedabc01cbff00aec4026571d233a3",
+                "fetch_bytes": 50980736, "write_bytes": 45670400}
+
+
+def kernel_sha256():
+    import hashlib
+    with open(os.path.join(ROOT, "paper_2007_06919_amd", "csrc", "qconv_mfma.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
 
 
 def log(*a):
@@ -66,11 +79,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="after the run, one device copy of 256 MiB (a kernel of known traffic "
+                         "for calibrating memory counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
-              f"layout (one image per GPU) is described in DESIGN.md and not run here.",
-              file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); several GPUs "
+              f"would each take whole images of the batch, which is not run here.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -144,13 +159,25 @@ def main():
                    "bits": 4, "conv_segments": sum(len(c.segs) for c in net.convs),
                    "launches_per_step": gpu.launches_per_forward(), "int_ops_per_step": total_ops},
         "ms_per_image": round(ms_step / n_img, 4),
-        "roofline": {"bound": "mfma", "kernel": "qconv_mfma_kernel<4,4,0> (head tower 3x3 256->256, "
-                                                "10 segments)",
+        "roofline": {"bound": "mfma",
+                     "kernel": "qconv_mfma_kernel<4,8,4,2,2,0,0,1,0> (head towers 3x3 256->256, "
+                               "10 segments, 256x128 tiles)",
                      "achieved": round(achieved, 2), "peak": MFMA_I8_PEAK_TOPS, "unit": "TOPS",
                      "frac": round(achieved / MFMA_I8_PEAK_TOPS, 4), "traffic": None,
                      "avg_launch_us": round(avg_ms * 1e3, 2), "ops_per_launch": int(avg_ops)},
     }
+    traffic = None
+    if HEAD_TRAFFIC and HEAD_TRAFFIC["kernel_sha256"] == kernel_sha256():
+        traffic = HEAD_TRAFFIC["fetch_bytes"] + HEAD_TRAFFIC["write_bytes"]
+    out["roofline"]["traffic"] = traffic
     gpu.close()
+    if args.copy_probe:
+        src = torch.ones(COPY_PROBE_BYTES, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copy probe: {COPY_PROBE_BYTES} bytes device to device")
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
         out["cpu_baseline"] = cpu_baseline(args.cpu_budget)

@@ -6,14 +6,14 @@
 // from the NHWC input per filter tap), K = taps x input channels; one K step
 // is 64 input channels of one tap.
 //
-// Workgroup: 256 threads = 4 waves in a WC x WP grid. A wave owns MI x NJ
-// accumulator tiles of 16 x 16 (128 int32 accumulators per lane), i.e.
-// 16*MI channels x 16*NJ pixels; the workgroup tile is WC*16*MI x WP*16*NJ.
-// Two workgroups share a CU.
+// Workgroup: 4 waves in a WC x WP grid; a wave owns MI x NJ accumulator tiles
+// of 16 x 16, i.e. 16*MI channels x 16*NJ pixels; the workgroup tile is
+// WC*16*MI x WP*16*NJ. Two workgroups share a CU.
 //
 // Operand path: every K step is copied from global memory straight into LDS
-// (global_load_lds_dwordx4, no VGPR staging) into a ring of NSTAGE stages,
-// NSTAGE-1 steps ahead of the MFMAs:
+// (global_load_lds_dwordx4, no VGPR staging) into a ring of NSTAGE stages; a
+// stage is refilled as soon as every wave has read it, so copies run NSTAGE
+// steps ahead of the MFMAs:
 //  * weights: int8, decoded and tiled at create ([co_tile][k step][rows][64]),
 //    64-byte rows whose 16-byte columns are XOR-swizzled;
 //  * activations: the packed b-bit codes as stored in HBM (32 B per pixel and
@@ -33,7 +33,13 @@
 // requantisation uses 32-bit operations when every shift is >= 2: with
 // d = 31 + shift, floor((u*M + 2^(d-1)) / 2^d) = (mulhi(u, M) + 2^(d-33)) >>
 // (d-32) exactly (u*M = hi*2^32 + lo with 0 <= lo < 2^32 cannot carry into
-// the quotient); other levels take the 64-bit path.
+// the quotient); other levels take the 64-bit path. int32 outputs and int32
+// skips pass through LDS so that global accesses cover whole channel runs.
+//
+// Variants: a part of a split K range writes raw int32 partial sums (summed
+// and finished by the split-K epilogue kernel); the fused projection
+// shortcut (DUAL) runs a second 1x1 convolution into a second accumulator set
+// before the main one and aligns the two in the epilogue.
 //
 // Workgroup order: consecutive workgroup ids are dispatched round-robin over
 // the 8 XCDs; ids are remapped so that each XCD receives a contiguous range

@@ -1,10 +1,13 @@
-"""Per-layer durations from a rocprofv3 kernel trace of bench.py.
+"""Per-launch durations from a rocprofv3 kernel trace of bench.py.
 
-The runner issues its grouped launches in schedule order, so the last
-len(schedule) convolution dispatches of a trace are one forward pass; this
-maps them to layer names and prints duration, share and integer TOPS.
+The runner issues its launches in a fixed order (grouped convolutions, fused
+projection shortcuts, split-K convolutions followed by their combining
+kernel); this rebuilds that order for the workload, maps the trace's last
+forward passes onto it and prints, per launch, the median duration over
+those passes, its share and its integer TOPS (the fused launches count the
+shortcut's MACs too).
 
-usage: python -m paper_2007_06919_amd.trace_layers <kernel_trace.csv> [workload] [top]
+usage: python -m paper_2007_06919_amd.trace_layers <kernel_trace.csv> [workload] [top] [passes]
 """
 import csv
 import sys
@@ -13,29 +16,65 @@ import types
 from . import runner, workloads
 
 
-def layer_table(trace_csv, workload=4, top=30):
+def launch_list(net):
+    """[(name, convs, macs)] in the runner's launch order."""
+    o = types.SimpleNamespace(net=net)
+    sched = runner.Net._make_schedule(o)
+    fused = runner.Net._fusable(o)
+    away = {d.name for d in fused.values()}
+
+    def macs(c, si):
+        t = net.tensors[c.segs[si][2]]
+        return t.n * t.h * t.w * c.cout * c.k * c.k * c.cin
+
+    out = []
+    for g in sched:
+        plain = [(c, si) for c, si in g if c.name not in away and c.name not in fused]
+        if plain:
+            c = plain[0][0]
+            out.append((c.name + (f"+{len(plain) - 1}seg" if len(plain) > 1 else ""), c,
+                        sum(macs(cc, si) for cc, si in plain)))
+        for c, si in g:
+            if c.name in fused:
+                d = fused[c.name]
+                out.append((c.name + "+" + d.name.split(".")[-1], c, macs(c, si) + macs(d, 0)))
+    return out
+
+
+def layer_table(trace_csv, workload=4, top=30, passes=5):
     net, _ = workloads.config(workload)
-    sched = runner.Net._make_schedule(types.SimpleNamespace(net=net))
-    rows = [r for r in csv.DictReader(open(trace_csv))
-            if "qconv_mfma" in r["Kernel_Name"] or "qconv_direct" in r["Kernel_Name"]]
-    last = rows[-len(sched):]
-    out, tot = [], 0.0
-    for g, r in zip(sched, last):
+    launches = launch_list(net)
+    rows = sorted((r for r in csv.DictReader(open(trace_csv))
+                   if any(k in r["Kernel_Name"] for k in ("qconv_mfma", "qconv_direct", "splitk"))),
+                  key=lambda r: int(r["Start_Timestamp"]))
+    # one entry per launch; a combining kernel belongs to the launch before it
+    seq = []
+    for r in rows:
         us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-        macs = sum(net.tensors[c.segs[si][2]].n * net.tensors[c.segs[si][2]].h *
-                   net.tensors[c.segs[si][2]].w * c.cout * c.k * c.k * c.cin for c, si in g)
-        c = g[0][0]
-        name = c.name + (f"+{len(g) - 1}seg" if len(g) > 1 else "")
-        out.append((us, name, f"{c.k}x{c.k}s{c.stride} {c.cin}->{c.cout}",
-                    int(r["Grid_Size_X"]) // int(r["Workgroup_Size_X"]), 2 * macs / (us * 1e-6) / 1e12))
+        if "splitk" in r["Kernel_Name"] and seq:
+            seq[-1][0] += us
+            seq[-1][2] = True
+        else:
+            seq.append([us, int(r["Grid_Size_X"]) // int(r["Workgroup_Size_X"]), False])
+    n = len(launches)
+    passes = min(passes, len(seq) // n)
+    seq = seq[len(seq) - passes * n:]
+    out, tot = [], 0.0
+    for k, (name, c, macs) in enumerate(launches):
+        ts = sorted(seq[p * n + k][0] for p in range(passes))
+        us = ts[len(ts) // 2]
+        wg, split = seq[k][1], seq[k][2]
+        out.append((us, name + (" (split K)" if split else ""),
+                    f"{c.k}x{c.k}s{c.stride} {c.cin}->{c.cout}", wg, 2 * macs / (us * 1e-6) / 1e12))
         tot += us
-    lines = [f"total {tot / 1e3:.3f} ms over {len(sched)} launches"]
+    lines = [f"total {tot / 1e3:.3f} ms over {n} launches (median of {passes} passes)"]
     for us, name, shape, wg, tops in sorted(out, reverse=True)[:top]:
-        lines.append(f"{us:8.1f} us {100 * us / tot:5.1f}%  {name:22s} {shape:18s} wg={wg:6d} "
+        lines.append(f"{us:8.1f} us {100 * us / tot:5.1f}%  {name:30s} {shape:18s} wg={wg:6d} "
                      f"{tops:7.1f} TOPS")
     return "\n".join(lines)
 
 
 if __name__ == "__main__":
     print(layer_table(sys.argv[1], int(sys.argv[2]) if len(sys.argv) > 2 else 4,
-                      int(sys.argv[3]) if len(sys.argv) > 3 else 30))
+                      int(sys.argv[3]) if len(sys.argv) > 3 else 30,
+                      int(sys.argv[4]) if len(sys.argv) > 4 else 5))
