@@ -448,6 +448,7 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         return AQD_OK;
     MfmaArgs &a = *out;
     a = MfmaArgs{};
+    const int tile_cfg = h0.tile_cfg, blk_px = h0.blk_px;
     int tiles = 0;
     for (int i = 0; i < count; ++i) {
         const qconv_seg_t &s = segs[i];
@@ -470,7 +471,7 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         m.tile_begin = tiles;
         m.fast = s.conv->fast[s.level];
         m.side0 = s.conv->side0[s.level];
-        const long long px_tiles = (m.P + h0.blk_px - 1) / h0.blk_px;
+        const long long px_tiles = (m.P + blk_px - 1) / blk_px;
         REQUIRE(tiles + px_tiles * h0.co_tiles < (1LL << 26), "too many tiles for one launch");
         tiles += (int)(px_tiles * h0.co_tiles);
     }
@@ -489,7 +490,7 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
     a.co_tiles = h0.co_tiles;
     a.ksteps = h0.ksteps;
     a.up2 = h0.d.skip_up2;
-    a.tile_cfg = h0.tile_cfg;
+    a.tile_cfg = tile_cfg;
     a.bits_out = h0.d.out_mode == AQD_OUT_INT32 ? 32 : h0.d.bits_out;
     a.skip_bits = h0.d.skip_bits;
     a.zero = h0.zero;

@@ -96,9 +96,13 @@ struct Cfg {
     static constexpr int A_STAGE = BCO * KC;      // int8 weight rows of 64 B
     static constexpr int B_STAGE = BPX * PB;      // packed code rows of PB bytes
     static constexpr int STAGE = A_STAGE + B_STAGE;
-    // ring depth: 8-wave workgroups own the CU's LDS, 4-wave ones share it with a
-    // second; the epilogue table reuses the ring after the last K step
-    static constexpr int LDS_BUDGET = NW == 8 ? 163840 : 81920;
+    // one workgroup per CU when a wave holds 256 accumulators (they live in the
+    // AGPRs: 512 registers per lane at one wave per SIMD), else two
+    static constexpr int WG_PER_CU = (MI * NJ >= 64 || NW == 8) ? 1 : 2;
+    static constexpr int WAVES_PER_SIMD = NW / 4 * WG_PER_CU;  // occupancy the register budget targets
+    // ring depth: the workgroup's share of the CU's 160 KiB of LDS; the
+    // epilogue table reuses the ring after the last K step
+    static constexpr int LDS_BUDGET = WG_PER_CU == 1 ? 163840 : 81920;
     static constexpr int NSTAGE = LDS_BUDGET / STAGE < 6 ? LDS_BUDGET / STAGE : 6;
     static constexpr int A_PER = A_STAGE / 1024 / NW;      // 1 KiB copies per wave and K step
     // activation copies: 1 KiB each, or one copy per wave with only BLANES
@@ -134,7 +138,7 @@ __device__ __forceinline__ int swz_b4(int p) { return (p >> 3) & 1; }
 __device__ __forceinline__ void dma16(const void *g, uint32_t la)
 {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-                 ::"s"(la), "v"(g) : "memory", "m0");
+                 ::"s"(__builtin_amdgcn_readfirstlane(la)), "v"(g) : "memory", "m0");
 }
 #pragma clang diagnostic pop
 
@@ -194,7 +198,7 @@ __device__ __forceinline__ void store_words(uint8_t *p, const uint32_t *w)
 //   accumulator set, then the main convolution's; the epilogue aligns
 //   v = acc + bias with v2 = acc2 + bias2 (Eq. 7-8) from registers.
 template <int BI, int MI, int NJ, int WC, int WP, int OUTK, int SKK, int FAST, int DUAL = 0>
-__global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel(MfmaArgs A)
+__global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP>::WAVES_PER_SIMD)) qconv_mfma_kernel(MfmaArgs A)
 {
     static_assert(!DUAL || (OUTK == 0 && SKK == 2), "the projection is an int32 skip of a codes output");
     using C = Cfg<BI, MI, NJ, WC, WP>;
@@ -490,7 +494,7 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
     // epilogue table, the side-0 skip table and the int32 output staging.
     constexpr int QMAX = (1 << BI) - 1;
     int32_t *prm = (int32_t *)lds_stages;
-    int32_t *lut = prm + EPI_FIELDS * C::BCO;            // [BCO][2^BI]: RSM(k, c, d)
+    int32_t *lut = prm + EPI_FIELDS * C::BCO;            // [BCO][2^BI]: bias + RSM(k, c, d)
     const bool use_lut = SKK == 1 && S.side0;            // uniform over the workgroup
     // skip codes: issued before the table goes to LDS, so that the two overlap
     uint32_t skw[NJ][C::OW];
@@ -522,9 +526,11 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
     __syncthreads();
     if (use_lut) {
         // every skip operand is a b-bit code scaled by c / 2^d (side 0): tabulate
+        // bias + RSM(k, c, d), so that u = acc + table (modulo 2^32; u fits in int32)
         for (int i = tid; i < C::BCO * (QMAX + 1); i += NT) {
             const int cl = i >> BI;
-            lut[i] = rsm32(i & QMAX, prm[EPI_SKIP_C * C::BCO + cl], prm[EPI_SKIP_D * C::BCO + cl]);
+            lut[i] = (int)((unsigned)prm[EPI_BIAS * C::BCO + cl] +
+                           (unsigned)rsm32(i & QMAX, prm[EPI_SKIP_C * C::BCO + cl], prm[EPI_SKIP_D * C::BCO + cl]));
         }
         __syncthreads();
     }
@@ -642,7 +648,7 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
                         int u = v;
                         // u fits in int32, so the sum modulo 2^32 is exact
                         if constexpr (LUT) {
-                            u = (int)((unsigned)v + (unsigned)lut[((cl + e) << BI) | kv[e]]);
+                            u = (int)((unsigned)acc[i][j][e] + (unsigned)lut[((cl + e) << BI) | kv[e]]);
                         } else if constexpr (SKK != 0) {
                             const int scaled = rsm32(sside[e] ? v : kv[e], sc[e], sd[e]);
                             u = (int)((unsigned)scaled + (unsigned)(sside[e] ? kv[e] : v));
@@ -652,7 +658,7 @@ __global__ void __launch_bounds__(64 * WC * WP, 8 / (WC * WP)) qconv_mfma_kernel
                     } else {
                         long long u = v;
                         if constexpr (LUT)
-                            u = (int)((unsigned)v + (unsigned)lut[((cl + e) << BI) | kv[e]]);
+                            u = (int)((unsigned)acc[i][j][e] + (unsigned)lut[((cl + e) << BI) | kv[e]]);
                         else if constexpr (SKK != 0)
                             u = align_add(v, kv[e], sc[e], sd[e], sside[e]);
                         y = (int)requant_clamp(u, mult[e], shf[e], QMAX);
