@@ -448,7 +448,14 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         return AQD_OK;
     MfmaArgs &a = *out;
     a = MfmaArgs{};
-    const int tile_cfg = h0.tile_cfg, blk_px = h0.blk_px;
+    // launch tile: a handle laid out for 256-channel tiles runs short K ranges
+    // with code outputs on 256 x 64 tiles (three workgroups per CU)
+    int tile_cfg = h0.tile_cfg, blk_px = h0.blk_px;
+    if (h0.tile_cfg == TILE_256x128 && h0.ksteps <= 4 && h0.d.out_mode == AQD_OUT_CODES &&
+        h0.d.bits_in == 4 && (h0.d.skip_bits == 0 || h0.d.skip_bits == 4)) {
+        tile_cfg = TILE_256x64;
+        blk_px = 64;
+    }
     int tiles = 0;
     for (int i = 0; i < count; ++i) {
         const qconv_seg_t &s = segs[i];
@@ -506,6 +513,11 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
 // when the model gains 20%.
 void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
 {
+    if (a.tile_cfg == TILE_256x64) {  // short K: never split (its tile has no int32 path)
+        *nparts = 1;
+        *kchunk = a.ksteps;
+        return;
+    }
     long long P = 0;
     for (int i = 0; i < a.nseg; ++i)
         P += a.seg[i].P;

@@ -11,7 +11,8 @@ namespace aqd {
 // ---- implicit-GEMM MFMA kernel (qconv_mfma.hip) ----------------------------
 // One K step is KC input channels of one filter tap. Workgroup tile shapes
 // (output channels x output pixels), chosen per handle from cout:
-enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2 };
+enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
+       TILE_256x64 = 3 };  // launch-time choice for 256x128 handles: short K, code outputs
 constexpr int KC = 64;
 
 // tile shape of a configuration, and the channels one lane holds per pixel

@@ -83,7 +83,9 @@ __device__ __forceinline__ int rsm32(int a, int c, int d)
 }
 
 
-template <int BI, int MI, int NJ, int WC, int WP>
+// OCC: workgroups per CU the tile is built for (0: two, or one when a wave
+// holds 256 accumulators or the workgroup has 8 waves)
+template <int BI, int MI, int NJ, int WC, int WP, int OCC = 0>
 struct Cfg {
     static constexpr int WPC = WP;                // waves along pixels
     static constexpr int NW = WC * WP;            // waves per workgroup
@@ -98,11 +100,11 @@ struct Cfg {
     static constexpr int STAGE = A_STAGE + B_STAGE;
     // one workgroup per CU when a wave holds 256 accumulators (they live in the
     // AGPRs: 512 registers per lane at one wave per SIMD), else two
-    static constexpr int WG_PER_CU = (MI * NJ >= 64 || NW == 8) ? 1 : 2;
+    static constexpr int WG_PER_CU = OCC ? OCC : ((MI * NJ >= 64 || NW == 8) ? 1 : 2);
     static constexpr int WAVES_PER_SIMD = NW / 4 * WG_PER_CU;  // occupancy the register budget targets
     // ring depth: the workgroup's share of the CU's 160 KiB of LDS; the
     // epilogue table reuses the ring after the last K step
-    static constexpr int LDS_BUDGET = WG_PER_CU == 1 ? 163840 : 81920;
+    static constexpr int LDS_BUDGET = 163840 / WG_PER_CU / 1024 * 1024;
     static constexpr int NSTAGE = LDS_BUDGET / STAGE < 6 ? LDS_BUDGET / STAGE : 6;
     static constexpr int A_PER = A_STAGE / 1024 / NW;      // 1 KiB copies per wave and K step
     // activation copies: 1 KiB each, or one copy per wave with only BLANES
@@ -117,7 +119,7 @@ struct Cfg {
     static constexpr int OW = CPL * BI / 32;               // packed output dwords per lane and pixel
     static_assert(A_STAGE % (1024 * NW) == 0 && B_STAGE % (BCH * NW) == 0 && BCH % PB == 0,
                   "a stage splits into copies, the same number per wave");
-    static_assert(NSTAGE >= 3, "ring of at least three stages");
+    static_assert(NSTAGE >= 2, "ring of at least two stages");
     static_assert(NSTAGE * STAGE >= EPI_FIELDS * BCO * 4, "epilogue table fits in the ring");
 };
 
@@ -197,11 +199,11 @@ __device__ __forceinline__ void store_words(uint8_t *p, const uint32_t *w)
 //   A.stride2 on the block input x2): its K steps run first into a second
 //   accumulator set, then the main convolution's; the epilogue aligns
 //   v = acc + bias with v2 = acc2 + bias2 (Eq. 7-8) from registers.
-template <int BI, int MI, int NJ, int WC, int WP, int OUTK, int SKK, int FAST, int DUAL = 0>
-__global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP>::WAVES_PER_SIMD)) qconv_mfma_kernel(MfmaArgs A)
+template <int BI, int MI, int NJ, int WC, int WP, int OUTK, int SKK, int FAST, int DUAL = 0, int OCC = 0>
+__global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::WAVES_PER_SIMD)) qconv_mfma_kernel(MfmaArgs A)
 {
     static_assert(!DUAL || (OUTK == 0 && SKK == 2), "the projection is an int32 skip of a codes output");
-    using C = Cfg<BI, MI, NJ, WC, WP>;
+    using C = Cfg<BI, MI, NJ, WC, WP, OCC>;
     constexpr int NT = C::NTH;
     __shared__ __attribute__((aligned(1024))) uint8_t lds_stages[C::NSTAGE * C::STAGE];
 
@@ -546,6 +548,8 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP>::WAVES_
                       EPI_FIELDS * C::BCO * 4 + C::NW * 16 * JP * ROWB <= C::NSTAGE * C::STAGE,
                   "int32 staging fits in the ring");
     static_assert((EPI_FIELDS + 1) * C::BCO * 4 <= C::NSTAGE * C::STAGE, "epilogue tables fit in the ring");
+    static_assert(SKK != 1 || (EPI_FIELDS + (QMAX + 1)) * C::BCO * 4 <= C::NSTAGE * C::STAGE,
+                  "the skip table fits in the ring");
     uint8_t *stg = lds_stages + EPI_FIELDS * C::BCO * 4 + wave * (16 * JP * ROWB);
 
     if constexpr (OUTK == 1) {
@@ -753,9 +757,35 @@ void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane)
 {
     switch (tile_cfg) {
     case TILE_256x128: *blk_co = 256; *blk_px = 128; *chan_per_lane = 32; return;
+    case TILE_256x64: *blk_co = 256; *blk_px = 64; *chan_per_lane = 32; return;
     case TILE_128x256: *blk_co = 128; *blk_px = 256; *chan_per_lane = 16; return;
     default: *blk_co = 64; *blk_px = 512; *chan_per_lane = 16; return;
     }
+}
+
+// 256 x 64 tiles, three workgroups per CU: short K ranges (up to 4 steps)
+// with code outputs, where the epilogue, not the matrix cores, sets the pace
+hipError_t launch_qconv_short(const MfmaArgs &a, hipStream_t stream)
+{
+    constexpr int BI = 4, MI = 8, NJ = 2, WC = 2, WP = 2, OCC = 3;
+    if (a.bits_out != BI || (a.skip_bits != 0 && a.skip_bits != BI))
+        return hipErrorInvalidValue;
+    dim3 grid(8 * a.tiles_per_xcd), block(64 * WC * WP);
+    bool fast = true;
+    for (int i = 0; i < a.nseg; ++i)
+        fast = fast && a.seg[i].fast;
+    if (a.skip_bits == 0) {
+        if (fast)
+            hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, WP, 0, 0, 1, 0, OCC>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, WP, 0, 0, 0, 0, OCC>), grid, block, 0, stream, a);
+    } else {
+        if (fast)
+            hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, WP, 0, 1, 1, 0, OCC>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, WP, 0, 1, 0, 0, OCC>), grid, block, 0, stream, a);
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_qconv_proj(const MfmaArgs &a, hipStream_t stream)
@@ -780,6 +810,7 @@ hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
     if (bits_in == 4) {
         switch (a.tile_cfg) {
         case TILE_256x128: return launch_modes<4, 8, 4, 2, 2>(a, stream);
+        case TILE_256x64: return launch_qconv_short(a, stream);
         case TILE_128x256: return launch_modes<4, 4, 8, 2, 2>(a, stream);
         case TILE_64x512: return launch_modes<4, 4, 8, 1, 4>(a, stream);
         }
