@@ -448,13 +448,24 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         return AQD_OK;
     MfmaArgs &a = *out;
     a = MfmaArgs{};
-    // launch tile: a handle laid out for 256-channel tiles runs short K ranges
-    // with code outputs on 256 x 64 tiles (three workgroups per CU)
+    // launch tile for a handle laid out for 256-channel tiles: short K ranges with
+    // code outputs run on 256 x 64 tiles three to a CU; launches with fewer
+    // 256 x 128 tiles than CUs (but not tiny, and not so long in K that
+    // splitting K is the better cure) on 256 x 64 tiles two to a CU (measured:
+    // from ~260 tiles on, the larger tile is faster)
     int tile_cfg = h0.tile_cfg, blk_px = h0.blk_px;
-    if (h0.tile_cfg == TILE_256x128 && h0.ksteps <= 4 && h0.d.out_mode == AQD_OUT_CODES &&
-        h0.d.bits_in == 4 && (h0.d.skip_bits == 0 || h0.d.skip_bits == 4)) {
-        tile_cfg = TILE_256x64;
-        blk_px = 64;
+    if (h0.tile_cfg == TILE_256x128) {
+        long long t128 = 0;
+        for (int i = 0; i < count; ++i)
+            t128 += ((long long)segs[i].n * chk[i].ho * chk[i].wo + 127) / 128 * h0.co_tiles;
+        if (h0.ksteps <= 4 && h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_in == 4 &&
+            (h0.d.skip_bits == 0 || h0.d.skip_bits == 4)) {
+            tile_cfg = TILE_256x64S;
+            blk_px = 64;
+        } else if (t128 >= 64 && t128 < 200 && h0.ksteps <= 80) {
+            tile_cfg = TILE_256x64;
+            blk_px = 64;
+        }
     }
     int tiles = 0;
     for (int i = 0; i < count; ++i) {
@@ -513,7 +524,7 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
 // when the model gains 20%.
 void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
 {
-    if (a.tile_cfg == TILE_256x64) {  // short K: never split (its tile has no int32 path)
+    if (a.tile_cfg == TILE_256x64S || a.tile_cfg == TILE_256x64) {  // already balanced: never split
         *nparts = 1;
         *kchunk = a.ksteps;
         return;

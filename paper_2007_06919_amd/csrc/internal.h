@@ -12,7 +12,9 @@ namespace aqd {
 // One K step is KC input channels of one filter tap. Workgroup tile shapes
 // (output channels x output pixels), chosen per handle from cout:
 enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
-       TILE_256x64 = 3 };  // launch-time choice for 256x128 handles: short K, code outputs
+       // launch-time choices for handles laid out for 256x128 (same weight layout):
+       TILE_256x64S = 3,   // short K, code outputs: three workgroups per CU
+       TILE_256x64 = 4 };  // launches with too few 256x128 tiles to fill the GPU
 constexpr int KC = 64;
 
 // tile shape of a configuration, and the channels one lane holds per pixel

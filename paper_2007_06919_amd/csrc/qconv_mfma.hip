@@ -541,7 +541,8 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
     // a per-wave LDS staging area, JP column tiles (16 JP pixel rows) at a time,
     // so that global accesses cover whole contiguous channel runs of a pixel row
     constexpr int ROWB = C::TM * 4 + 16;          // staged row: TM channels + pad (bank spread)
-    constexpr int JP = 2;                         // column tiles per pass
+    // column tiles per pass: two when the staging fits in the ring, else one
+    constexpr int JP = EPI_FIELDS * C::BCO * 4 + C::NW * 32 * ROWB <= C::NSTAGE * C::STAGE ? 2 : 1;
     constexpr int LPR = C::TM / 4;                // lanes per staged row (16 B each)
     constexpr int RPI = 64 / LPR;                 // rows per instruction
     static_assert((OUTK == 0 && (SKK != 2 || DUAL)) ||
@@ -757,6 +758,7 @@ void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane)
 {
     switch (tile_cfg) {
     case TILE_256x128: *blk_co = 256; *blk_px = 128; *chan_per_lane = 32; return;
+    case TILE_256x64S:
     case TILE_256x64: *blk_co = 256; *blk_px = 64; *chan_per_lane = 32; return;
     case TILE_128x256: *blk_co = 128; *blk_px = 256; *chan_per_lane = 16; return;
     default: *blk_co = 64; *blk_px = 512; *chan_per_lane = 16; return;
@@ -810,7 +812,8 @@ hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
     if (bits_in == 4) {
         switch (a.tile_cfg) {
         case TILE_256x128: return launch_modes<4, 8, 4, 2, 2>(a, stream);
-        case TILE_256x64: return launch_qconv_short(a, stream);
+        case TILE_256x64S: return launch_qconv_short(a, stream);
+        case TILE_256x64: return launch_modes<4, 8, 2, 2, 2>(a, stream);
         case TILE_128x256: return launch_modes<4, 4, 8, 2, 2>(a, stream);
         case TILE_64x512: return launch_modes<4, 4, 8, 1, 4>(a, stream);
         }
