@@ -53,7 +53,7 @@ struct MfmaArgs {
     int tiles_per_xcd;   // grid = 8 * tiles_per_xcd workgroups
     int ksplit;          // parts of the K range per output tile (1: no split)
     int kchunk;          // K steps per part (the last part may have fewer)
-    int part;            // 1: write raw int32 partial sums (no bias) to y + part * P * cout
+    int part;            // 1: write int32 partial sums (part 0 with the bias) to y + part * P * cout
     int tile_cfg;
     int cin, cout, cout_pad;
     int kh, kw, stride, pad;

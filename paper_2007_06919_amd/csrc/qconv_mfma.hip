@@ -348,16 +348,30 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
         }
     };
 
+    // accumulators start at the bias (Eq. 6: v = acc + bias, one add per output
+    // saved): lane group g of tile i holds channels CPL*g + 4i + e of the wave's
+    // rows; a part of a split K range other than the first starts at zero
     v4i acc[MI][NJ];
     v4i acc2[DUAL ? MI : 1][DUAL ? NJ : 1];  // projection accumulators (DUAL)
+    {
+        const int ch0 = co_tile * C::BCO + wc * C::TM + C::CPL * (lane >> 4);
+        const bool with_bias = !(A.part && kpart > 0);
 #pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            acc[i][j] = v4i{0, 0, 0, 0};
+        for (int i = 0; i < MI; ++i) {
+            v4i b = v4i{0, 0, 0, 0};
+            if (with_bias)
+                b = *(const v4i *)(S.epi + EPI_BIAS * A.cout_pad + ch0 + 4 * i);
+            v4i b2 = v4i{0, 0, 0, 0};
             if constexpr (DUAL)
-                acc2[i][j] = v4i{0, 0, 0, 0};
+                b2 = *(const v4i *)(S.epi2 + EPI_BIAS * A.cout_pad + ch0 + 4 * i);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                acc[i][j] = b;
+                if constexpr (DUAL)
+                    acc2[i][j] = b2;
+            }
         }
+    }
 
     // fragment addresses inside a stage (swizzled as written above)
     const int a_off = (wc * C::TM + (lane & 15)) * KC + 16 * ((lane >> 4) ^ swz_a(lane & 15));
@@ -402,8 +416,7 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
         const int which = i / C::BCO, c = i - which * C::BCO;
         prm_r[t] = S.epi[which * A.cout_pad + co_tile * C::BCO + c];
     }
-    static_assert(!DUAL || C::BCO <= NT, "one projection bias per thread");
-    const int prm2_r = DUAL && tid < C::BCO ? S.epi2[EPI_BIAS * A.cout_pad + co_tile * C::BCO + tid] : 0;
+
     constexpr int CPL = C::CPL;
     const int g = lane >> 4;
     const int co_loc = wc * C::TM + CPL * g;      // first of this lane's CPL channels (in the tile)
@@ -496,7 +509,7 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
     // epilogue table, the side-0 skip table and the int32 output staging.
     constexpr int QMAX = (1 << BI) - 1;
     int32_t *prm = (int32_t *)lds_stages;
-    int32_t *lut = prm + EPI_FIELDS * C::BCO;            // [BCO][2^BI]: bias + RSM(k, c, d)
+    int32_t *lut = prm + EPI_FIELDS * C::BCO;            // [BCO][2^BI]: RSM(k, c, d)
     const bool use_lut = SKK == 1 && S.side0;            // uniform over the workgroup
     // skip codes: issued before the table goes to LDS, so that the two overlap
     uint32_t skw[NJ][C::OW];
@@ -523,16 +536,12 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
 #pragma unroll
     for (int t = 0; t < PRM_PER; ++t)
         prm[tid + t * NT] = prm_r[t];
-    if (DUAL && tid < C::BCO)
-        prm[EPI_FIELDS * C::BCO + tid] = prm2_r;  // projection bias (no table follows)
     __syncthreads();
     if (use_lut) {
         // every skip operand is a b-bit code scaled by c / 2^d (side 0): tabulate
-        // bias + RSM(k, c, d), so that u = acc + table (modulo 2^32; u fits in int32)
         for (int i = tid; i < C::BCO * (QMAX + 1); i += NT) {
             const int cl = i >> BI;
-            lut[i] = (int)((unsigned)prm[EPI_BIAS * C::BCO + cl] +
-                           (unsigned)rsm32(i & QMAX, prm[EPI_SKIP_C * C::BCO + cl], prm[EPI_SKIP_D * C::BCO + cl]));
+            lut[i] = rsm32(i & QMAX, prm[EPI_SKIP_C * C::BCO + cl], prm[EPI_SKIP_D * C::BCO + cl]);
         }
         __syncthreads();
     }
@@ -561,14 +570,11 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
                 constexpr int j = pass * JP + jj;
 #pragma unroll
                 for (int i = 0; i < MI; ++i) {
-                    int4 b4 = *(const int4 *)(prm + co_loc + 4 * i);
-                    if (A.part)
-                        b4 = make_int4(0, 0, 0, 0);   // partial sums: the bias is added once, later
-                    int4 o;
-                    o.x = acc[i][j][0] + b4.x;
-                    o.y = acc[i][j][1] + b4.y;
-                    o.z = acc[i][j][2] + b4.z;
-                    o.w = acc[i][j][3] + b4.w;
+                    int4 o;  // v = acc + bias (the bias is in the accumulators)
+                    o.x = acc[i][j][0];
+                    o.y = acc[i][j][1];
+                    o.z = acc[i][j][2];
+                    o.w = acc[i][j][3];
                     *(int4 *)(stg + (jj * 16 + (lane & 15)) * ROWB + (CPL * g + 4 * i) * 4) = o;
                 }
             });
@@ -603,10 +609,8 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
         static_for<MI>([&](auto ic) {
             constexpr int i = decltype(ic)::value;
             const int cl = co_loc + 4 * i;
-            const int4 b4 = *(const int4 *)(prm + EPI_BIAS * C::BCO + cl);
             const int4 m4 = *(const int4 *)(prm + EPI_MULT * C::BCO + cl);
             const int4 s4 = *(const int4 *)(prm + (FAST ? EPI_SHR : EPI_SHIFT) * C::BCO + cl);
-            const int bias[4] = {b4.x, b4.y, b4.z, b4.w};
             const int mult[4] = {m4.x, m4.y, m4.z, m4.w};
             const int shf[4] = {s4.x, s4.y, s4.z, s4.w};
             int rnd[4] = {0, 0, 0, 0};
@@ -629,12 +633,11 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
                     return;
                 int kv[4] = {0, 0, 0, 0};
                 if constexpr (DUAL) {
-                    // v2 = acc2 + bias2, the projection's int32 output (wraps like the stored tensor)
-                    const int4 p4 = *(const int4 *)(prm + EPI_FIELDS * C::BCO + cl);
-                    kv[0] = (int)((unsigned)acc2[i][j][0] + (unsigned)p4.x);
-                    kv[1] = (int)((unsigned)acc2[i][j][1] + (unsigned)p4.y);
-                    kv[2] = (int)((unsigned)acc2[i][j][2] + (unsigned)p4.z);
-                    kv[3] = (int)((unsigned)acc2[i][j][3] + (unsigned)p4.w);
+                    // v2 = acc2 (its bias included), the projection's int32 output
+                    kv[0] = acc2[i][j][0];
+                    kv[1] = acc2[i][j][1];
+                    kv[2] = acc2[i][j][2];
+                    kv[3] = acc2[i][j][3];
                 } else if constexpr (SKK == 2) {
                     const int4 k4 = *(const int4 *)(stg + ((j - J0) * 16 + (lane & 15)) * ROWB + (CPL * g + 4 * i) * 4);
                     kv[0] = k4.x; kv[1] = k4.y; kv[2] = k4.z; kv[3] = k4.w;
@@ -647,13 +650,13 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
                 }
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const int v = acc[i][j][e] + bias[e];
+                    const int v = acc[i][j][e];  // acc + bias
                     int y;
                     if constexpr (FAST) {
                         int u = v;
                         // u fits in int32, so the sum modulo 2^32 is exact
                         if constexpr (LUT) {
-                            u = (int)((unsigned)acc[i][j][e] + (unsigned)lut[((cl + e) << BI) | kv[e]]);
+                            u = (int)((unsigned)v + (unsigned)lut[((cl + e) << BI) | kv[e]]);
                         } else if constexpr (SKK != 0) {
                             const int scaled = rsm32(sside[e] ? v : kv[e], sc[e], sd[e]);
                             u = (int)((unsigned)scaled + (unsigned)(sside[e] ? kv[e] : v));
@@ -663,7 +666,7 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
                     } else {
                         long long u = v;
                         if constexpr (LUT)
-                            u = (int)((unsigned)acc[i][j][e] + (unsigned)lut[((cl + e) << BI) | kv[e]]);
+                            u = (int)((unsigned)v + (unsigned)lut[((cl + e) << BI) | kv[e]]);
                         else if constexpr (SKK != 0)
                             u = align_add(v, kv[e], sc[e], sd[e], sside[e]);
                         y = (int)requant_clamp(u, mult[e], shf[e], QMAX);

@@ -1,8 +1,9 @@
 // Second half of a split-K convolution: the int32 partial sums of the parts
 // of the K range (Sec. 3.2.1, Eq. 4: acc is an integer sum over taps and input
-// channels, so adding the parts gives acc exactly) are added, and the integer
-// epilogue runs on the result: v = acc + bias (Eq. 6), the optional skip
-// alignment (Eq. 7-8), requantisation and clamp.
+// channels, so adding the parts gives acc exactly; the first part started at
+// the bias, so the sum is v = acc + bias, Eq. 6) are added, and the rest of
+// the integer epilogue runs on the result: the optional skip alignment
+// (Eq. 7-8), requantisation and clamp.
 //
 // One work item = one output pixel x CPT consecutive channels: one packed
 // 32-bit word of b-bit codes (CPT = 32 / b) or four int32 outputs. The
@@ -51,10 +52,8 @@ __global__ void __launch_bounds__(256) splitk_epilogue_kernel(SplitArgs A)
         acc[q + 2] = t.z;
         acc[q + 3] = t.w;
     }
-    const int32_t *bias = S.epi + EPI_BIAS * A.cout_pad + c0;
     if constexpr (BO == 32) {
-        *(int4 *)((int32_t *)S.y + px * A.cout + c0) =
-            make_int4(acc[0] + bias[0], acc[1] + bias[1], acc[2] + bias[2], acc[3] + bias[3]);
+        *(int4 *)((int32_t *)S.y + px * A.cout + c0) = make_int4(acc[0], acc[1], acc[2], acc[3]);
     } else {
         long long spix = px;
         if (SB != 0 && A.up2) {
@@ -69,7 +68,7 @@ __global__ void __launch_bounds__(256) splitk_epilogue_kernel(SplitArgs A)
 #pragma unroll
         for (int e = 0; e < CPT; ++e) {
             const int c = c0 + e;
-            const int v = acc[e] + bias[e];
+            const int v = acc[e];
             long long u = v;
             if constexpr (SB == 32) {
                 const int k = ((const int32_t *)S.skip)[spix * A.cout + c];
