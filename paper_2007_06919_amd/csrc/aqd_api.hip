@@ -112,6 +112,7 @@ struct qconv_s {
     int co_tiles, ksteps, cout_pad;
     void *w_dev;
     int32_t *epi_dev;  // [num_levels][EPI_FIELDS][cout_pad]
+    int32_t *lut_dev;  // code skips: [num_levels][cout_pad][2^skip_bits] RSM(k, c, d), else null
     std::vector<int> fast;  // per level: every shift >= 2
     std::vector<int> side0; // per level: every skip side is 0
     const uint8_t *zero;    // the device's zero page
@@ -273,6 +274,25 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
         }
     }
 
+    // code skips: per level and channel the skip operand's scaled value
+    // RSM(k, c, d) for every code k (used when every side of the level is 0),
+    // computed exactly and kept modulo 2^32 as the kernels' 32-bit sums are
+    std::vector<int32_t> lut;
+    const int nk = (d.skip_bits > 0 && d.skip_bits < 32) ? (1 << d.skip_bits) : 0;
+    if (nk) {
+        lut.assign((size_t)d.num_levels * h.cout_pad * nk, 0);
+        for (int l = 0; l < d.num_levels; ++l)
+            for (int c = 0; c < d.cout; ++c) {
+                const long long cc = levels[l].skip_c[c];
+                const int dd = levels[l].skip_d[c];
+                for (int k = 0; k < nk; ++k) {
+                    const long long p = (long long)k * cc;
+                    const long long r = dd > 0 ? (p + (1LL << (dd - 1))) >> dd : p;
+                    lut[((size_t)l * h.cout_pad + c) * nk + k] = (int32_t)(uint32_t)(uint64_t)r;
+                }
+            }
+    }
+
     const char *inject = std::getenv("AQD_FAULT_INJECT");
     if (inject && std::strcmp(inject, "alloc") == 0)
         return fail(AQD_ERR_NOMEM, "device allocation failed (injected)");
@@ -292,11 +312,22 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
         delete hp;
         return fail(AQD_ERR_NOMEM, "hipMalloc of the epilogue tables failed");
     }
-    if (hipMemcpy(hp->w_dev, wbuf.data(), wbuf.size(), hipMemcpyHostToDevice) != hipSuccess ||
-        hipMemcpy(hp->epi_dev, epi.data(), epi.size() * sizeof(int32_t), hipMemcpyHostToDevice) !=
-            hipSuccess) {
+    hp->lut_dev = nullptr;
+    if (nk && hipMalloc((void **)&hp->lut_dev, lut.size() * sizeof(int32_t)) != hipSuccess) {
         (void)hipFree(hp->w_dev);
         (void)hipFree(hp->epi_dev);
+        delete hp;
+        return fail(AQD_ERR_NOMEM, "hipMalloc of the skip tables failed");
+    }
+    if (hipMemcpy(hp->w_dev, wbuf.data(), wbuf.size(), hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(hp->epi_dev, epi.data(), epi.size() * sizeof(int32_t), hipMemcpyHostToDevice) !=
+            hipSuccess ||
+        (nk && hipMemcpy(hp->lut_dev, lut.data(), lut.size() * sizeof(int32_t), hipMemcpyHostToDevice) !=
+                   hipSuccess)) {
+        (void)hipFree(hp->w_dev);
+        (void)hipFree(hp->epi_dev);
+        if (hp->lut_dev)
+            (void)hipFree(hp->lut_dev);
         delete hp;
         return fail(AQD_ERR_DEVICE, "copy of the weights to the device failed");
     }
@@ -310,6 +341,8 @@ void qconv_destroy(qconv_t conv)
         return;
     (void)hipFree(conv->w_dev);
     (void)hipFree(conv->epi_dev);
+    if (conv->lut_dev)
+        (void)hipFree(conv->lut_dev);
     delete conv;
 }
 
@@ -489,6 +522,8 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         m.tile_begin = tiles;
         m.fast = s.conv->fast[s.level];
         m.side0 = s.conv->side0[s.level];
+        m.lut = s.conv->lut_dev ? s.conv->lut_dev + (size_t)s.level * s.conv->cout_pad * (1 << h0.d.skip_bits)
+                                : nullptr;
         const long long px_tiles = (m.P + blk_px - 1) / blk_px;
         REQUIRE(tiles + px_tiles * h0.co_tiles < (1LL << 26), "too many tiles for one launch");
         tiles += (int)(px_tiles * h0.co_tiles);

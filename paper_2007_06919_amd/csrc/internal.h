@@ -39,6 +39,7 @@ struct MfmaSeg {
     int tile_begin;      // first workgroup tile of this segment
     int fast;            // every shift of the level >= 2: 32-bit requantisation
     int side0;           // every skip side of the level is 0 (code skips use a table)
+    const int32_t *lut;  // code skips: [cout_pad][2^bits] RSM(k, c, d) of the level
     // projection shortcut (fused launch only): 1x1 conv of x2 whose int32 output is the skip
     const uint8_t *x2;   // [n][h2][w2][cin2] codes
     const int8_t *wt2;   // its weight tiles (same tile layout)

@@ -532,19 +532,28 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
             }
         }
     });
+    // every skip operand is a b-bit code scaled by c / 2^d (side 0): the
+    // channel tile's table of RSM(k, c, d) (built at create) goes to LDS too
+    constexpr int LUT_PER = SKK == 1 ? (C::BCO * (QMAX + 1) + NT - 1) / NT : 1;
+    int lut_r[LUT_PER];
+    if (use_lut) {
+#pragma unroll
+        for (int t = 0; t < LUT_PER; ++t) {
+            const int i = tid + t * NT;
+            lut_r[t] = i < C::BCO * (QMAX + 1) ? S.lut[co_tile * C::BCO * (QMAX + 1) + i] : 0;
+        }
+    }
     __syncthreads();  // every wave is done with the ring
 #pragma unroll
     for (int t = 0; t < PRM_PER; ++t)
         prm[tid + t * NT] = prm_r[t];
-    __syncthreads();
     if (use_lut) {
-        // every skip operand is a b-bit code scaled by c / 2^d (side 0): tabulate
-        for (int i = tid; i < C::BCO * (QMAX + 1); i += NT) {
-            const int cl = i >> BI;
-            lut[i] = rsm32(i & QMAX, prm[EPI_SKIP_C * C::BCO + cl], prm[EPI_SKIP_D * C::BCO + cl]);
-        }
-        __syncthreads();
+#pragma unroll
+        for (int t = 0; t < LUT_PER; ++t)
+            if (tid + t * NT < C::BCO * (QMAX + 1))
+                lut[tid + t * NT] = lut_r[t];
     }
+    __syncthreads();
 
     // int32 tiles (outputs, int32 skips) move between HBM and registers through
     // a per-wave LDS staging area, JP column tiles (16 JP pixel rows) at a time,
