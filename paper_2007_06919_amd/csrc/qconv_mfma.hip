@@ -71,15 +71,25 @@ __device__ __forceinline__ void static_for(F &&f)
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 
-// round(a * c / 2^d), ties up, d in [0, 31], result assumed to fit in int32
+// round(a * c / 2^d), ties up, d in [0, 31], result modulo 2^32: one 64-bit
+// multiply-add (exact: |a*c| < 2^62) and a funnel shift
 __device__ __forceinline__ int rsm32(int a, int c, int d)
 {
-    const unsigned lo = (unsigned)a * (unsigned)c;
-    const int hi = __mulhi(a, c);
-    const unsigned r = d > 0 ? (1u << (d - 1)) : 0u;
-    const unsigned lo2 = lo + r;
-    const unsigned hi2 = (unsigned)hi + (lo2 < lo ? 1u : 0u);
-    return (int)__builtin_amdgcn_alignbit(hi2, lo2, (unsigned)d);
+    const long long t = (long long)a * c + (d > 0 ? (1LL << (d - 1)) : 0LL);
+    return (int)__builtin_amdgcn_alignbit((unsigned)((unsigned long long)t >> 32), (unsigned)t, (unsigned)d);
+}
+
+// Requantisation of u with shift >= 2, before the clamp: with d = 31 + shift,
+// floor((u*M + 2^(d-1)) / 2^d) = (high word of u*M + 2^(d-33) * 2^32) >> (d - 32),
+// the high word taken exactly from one 64-bit multiply-add (rnd = 2^(shift-2),
+// shr = shift - 1).
+// (written as one v_mad_i64_i32: left to itself the compiler splits it into a
+// high multiply and an add)
+__device__ __forceinline__ int requant32(int u, int m, long long rnd_hi, int shr)
+{
+    long long t;
+    asm("v_mad_i64_i32 %0, vcc, %1, %2, %3" : "=v"(t) : "v"(u), "v"(m), "v"(rnd_hi) : "vcc");
+    return (int)(t >> 32) >> shr;
 }
 
 
@@ -622,10 +632,11 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
             const int4 s4 = *(const int4 *)(prm + (FAST ? EPI_SHR : EPI_SHIFT) * C::BCO + cl);
             const int mult[4] = {m4.x, m4.y, m4.z, m4.w};
             const int shf[4] = {s4.x, s4.y, s4.z, s4.w};
-            int rnd[4] = {0, 0, 0, 0};
+            long long rnd[4] = {0, 0, 0, 0};  // 2^(shift-2) in the high word
             if constexpr (FAST) {
                 const int4 r4 = *(const int4 *)(prm + EPI_RND * C::BCO + cl);
-                rnd[0] = r4.x; rnd[1] = r4.y; rnd[2] = r4.z; rnd[3] = r4.w;
+                rnd[0] = (long long)r4.x << 32; rnd[1] = (long long)r4.y << 32;
+                rnd[2] = (long long)r4.z << 32; rnd[3] = (long long)r4.w << 32;
             }
             int sc[4] = {0, 0, 0, 0}, sd[4] = {0, 0, 0, 0}, sside[4] = {0, 0, 0, 0};
             if constexpr (SKK != 0 && !LUT) {
@@ -670,7 +681,7 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
                             const int scaled = rsm32(sside[e] ? v : kv[e], sc[e], sd[e]);
                             u = (int)((unsigned)scaled + (unsigned)(sside[e] ? kv[e] : v));
                         }
-                        y = (__mulhi(u, mult[e]) + rnd[e]) >> shf[e];
+                        y = requant32(u, mult[e], rnd[e], shf[e]);
                         y = y < 0 ? 0 : (y > QMAX ? QMAX : y);
                     } else {
                         long long u = v;
