@@ -481,8 +481,10 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         return AQD_OK;
     MfmaArgs &a = *out;
     a = MfmaArgs{};
-    // launch tile for a handle laid out for 256-channel tiles: short K ranges with
-    // code outputs run on 256 x 64 tiles three to a CU; launches with fewer
+    // launch tile for a handle laid out for 256-channel tiles: 1x1 convolutions
+    // with cin <= 128 and code outputs on persistent 256 x 64 tiles (weights kept
+    // in LDS, next tile's copies during the current epilogue); other short K
+    // ranges with code outputs on 256 x 64 tiles three to a CU; launches with fewer
     // 256 x 128 tiles than CUs (but not tiny, and not so long in K that
     // splitting K is the better cure) on 256 x 64 tiles two to a CU (measured:
     // from ~260 tiles on, the larger tile is faster)
@@ -491,8 +493,13 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         long long t128 = 0;
         for (int i = 0; i < count; ++i)
             t128 += ((long long)segs[i].n * chk[i].ho * chk[i].wo + 127) / 128 * h0.co_tiles;
-        if (h0.ksteps <= 4 && h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_in == 4 &&
-            (h0.d.skip_bits == 0 || h0.d.skip_bits == 4)) {
+        const bool short_codes = h0.ksteps <= 4 && h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_in == 4 &&
+                                 (h0.d.skip_bits == 0 || h0.d.skip_bits == 4);
+        if (short_codes && h0.ksteps <= 2 && h0.d.kh == 1 && h0.d.kw == 1 && h0.d.pad == 0 &&
+            h0.d.cout % 256 == 0) {
+            tile_cfg = TILE_STREAM;
+            blk_px = 64;
+        } else if (short_codes) {
             tile_cfg = TILE_256x64S;
             blk_px = 64;
         } else if (t128 >= 64 && t128 < 200 && h0.ksteps <= 80) {
@@ -559,7 +566,7 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
 // when the model gains 20%.
 void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
 {
-    if (a.tile_cfg == TILE_256x64S || a.tile_cfg == TILE_256x64) {  // already balanced: never split
+    if (a.tile_cfg == TILE_256x64S || a.tile_cfg == TILE_256x64 || a.tile_cfg == TILE_STREAM) {  // never split
         *nparts = 1;
         *kchunk = a.ksteps;
         return;

@@ -14,7 +14,8 @@ namespace aqd {
 enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
        // launch-time choices for handles laid out for 256x128 (same weight layout):
        TILE_256x64S = 3,   // short K, code outputs: three workgroups per CU
-       TILE_256x64 = 4 };  // launches with too few 256x128 tiles to fill the GPU
+       TILE_256x64 = 4,    // launches with too few 256x128 tiles to fill the GPU
+       TILE_STREAM = 5 };  // 1x1, cin <= 128, code outputs: persistent 256 x 64 tiles
 constexpr int KC = 64;
 
 // tile shape of a configuration, and the channels one lane holds per pixel

@@ -745,6 +745,269 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
     });
 }
 
+// ------------------------------------------------------------------ streaming
+// 1x1 convolutions with at most ST_KMAX K steps (cin <= 128), 4-bit code
+// outputs and no skip or a code skip: per 256 x 64 tile the matrix cores have
+// little to do, and a workgroup that does one tile spends its time waiting for
+// its copies and in the epilogue. This persistent variant runs two
+// workgroups per CU; each keeps its channel tile's weights (every K step) in
+// LDS and walks over pixel tiles, copying the activation codes and skip codes
+// of its next tile into the other half of a double buffer while the current
+// tile's MFMAs and epilogue run. Everything a tile's epilogue reads (table,
+// skip table, skip codes) is in LDS, so that the only waits for global memory
+// are the explicit ones at the top of each tile.
+constexpr int ST_KMAX = 2;
+
+template <int SKK, int FAST>
+__global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
+{
+    constexpr int BI = 4, MI = 8, NJ = 2, WPC = 2, NT = 256;
+    constexpr int TM = 128, TN = 32, BCO = 256, BPX = 64, PB = KC * BI / 8;
+    constexpr int CPL = 4 * MI, OW = CPL * BI / 32, QMAX = (1 << BI) - 1;
+    constexpr int A_STEP = BCO * KC;               // int8 weight rows of one K step (16 KiB)
+    constexpr int B_STEP = BPX * PB;               // packed codes of one K step (2 KiB)
+    constexpr int SK_TILE = BPX * BCO * BI / 8;    // skip codes of one tile (8 KiB)
+    constexpr int OFF_B = ST_KMAX * A_STEP;
+    constexpr int OFF_S = OFF_B + 2 * ST_KMAX * B_STEP;
+    constexpr int OFF_P = OFF_S + (SKK ? 2 * SK_TILE : 0);
+    constexpr int OFF_L = OFF_P + EPI_FIELDS * BCO * 4;
+    constexpr int LDS_BYTES = OFF_L + (SKK ? BCO * (QMAX + 1) * 4 : 0);
+    static_assert(LDS_BYTES <= 81920, "two workgroups per CU");
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS_BYTES];
+    int32_t *prm = (int32_t *)(lds + OFF_P);
+    int32_t *lut = (int32_t *)(lds + OFF_L);       // [BCO][2^BI]: RSM(k, c, d)
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wc = wave / WPC, wp = wave % WPC;
+    const int g = lane >> 4;
+    // workgroup -> channel tile (fixed) and a stride-nstream walk over the
+    // pixel tiles of every segment
+    const int co_tile = blockIdx.x % A.co_tiles;
+    const int nstream = gridDim.x / A.co_tiles;
+    const int qtiles = A.total_tiles / A.co_tiles;
+    const int K = A.ksteps;
+    const uint32_t lbase = lds_addr(lds);
+
+    auto seg_of = [&](int q) {
+        int s = 0;
+#pragma unroll
+        for (int i = 1; i < AQD_MAX_SEGS; ++i)
+            if (i < A.nseg && q * A.co_tiles >= A.seg[i].tile_begin)
+                s = i;
+        return s;
+    };
+
+    // copies of pixel tile q into buffer b: K steps of codes (wave w: pixels
+    // 16w .. 16w+15, 32 lanes, swizzled halves as in the main kernel) and the
+    // tile's skip codes (128 B per pixel, 16-byte chunk c of pixel p at
+    // position c ^ (p & 7))
+    auto issue_tile = [&](int q, int b) {
+        const MfmaSeg &S = A.seg[seg_of(q)];
+        const int pq = q - S.tile_begin / A.co_tiles;
+        const int hw = S.ho * S.wo;
+        {
+            const int ploc = 16 * wave + (lane >> 1);
+            const long long p = (long long)pq * BPX + ploc;
+            const uint8_t *src = nullptr;
+            if (p < S.P) {  // P < 2^31 (host): 32-bit index arithmetic
+                const int n_ = (int)p / hw;
+                const int rem = (int)p - n_ * hw;
+                const int oh = rem / S.wo, ow = rem - oh * S.wo;
+                src = S.x + (((long long)n_ * S.h + oh * A.stride) * S.w + ow * A.stride) * (A.cin * BI / 8) +
+                      16 * ((lane & 1) ^ swz_b4(ploc));
+            }
+            for (int k = 0; k < K; ++k)
+                if (lane < 32)
+                    dma16(src ? src + k * PB : A.zero, lbase + OFF_B + (b * ST_KMAX + k) * B_STEP + wave * 512);
+        }
+        if constexpr (SKK == 1) {
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const int ploc = (2 * wave + c) * 8 + (lane >> 3);
+                const long long p = (long long)pq * BPX + ploc;
+                const uint8_t *src = A.zero;
+                if (p < S.P) {
+                    long long spix = p;
+                    if (A.up2) {
+                        const int n_ = (int)p / hw;
+                        const int rem = (int)p - n_ * hw;
+                        const int oh = rem / S.wo, ow = rem - oh * S.wo;
+                        spix = ((long long)n_ * S.hs + (oh >> 1)) * S.ws + (ow >> 1);
+                    }
+                    src = (const uint8_t *)S.skip + spix * (A.cout * BI / 8) + co_tile * (BCO * BI / 8) +
+                          16 * ((lane & 7) ^ (ploc & 7));
+                }
+                dma16(src, lbase + OFF_S + b * SK_TILE + (2 * wave + c) * 1024);
+            }
+        }
+    };
+
+    // fragment addresses (the main kernel's swizzles)
+    const int a_off = (wc * TM + (lane & 15)) * KC + 16 * ((lane >> 4) ^ swz_a(lane & 15));
+    const int b_off = OFF_B + (wp * TN + (lane & 15)) * PB + 8 * ((lane >> 4) ^ (swz_b4(lane & 15) << 1));
+    const int co_loc = wc * TM + CPL * g;           // first of this lane's CPL channels (in the tile)
+    const int co_glob = co_tile * BCO + co_loc;
+
+    int q = blockIdx.x / A.co_tiles;
+    int cur = -1, buf = 0;
+    if (q < qtiles)
+        issue_tile(q, 0);
+    for (; q < qtiles; q += nstream, buf ^= 1) {
+        const int s = seg_of(q);
+        const MfmaSeg &S = A.seg[s];
+        wait_vmcnt<0>();   // this tile's copies (and the last tile's stores) are done
+        __syncthreads();   // ... for every wave, and every wave is done with the last tile
+        if (s != cur) {
+            // the segment's weights (every K step) and tables
+            for (int k = 0; k < K; ++k)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const int row = 16 * (4 * t + wave) + (lane >> 2);
+                    dma16(S.wt + ((long long)co_tile * A.ksteps + k) * A_STEP + row * KC +
+                              16 * ((lane & 3) ^ swz_a(row)),
+                          lbase + k * A_STEP + (4 * t + wave) * 1024);
+                }
+#pragma unroll
+            for (int t = 0; t < EPI_FIELDS * BCO / NT; ++t) {
+                const int i = tid + t * NT;
+                const int which = i / BCO, c = i - which * BCO;
+                prm[i] = S.epi[which * A.cout_pad + co_tile * BCO + c];
+            }
+            if (SKK == 1 && S.side0) {
+#pragma unroll
+                for (int t = 0; t < BCO * (QMAX + 1) / NT; ++t)
+                    lut[tid + t * NT] = S.lut[co_tile * BCO * (QMAX + 1) + tid + t * NT];
+            }
+            wait_vmcnt<0>();
+            __syncthreads();
+            cur = s;
+        }
+        if (q + nstream < qtiles)
+            issue_tile(q + nstream, buf ^ 1);
+
+        // MFMAs: accumulators start at the bias (v = acc + bias)
+        v4i acc[MI][NJ];
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            const v4i b = *(const v4i *)(prm + EPI_BIAS * BCO + co_loc + 4 * i);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+                acc[i][j] = b;
+        }
+#pragma unroll
+        for (int k = 0; k < ST_KMAX; ++k) {
+            if (k < K) {
+                v4i fa[MI];
+                uint2 fb[NJ];
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    fb[j] = *(const uint2 *)(lds + b_off + (buf * ST_KMAX + k) * B_STEP + j * 16 * PB);
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+                    fa[i] = *(const v4i *)(lds + k * A_STEP + a_off + i * 16 * KC);
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    const uint2 w = fb[j];
+                    const v4i bj = v4i{(int)(w.x & 0x0F0F0F0Fu), (int)((w.x >> 4) & 0x0F0F0F0Fu),
+                                       (int)(w.y & 0x0F0F0F0Fu), (int)((w.y >> 4) & 0x0F0F0F0Fu)};
+#pragma unroll
+                    for (int i = 0; i < MI; ++i)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], bj, acc[i][j], 0, 0, 0);
+                }
+            }
+        }
+
+        // epilogue
+        const int pq = q - S.tile_begin / A.co_tiles;
+        const long long px0 = (long long)pq * BPX + wp * TN + (lane & 15);
+        const bool co_ok = co_glob < A.cout;
+        const bool use_lut = SKK == 1 && S.side0;
+        uint32_t outw[NJ][OW];
+        uint32_t skw[NJ][OW];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+#pragma unroll
+            for (int u = 0; u < OW; ++u)
+                outw[j][u] = skw[j][u] = 0;
+            if constexpr (SKK == 1) {
+                const int ploc = wp * TN + j * 16 + (lane & 15);
+                const uint4 t = *(const uint4 *)(lds + OFF_S + buf * SK_TILE + ploc * (BCO * BI / 8) +
+                                                 16 * ((wc * 4 + g) ^ (ploc & 7)));
+                skw[j][0] = t.x;
+                skw[j][1] = t.y;
+                skw[j][2] = t.z;
+                skw[j][3] = t.w;
+            }
+        }
+        auto body = [&](auto lut_c) {
+            constexpr bool LUT = decltype(lut_c)::value;
+            static_for<MI>([&](auto ic) {
+                constexpr int i = decltype(ic)::value;
+                const int cl = co_loc + 4 * i;
+                const int4 m4 = *(const int4 *)(prm + EPI_MULT * BCO + cl);
+                const int4 s4 = *(const int4 *)(prm + (FAST ? EPI_SHR : EPI_SHIFT) * BCO + cl);
+                const int mult[4] = {m4.x, m4.y, m4.z, m4.w};
+                const int shf[4] = {s4.x, s4.y, s4.z, s4.w};
+                long long rnd[4] = {0, 0, 0, 0};
+                if constexpr (FAST) {
+                    const int4 r4 = *(const int4 *)(prm + EPI_RND * BCO + cl);
+                    rnd[0] = (long long)r4.x << 32; rnd[1] = (long long)r4.y << 32;
+                    rnd[2] = (long long)r4.z << 32; rnd[3] = (long long)r4.w << 32;
+                }
+                int sc[4] = {0, 0, 0, 0}, sd[4] = {0, 0, 0, 0}, sside[4] = {0, 0, 0, 0};
+                if constexpr (SKK != 0 && !LUT) {
+                    const int4 c4 = *(const int4 *)(prm + EPI_SKIP_C * BCO + cl);
+                    const int4 d4 = *(const int4 *)(prm + EPI_SKIP_D * BCO + cl);
+                    const int4 e4 = *(const int4 *)(prm + EPI_SKIP_SIDE * BCO + cl);
+                    sc[0] = c4.x; sc[1] = c4.y; sc[2] = c4.z; sc[3] = c4.w;
+                    sd[0] = d4.x; sd[1] = d4.y; sd[2] = d4.z; sd[3] = d4.w;
+                    sside[0] = e4.x; sside[1] = e4.y; sside[2] = e4.z; sside[3] = e4.w;
+                }
+                static_for<NJ>([&](auto jc) {
+                    constexpr int j = decltype(jc)::value;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int v = acc[i][j][e];  // acc + bias
+                        const int bit = (4 * i + e) * BI;
+                        const int kv = SKK == 1 ? (int)((skw[j][bit >> 5] >> (bit & 31)) & QMAX) : 0;
+                        int y;
+                        if constexpr (FAST) {
+                            int u = v;
+                            // u fits in int32, so the sum modulo 2^32 is exact
+                            if constexpr (LUT) {
+                                u = (int)((unsigned)v + (unsigned)lut[((cl + e) << BI) | kv]);
+                            } else if constexpr (SKK != 0) {
+                                const int scaled = rsm32(sside[e] ? v : kv, sc[e], sd[e]);
+                                u = (int)((unsigned)scaled + (unsigned)(sside[e] ? kv : v));
+                            }
+                            y = requant32(u, mult[e], rnd[e], shf[e]);
+                            y = y < 0 ? 0 : (y > QMAX ? QMAX : y);
+                        } else {
+                            long long u = v;
+                            if constexpr (LUT)
+                                u = (int)((unsigned)v + (unsigned)lut[((cl + e) << BI) | kv]);
+                            else if constexpr (SKK != 0)
+                                u = align_add(v, kv, sc[e], sd[e], sside[e]);
+                            y = (int)requant_clamp(u, mult[e], shf[e], QMAX);
+                        }
+                        outw[j][bit >> 5] |= (uint32_t)y << (bit & 31);
+                    }
+                });
+            });
+        };
+        if (use_lut)
+            body(std::true_type{});
+        else
+            body(std::false_type{});
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+            if (co_ok && px0 + j * 16 < S.P)
+                store_words<OW>((uint8_t *)S.y + (px0 + j * 16) * (A.cout * BI / 8) + co_glob * BI / 8, outw[j]);
+    }
+}
+
 template <int BI, int MI, int NJ, int WC, int WP, int OUTK, int SKK>
 hipError_t launch_t(const MfmaArgs &a, hipStream_t stream)
 {
@@ -782,7 +1045,8 @@ void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane)
     switch (tile_cfg) {
     case TILE_256x128: *blk_co = 256; *blk_px = 128; *chan_per_lane = 32; return;
     case TILE_256x64S:
-    case TILE_256x64: *blk_co = 256; *blk_px = 64; *chan_per_lane = 32; return;
+    case TILE_256x64:
+    case TILE_STREAM: *blk_co = 256; *blk_px = 64; *chan_per_lane = 32; return;
     case TILE_128x256: *blk_co = 128; *blk_px = 256; *chan_per_lane = 16; return;
     default: *blk_co = 64; *blk_px = 512; *chan_per_lane = 16; return;
     }
@@ -813,6 +1077,35 @@ hipError_t launch_qconv_short(const MfmaArgs &a, hipStream_t stream)
     return hipGetLastError();
 }
 
+// streaming 256 x 64 tiles: two persistent workgroups per CU (a multiple of
+// the channel tiles, each workgroup on one channel tile)
+hipError_t launch_qconv_stream(const MfmaArgs &a, hipStream_t stream)
+{
+    if (a.ksteps > ST_KMAX || a.bits_out != 4 || (a.skip_bits != 0 && a.skip_bits != 4) || a.kh != 1 ||
+        a.kw != 1 || a.pad != 0 || a.cout % 256 != 0 || a.co_tiles < 1 || a.co_tiles > 256)
+        return hipErrorInvalidValue;
+    const int qtiles = a.total_tiles / a.co_tiles;
+    if (qtiles <= 0)
+        return hipSuccess;
+    const int nstream = qtiles < 512 / a.co_tiles ? qtiles : 512 / a.co_tiles;
+    dim3 grid(nstream * a.co_tiles), block(256);
+    bool fast = true;
+    for (int i = 0; i < a.nseg; ++i)
+        fast = fast && a.seg[i].fast;
+    if (a.skip_bits == 0) {
+        if (fast)
+            hipLaunchKernelGGL((qconv_stream_kernel<0, 1>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_stream_kernel<0, 0>), grid, block, 0, stream, a);
+    } else {
+        if (fast)
+            hipLaunchKernelGGL((qconv_stream_kernel<1, 1>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_stream_kernel<1, 0>), grid, block, 0, stream, a);
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_qconv_proj(const MfmaArgs &a, hipStream_t stream)
 {
     // 256 x 64 tiles (two accumulator sets per wave), the 256-channel weight layout
@@ -837,6 +1130,7 @@ hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
         case TILE_256x128: return launch_modes<4, 8, 4, 2, 2>(a, stream);
         case TILE_256x64S: return launch_qconv_short(a, stream);
         case TILE_256x64: return launch_modes<4, 8, 2, 2, 2>(a, stream);
+        case TILE_STREAM: return launch_qconv_stream(a, stream);
         case TILE_128x256: return launch_modes<4, 4, 8, 2, 2>(a, stream);
         case TILE_64x512: return launch_modes<4, 4, 8, 1, 4>(a, stream);
         }

@@ -110,6 +110,80 @@ def test_split_k_not_used_for_full_launches(torch):
         aqd.qconv_destroy(h)
 
 
+# 1x1 convolutions with cin <= 128, code outputs and cout a multiple of 256
+# run on persistent 256 x 64 tiles (weights kept in LDS, the next tile's
+# copies overlapping the current epilogue): ragged tails, several channel
+# tiles, code skips with and without the upsample, stride 2, several tiles
+# per workgroup.
+STREAM_CASES = [
+    # (n, h, w, cin, cout, k, stride, bits_in, bits_w, wenc, bits_out, skip_bits, up2)
+    (2, 41, 52, 64, 256, 1, 1, 4, 4, 1, 4, 4, False),       # 1 K step, code skip
+    (1, 33, 37, 128, 512, 1, 1, 4, 4, 0, 4, 4, False),      # 2 K steps, 2 channel tiles
+    (2, 16, 18, 64, 256, 1, 1, 4, 4, 0, 4, 4, True),        # upsampled code skip
+    (1, 25, 21, 128, 256, 1, 2, 4, 4, 1, 4, 0, False),      # stride 2, no skip
+    (8, 120, 161, 64, 256, 1, 1, 4, 4, 1, 4, 4, False),     # ~4.7 tiles per workgroup
+    (3, 70, 90, 128, 768, 1, 1, 4, 4, 0, 4, 4, False),      # 3 channel tiles, 2 tiles per workgroup
+]
+
+
+@pytest.mark.parametrize("case", STREAM_CASES, ids=lambda c: "x".join(map(str, c)))
+@pytest.mark.parametrize("variant", ["random_sides", "side0", "small_shifts"])
+def test_conv_stream_parity(torch, case, variant):
+    """Per-channel skip sides (64-bit-free alignment), all sides 0 (the skip
+    table), and shifts < 2 (64-bit requantisation)."""
+    n, h, w, cin, cout, k, s, bi, bw, wenc, bo, sb, up2 = case
+    c = workloads.random_conv_case(seed=hash(case) % 1000 + 21, n=n, h=h, w=w, cin=cin, cout=cout,
+                                   k=k, stride=s, bits_in=bi, bits_w=bw, wenc=wenc, bits_out=bo,
+                                   skip_bits=sb, skip_up2=up2)
+    rng = np.random.Generator(np.random.PCG64(17))
+    for lv in c.levels:
+        if variant == "side0" and sb:
+            lv["skip_side"][:] = 0
+        if variant == "small_shifts":
+            lv["shift"] = rng.integers(-2, 2, size=cout).astype(np.int32)
+            lv["mult"] = rng.integers(1 << 24, 1 << 27, size=cout).astype(np.int32)
+    for level, got in enumerate(gpu_conv(c, torch)):
+        assert_same(got, oracle_conv(c, level), f"stream {variant} {case} level {level}")
+
+
+def test_stream_grouped_segments(torch):
+    """One launch over segments of two handles (weights and tables reloaded at
+    each segment change) and two levels, with code skips."""
+    dev = torch.device("cuda:0")
+    sizes = [(40, 57), (20, 29), (10, 15)]
+    cases = [workloads.random_conv_case(seed=60 + t, n=2, h=40, w=57, cin=64, cout=256, k=1,
+                                        bits_in=4, bits_w=4, wenc=1, bits_out=4, skip_bits=4,
+                                        num_levels=2)
+             for t in range(2)]
+    handles = [aqd.qconv_create(64, 256, 1, 1, 0, 4, 4, aqd.pack_codes(c.w_fields, 4), c.levels,
+                                wenc=1, bits_out=4, skip_bits=4) for c in cases]
+    rng = np.random.Generator(np.random.PCG64(19))
+    try:
+        segs, expect, outs = [], [], []
+        for t, c in enumerate(cases):
+            for i, (h, w) in enumerate(sizes):
+                lv = i % 2
+                x = rng.integers(0, 16, size=(2, h, w, 64))
+                sk = rng.integers(0, 16, size=(2, h, w, 256))
+                xd = torch.from_numpy(aqd.pack_codes(x, 4)).to(dev)
+                sd = torch.from_numpy(aqd.pack_codes(sk, 4)).to(dev)
+                yd = torch.zeros((2, h, w, 128), dtype=torch.uint8, device=dev)
+                segs.append((handles[t], lv, 2, h, w, xd, sd, h, w, yd))
+                outs.append(yd)
+                L = c.levels[lv]
+                want = ref.qconv(x, c.w_fields, 4, 1, 0, L["bias"], wenc=1, mult=L["mult"],
+                                 shift=L["shift"], bits_out=4, skip=sk, skip_c=L["skip_c"],
+                                 skip_d=L["skip_d"], skip_side=L["skip_side"])
+                expect.append(ref.pack_codes(want, 4))
+        aqd.qconv_run_group(segs)
+        torch.cuda.synchronize()
+        for i, (yd, want) in enumerate(zip(outs, expect)):
+            assert_same(yd.cpu().numpy(), want, f"segment {i}")
+    finally:
+        for h in handles:
+            aqd.qconv_destroy(h)
+
+
 DIRECT_CASES = [
     (1, 9, 10, 32, 16, 3, 1, 4, 4, 0, 4, 0, False),         # cin not a multiple of 64
     (2, 8, 7, 16, 12, 3, 2, 8, 4, 0, 8, 0, False),          # 8-bit activations
