@@ -3,10 +3,11 @@
 800 x 1333 images) on one MI355X, through the C ABI.
 
 One step = one forward pass of all 110 convolution segments over the batch
-(grouped launches on one HIP stream), inputs resident in HBM. The dominant
-kernel is the grouped head-tower launch (3x3, 256 -> 256, class and box
-towers, five pyramid levels, eight images); HIP events on the launch stream
-bracket each of its launches inside the timed region.
+(grouped launches on one HIP stream, recorded once into a HIP graph and
+replayed), inputs resident in HBM. The dominant kernel is the grouped
+head-tower launch (3x3, 256 -> 256, class and box towers, five pyramid
+levels, eight images); a second timed pass enqueues the same steps launch by
+launch, with HIP events on the launch stream around each head-tower launch.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -123,19 +124,34 @@ def main():
         for _ in range(args.warmup):
             gpu.forward(stream)
         stream.synchronize()
+        # the whole network recorded once into a HIP graph; a step = one replay
+        gpu.capture(stream)
+        for _ in range(args.warmup):
+            gpu.replay()
+        stream.synchronize()
         torch.cuda.synchronize()
         start = torch.cuda.Event(enable_timing=True)
         end = torch.cuda.Event(enable_timing=True)
         wall0 = time.perf_counter()
         start.record(stream)
         for _ in range(args.steps):
-            gpu.forward(stream, launch_hook=hook)
+            gpu.replay()
         end.record(stream)
         stream.synchronize()
         torch.cuda.synchronize()
         wall = time.perf_counter() - wall0
+        # the same steps launch by launch, with events around the dominant launch
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            gpu.forward(stream, launch_hook=hook)
+        e1.record(stream)
+        stream.synchronize()
+        torch.cuda.synchronize()
     ms_total = start.elapsed_time(end)
     ms_step = ms_total / args.steps
+    eager_ms_step = e0.elapsed_time(e1) / args.steps
     value = total_ops / (ms_step / 1e3) / 1e12
 
     durs, ops = [], []
@@ -147,7 +163,8 @@ def main():
     avg_ms = float(np.mean(durs))
     avg_ops = float(np.mean(ops))
     achieved = avg_ops / (avg_ms / 1e3) / 1e12
-    log(f"[bench] {ms_step:.3f} ms/step (wall {wall / args.steps * 1e3:.3f} ms), "
+    log(f"[bench] {ms_step:.3f} ms/step as a graph replay (wall {wall / args.steps * 1e3:.3f} ms; "
+        f"{eager_ms_step:.3f} ms launch by launch), "
         f"{value:.1f} int TOPS; head-tower launch {avg_ms * 1e3:.1f} us, {achieved:.1f} TOPS")
 
     out = {
@@ -157,8 +174,10 @@ def main():
         "dtype": "i8", "data": "synthetic",
         "config": {"workload": workloads.CONFIG_NAMES[4], "batch": n_img, "image": [800, 1333],
                    "bits": 4, "conv_segments": sum(len(c.segs) for c in net.convs),
-                   "launches_per_step": gpu.launches_per_forward(), "int_ops_per_step": total_ops},
+                   "launches_per_step": gpu.launches_per_forward(), "int_ops_per_step": total_ops,
+                   "hip_graph": True},
         "ms_per_image": round(ms_step / n_img, 4),
+        "eager_ms_per_step": round(eager_ms_step, 4),
         "roofline": {"bound": "mfma",
                      "kernel": "qconv_mfma_kernel<4,8,4,2,2,0,0,1,0> (head towers 3x3 256->256, "
                                "10 segments, 256x128 tiles)",

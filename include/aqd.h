@@ -239,6 +239,28 @@ aqd_status_t qadd_run(const qadd_desc_t *desc, const void *a, const void *b, voi
 aqd_status_t aqd_channel_sums(const int32_t *v, int64_t rows, int c, int64_t *sums,
                               aqd_stream_t stream);
 
+/* Whole-network capture: the launches a network pass enqueues on one stream
+ * (each a grouped convolution of Sec. 3.2.2's multi-level tables, a fused
+ * shortcut or a split K range) are recorded once into a HIP graph and
+ * replayed as one launch.
+ * aqd_graph_begin: starts capturing `stream` (not the null stream, not a
+ *   stream already capturing), in thread-local mode: until aqd_graph_end,
+ *   calls of this library from the calling thread on that stream are
+ *   recorded, not run. qconv_run, qconv_run_group(_ws), qconv_run_proj,
+ *   qadd_run and aqd_channel_sums allocate nothing and may be recorded.
+ * aqd_graph_end: ends the capture and instantiates the graph; *graph_exec
+ *   receives the executable graph (owned by the caller, freed by
+ *   aqd_graph_destroy), or NULL with AQD_ERR_DEVICE if the capture failed.
+ * aqd_graph_launch: enqueues one replay on `stream`; the device pointers and
+ *   argument values recorded at capture are used again, so the tensors must
+ *   still be allocated (their contents may change between replays).
+ * aqd_graph_destroy: frees an executable graph (NULL is ignored); no replay
+ *   of it may be pending. */
+aqd_status_t aqd_graph_begin(aqd_stream_t stream);
+aqd_status_t aqd_graph_end(aqd_stream_t stream, void **graph_exec);
+aqd_status_t aqd_graph_launch(void *graph_exec, aqd_stream_t stream);
+void aqd_graph_destroy(void *graph_exec);
+
 /* Message of the calling thread's last failed call ("" if none). */
 const char *aqd_last_error(void);
 

@@ -78,6 +78,10 @@ def lib():
             "qconv_destroy": ([vp], None),
             "qadd_run": ([POINTER(QaddDesc), vp, vp, vp, POINTER(QaddParams), vp], st),
             "aqd_channel_sums": ([vp, c_int64, i, vp, vp], st),
+            "aqd_graph_begin": ([vp], st),
+            "aqd_graph_end": ([vp, POINTER(c_void_p)], st),
+            "aqd_graph_launch": ([vp, vp], st),
+            "aqd_graph_destroy": ([vp], None),
             "aqd_last_error": ([], ctypes.c_char_p),
             "aqd_pack_codes": ([vp, c_int64, i, i, vp], st),
             "aqd_unpack_codes": ([vp, c_int64, i, i, vp], st),
@@ -99,7 +103,8 @@ def lib():
 def exported_symbols():
     return ["qconv_create", "qconv_out_shape", "qconv_run", "qconv_run_group",
             "qconv_group_workspace", "qconv_run_group_ws", "qconv_run_proj", "qconv_destroy",
-            "qadd_run", "aqd_channel_sums", "aqd_last_error", "aqd_pack_codes",
+            "qadd_run", "aqd_channel_sums", "aqd_graph_begin", "aqd_graph_end",
+            "aqd_graph_launch", "aqd_graph_destroy", "aqd_last_error", "aqd_pack_codes",
             "aqd_unpack_codes", "aqd_approx_ratio", "aqd_normalize_multiplier",
             "aqd_bn_stats_from_sums", "aqd_fold_bn", "aqd_skip_params", "aqd_requant_params"]
 
@@ -215,6 +220,26 @@ def qadd_run(n, h, w, c, bits_a, bits_b, bits_out, up2, hb, wb, a, b, y, params,
 
 def channel_sums(v, rows, c, sums, stream=None):
     _check(lib().aqd_channel_sums(_addr(v), rows, c, _addr(sums), _stream(stream)))
+
+
+def graph_begin(stream):
+    """Start recording the library calls on `stream` (not the null stream)."""
+    _check(lib().aqd_graph_begin(_stream(stream)))
+
+
+def graph_end(stream) -> int:
+    """End the recording; returns the executable graph handle."""
+    h = c_void_p()
+    _check(lib().aqd_graph_end(_stream(stream), ctypes.byref(h)))
+    return h.value
+
+
+def graph_launch(graph, stream=None):
+    _check(lib().aqd_graph_launch(graph, _stream(stream)))
+
+
+def graph_destroy(graph):
+    lib().aqd_graph_destroy(graph)
 
 
 # ----------------------------------------------------------- host helpers

@@ -871,6 +871,51 @@ aqd_status_t aqd_channel_sums(const int32_t *v, int64_t rows, int c, int64_t *su
     return AQD_OK;
 }
 
+// ------------------------------------------------------------------ graph capture
+aqd_status_t aqd_graph_begin(aqd_stream_t stream)
+{
+    REQUIRE(stream, "capture needs a stream other than the null stream");
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing((hipStream_t)stream, &st) != hipSuccess)
+        return fail(AQD_ERR_DEVICE, "stream query failed");
+    REQUIRE(st == hipStreamCaptureStatusNone, "the stream is already capturing");
+    if (hipStreamBeginCapture((hipStream_t)stream, hipStreamCaptureModeThreadLocal) != hipSuccess)
+        return fail(AQD_ERR_DEVICE, "stream capture could not start");
+    return AQD_OK;
+}
+
+aqd_status_t aqd_graph_end(aqd_stream_t stream, void **graph_exec)
+{
+    REQUIRE(stream && graph_exec, "null stream or output pointer");
+    *graph_exec = nullptr;
+    hipGraph_t g = nullptr;
+    if (hipStreamEndCapture((hipStream_t)stream, &g) != hipSuccess || !g) {
+        (void)hipGetLastError();
+        return fail(AQD_ERR_DEVICE, "stream capture failed (an operation was not capturable)");
+    }
+    hipGraphExec_t e = nullptr;
+    const hipError_t r = hipGraphInstantiate(&e, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (r != hipSuccess || !e)
+        return fail(AQD_ERR_DEVICE, "graph instantiation failed");
+    *graph_exec = (void *)e;
+    return AQD_OK;
+}
+
+aqd_status_t aqd_graph_launch(void *graph_exec, aqd_stream_t stream)
+{
+    REQUIRE(graph_exec, "null graph");
+    if (hipGraphLaunch((hipGraphExec_t)graph_exec, (hipStream_t)stream) != hipSuccess)
+        return fail(AQD_ERR_DEVICE, "graph launch failed");
+    return AQD_OK;
+}
+
+void aqd_graph_destroy(void *graph_exec)
+{
+    if (graph_exec)
+        (void)hipGraphExecDestroy((hipGraphExec_t)graph_exec);
+}
+
 // ------------------------------------------------------------------ host helpers
 aqd_status_t aqd_pack_codes(const uint8_t *codes, int64_t rows, int c, int bits, uint8_t *out)
 {

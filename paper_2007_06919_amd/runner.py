@@ -13,6 +13,8 @@ A network description (``workloads.NetSpec``) becomes a list of grouped
   only by the block's last conv) runs fused into that conv
   (``qconv_run_proj``): its int32 tensor is not written during a forward
   pass (it is written once, at set-up, by the calibration pass);
+* ``capture()`` records one forward pass into a HIP graph (``aqd_graph_*``)
+  and ``replay()`` enqueues the whole network as one graph launch;
 * one workspace, sized for the largest group's split-K need
   (``qconv_group_workspace``), lets small launches split their K reduction
   over more workgroups (``qconv_run_group_ws``);
@@ -74,6 +76,8 @@ class Net:
                                 for g in self.schedule)
         self.ws = (torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
                    if self.ws_bytes else None)
+        self.graph = None
+        self.graph_stream = None
 
     # ---------------------------------------------------------------- setup
     def _fusable(self) -> dict:
@@ -242,6 +246,30 @@ class Net:
             if launch_hook:
                 launch_hook(gi, "after")
 
+    def capture(self, stream=None):
+        """Record one forward pass on the (non-null) stream into a HIP graph;
+        replay() then enqueues the whole network as one launch. The recorded
+        pointers are this runner's buffers and workspace."""
+        s = self.stream if stream is None else stream
+        if self.graph is not None:
+            aqd.graph_destroy(self.graph)
+            self.graph = None
+        aqd.graph_begin(s)
+        try:
+            self.forward(s)
+        except Exception:
+            try:
+                aqd.graph_destroy(aqd.graph_end(s))
+            except aqd.AqdError:
+                pass
+            raise
+        self.graph = aqd.graph_end(s)
+        self.graph_stream = s
+
+    def replay(self, stream=None):
+        assert self.graph is not None, "capture() first"
+        aqd.graph_launch(self.graph, self.graph_stream if stream is None else stream)
+
     def _run_fused(self, conv, proj, stream):
         x, _, y = conv.segs[0]
         xp = proj.segs[0][0]
@@ -261,6 +289,10 @@ class Net:
         return self.bufs[name].cpu().numpy()
 
     def close(self):
+        if getattr(self, "graph", None) is not None:
+            self.torch.cuda.synchronize(self.device)   # no replay may be pending
+            aqd.graph_destroy(self.graph)
+            self.graph = None
         for h in self.handles.values():
             aqd.qconv_destroy(h)
         self.handles = {}

@@ -87,3 +87,33 @@ def test_config4_bench_configuration(torch):
     net, params = workloads.config(4)
     gpu, _ = compare_network(torch, net, params, images=[0, 7])
     assert gpu.fused and gpu.ws_bytes > 0
+
+
+def test_graph_replay_matches_eager(torch):
+    """The network recorded once into a HIP graph (aqd_graph_*): three
+    replays, each after the output buffers were overwritten by eager work and
+    the device synchronised, reproduce the eager pass's bytes for every
+    tensor the pass writes."""
+    net, params = workloads.scaled_config(4, 1, 192, 256)
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        gpu = runner.Net(net, params, device="cuda:0", stream=stream)
+    try:
+        with torch.cuda.stream(stream):
+            gpu.forward()
+            torch.cuda.synchronize()
+            # outputs of fused-away projections are written at set-up only
+            skipped = {c.segs[0][2] for c in net.convs if c.name in gpu._fused_away}
+            written = [n for n in net.tensors if n not in net.inputs and n not in skipped]
+            want = {n: gpu.raw(n).copy() for n in written}
+            gpu.capture()
+            for r in range(3):
+                for n in written:
+                    gpu.bufs[n].fill_(-7 if net.tensors[n].bits == 32 else 0x5A)
+                torch.cuda.synchronize()
+                gpu.replay()
+                torch.cuda.synchronize()
+                for n in written:
+                    assert_same(gpu.raw(n), want[n], f"replay {r}: {n}")
+    finally:
+        gpu.close()
