@@ -29,8 +29,8 @@ COPY_PROBE_BYTES = 256 << 20
 # HBM traffic of one head-tower launch, from two rocprofv3 counter runs
 # (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain copy of
 # COPY_PROBE_BYTES; valid only for the kernel source it was measured on.
-HEAD_TRAFFIC = {"kernel_sha256": "9b9349f9d9345103cd64ce485aa4f2ca382ed85389a864a34f4bb16ac3c6c3fe",
-                "fetch_bytes": 50969621, "write_bytes": 45670400}
+HEAD_TRAFFIC = {"kernel_sha256": "77e93740612892dddcdfe933a86ba057cf99563b4bb90f79802defc2b0a0e4ab",
+                "fetch_bytes": 50969628, "write_bytes": 45670400}
 
 
 def kernel_sha256():
