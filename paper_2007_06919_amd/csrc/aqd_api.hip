@@ -797,7 +797,13 @@ aqd_status_t qconv_run_proj(qconv_t conv, qconv_t proj, int level, int n, int h,
     a.cin2 = e.cin;
     a.stride2 = e.stride;
     a.ksteps2 = proj->ksteps;
-    if (launch_qconv_proj(a, (hipStream_t)stream_) != hipSuccess)
+    // one K step each (cin 64): persistent streaming tiles (same 256 x 64 tiles)
+    const bool stream_tiles = conv->ksteps == 1 && proj->ksteps == 1 && d.kh == 1 && d.kw == 1 &&
+                              d.pad == 0 && d.cout % 256 == 0;
+    if (stream_tiles)
+        a.tile_cfg = TILE_STREAM;
+    if ((stream_tiles ? launch_qconv_mfma(4, a, (hipStream_t)stream_) : launch_qconv_proj(a, (hipStream_t)stream_)) !=
+        hipSuccess)
         return fail(AQD_ERR_DEVICE, "fused projection launch failed");
     return AQD_OK;
 }

@@ -756,6 +756,10 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
 // tile's MFMAs and epilogue run. Everything a tile's epilogue reads (table,
 // skip table, skip codes) is in LDS, so that the only waits for global memory
 // are the explicit ones at the top of each tile.
+// SKK: 0 = no skip, 1 = code skip, 2 = a residual block's projection shortcut
+// fused in (1x1 of x2 with one K step, int32, aligned with v as in Eq. 7-8;
+// the main convolution then has one K step too): its weights and codes use
+// the second K-step slots of the weight and code buffers.
 constexpr int ST_KMAX = 2;
 
 template <int SKK, int FAST>
@@ -769,13 +773,14 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
     constexpr int SK_TILE = BPX * BCO * BI / 8;    // skip codes of one tile (8 KiB)
     constexpr int OFF_B = ST_KMAX * A_STEP;
     constexpr int OFF_S = OFF_B + 2 * ST_KMAX * B_STEP;
-    constexpr int OFF_P = OFF_S + (SKK ? 2 * SK_TILE : 0);
-    constexpr int OFF_L = OFF_P + EPI_FIELDS * BCO * 4;
-    constexpr int LDS_BYTES = OFF_L + (SKK ? BCO * (QMAX + 1) * 4 : 0);
+    constexpr int OFF_P = OFF_S + (SKK == 1 ? 2 * SK_TILE : 0);
+    constexpr int OFF_L = OFF_P + EPI_FIELDS * BCO * 4;   // skip table (SKK 1) or the shortcut's bias (SKK 2)
+    constexpr int LDS_BYTES = OFF_L + (SKK == 1 ? BCO * (QMAX + 1) * 4 : SKK == 2 ? BCO * 4 : 0);
     static_assert(LDS_BYTES <= 81920, "two workgroups per CU");
     __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS_BYTES];
     int32_t *prm = (int32_t *)(lds + OFF_P);
     int32_t *lut = (int32_t *)(lds + OFF_L);       // [BCO][2^BI]: RSM(k, c, d)
+    int32_t *bias2 = (int32_t *)(lds + OFF_L);     // [BCO]: the shortcut's bias
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -821,6 +826,19 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
             for (int k = 0; k < K; ++k)
                 if (lane < 32)
                     dma16(src ? src + k * PB : A.zero, lbase + OFF_B + (b * ST_KMAX + k) * B_STEP + wave * 512);
+            if constexpr (SKK == 2) {
+                // the shortcut's input pixel (1x1, stride A.stride2, always inside x2)
+                const uint8_t *src2 = A.zero;
+                if (p < S.P) {
+                    const int n_ = (int)p / hw;
+                    const int rem = (int)p - n_ * hw;
+                    const int oh = rem / S.wo, ow = rem - oh * S.wo;
+                    src2 = S.x2 + (((long long)n_ * S.h2 + oh * A.stride2) * S.w2 + ow * A.stride2) *
+                                      (A.cin2 * BI / 8) + 16 * ((lane & 1) ^ swz_b4(ploc));
+                }
+                if (lane < 32)
+                    dma16(src2, lbase + OFF_B + (b * ST_KMAX + 1) * B_STEP + wave * 512);
+            }
         }
         if constexpr (SKK == 1) {
 #pragma unroll
@@ -880,12 +898,51 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
                 for (int t = 0; t < BCO * (QMAX + 1) / NT; ++t)
                     lut[tid + t * NT] = S.lut[co_tile * BCO * (QMAX + 1) + tid + t * NT];
             }
+            if constexpr (SKK == 2) {
+                // the shortcut's weights in the second K-step slot, its bias
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const int row = 16 * (4 * t + wave) + (lane >> 2);
+                    dma16(S.wt2 + (long long)co_tile * A.ksteps2 * A_STEP + row * KC + 16 * ((lane & 3) ^ swz_a(row)),
+                          lbase + A_STEP + (4 * t + wave) * 1024);
+                }
+                bias2[tid] = S.epi2[EPI_BIAS * A.cout_pad + co_tile * BCO + tid];
+            }
             wait_vmcnt<0>();
             __syncthreads();
             cur = s;
         }
         if (q + nstream < qtiles)
             issue_tile(q + nstream, buf ^ 1);
+
+        // the shortcut first: v2 = acc2 + bias2
+        v4i acc2[SKK == 2 ? MI : 1][SKK == 2 ? NJ : 1];
+        if constexpr (SKK == 2) {
+#pragma unroll
+            for (int i = 0; i < MI; ++i) {
+                const v4i b = *(const v4i *)(bias2 + co_loc + 4 * i);
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    acc2[i][j] = b;
+            }
+            v4i fa[MI];
+            uint2 fb[NJ];
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+                fb[j] = *(const uint2 *)(lds + b_off + (buf * ST_KMAX + 1) * B_STEP + j * 16 * PB);
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+                fa[i] = *(const v4i *)(lds + A_STEP + a_off + i * 16 * KC);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                const uint2 w = fb[j];
+                const v4i bj = v4i{(int)(w.x & 0x0F0F0F0Fu), (int)((w.x >> 4) & 0x0F0F0F0Fu),
+                                   (int)(w.y & 0x0F0F0F0Fu), (int)((w.y >> 4) & 0x0F0F0F0Fu)};
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+                    acc2[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], bj, acc2[i][j], 0, 0, 0);
+            }
+        }
 
         // MFMAs: accumulators start at the bias (v = acc + bias)
         v4i acc[MI][NJ];
@@ -897,7 +954,7 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
                 acc[i][j] = b;
         }
 #pragma unroll
-        for (int k = 0; k < ST_KMAX; ++k) {
+        for (int k = 0; k < (SKK == 2 ? 1 : ST_KMAX); ++k) {
             if (k < K) {
                 v4i fa[MI];
                 uint2 fb[NJ];
@@ -971,7 +1028,11 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
                     for (int e = 0; e < 4; ++e) {
                         const int v = acc[i][j][e];  // acc + bias
                         const int bit = (4 * i + e) * BI;
-                        const int kv = SKK == 1 ? (int)((skw[j][bit >> 5] >> (bit & 31)) & QMAX) : 0;
+                        int kv = 0;
+                        if constexpr (SKK == 1)
+                            kv = (int)((skw[j][bit >> 5] >> (bit & 31)) & QMAX);
+                        else if constexpr (SKK == 2)
+                            kv = acc2[i][j][e];  // v2 = acc2 + bias2
                         int y;
                         if constexpr (FAST) {
                             int u = v;
@@ -1081,8 +1142,11 @@ hipError_t launch_qconv_short(const MfmaArgs &a, hipStream_t stream)
 // the channel tiles, each workgroup on one channel tile)
 hipError_t launch_qconv_stream(const MfmaArgs &a, hipStream_t stream)
 {
-    if (a.ksteps > ST_KMAX || a.bits_out != 4 || (a.skip_bits != 0 && a.skip_bits != 4) || a.kh != 1 ||
-        a.kw != 1 || a.pad != 0 || a.cout % 256 != 0 || a.co_tiles < 1 || a.co_tiles > 256)
+    // skip_bits 32: the fused projection shortcut, one K step each
+    const bool dual = a.skip_bits == 32;
+    if (a.ksteps > ST_KMAX || a.bits_out != 4 || (a.skip_bits != 0 && a.skip_bits != 4 && !dual) ||
+        (dual && (a.ksteps != 1 || a.ksteps2 != 1 || a.cin2 != KC || a.up2)) || a.kh != 1 || a.kw != 1 ||
+        a.pad != 0 || a.cout % 256 != 0 || a.co_tiles < 1 || a.co_tiles > 256)
         return hipErrorInvalidValue;
     const int qtiles = a.total_tiles / a.co_tiles;
     if (qtiles <= 0)
@@ -1092,7 +1156,12 @@ hipError_t launch_qconv_stream(const MfmaArgs &a, hipStream_t stream)
     bool fast = true;
     for (int i = 0; i < a.nseg; ++i)
         fast = fast && a.seg[i].fast;
-    if (a.skip_bits == 0) {
+    if (dual) {
+        if (fast)
+            hipLaunchKernelGGL((qconv_stream_kernel<2, 1>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_stream_kernel<2, 0>), grid, block, 0, stream, a);
+    } else if (a.skip_bits == 0) {
         if (fast)
             hipLaunchKernelGGL((qconv_stream_kernel<0, 1>), grid, block, 0, stream, a);
         else

@@ -316,6 +316,10 @@ PROJ_CASES = [
     (2, 13, 17, 128, 26, 33, 256, 2, 512, 1, 1),     # later stages: stride 2 shortcut, 2 channel tiles
     (1, 9, 11, 256, 17, 21, 512, 2, 1024, 1, 0),     # ragged pixels, two's-complement weights
     (1, 12, 10, 64, 12, 10, 128, 1, 256, 3, 1),      # 3x3 main convolution
+    # one K step each (cin 64): persistent streaming tiles
+    (8, 120, 100, 64, 120, 100, 64, 1, 256, 1, 1),   # ~3 tiles per workgroup
+    (2, 13, 17, 64, 26, 33, 64, 2, 512, 1, 0),       # stride 2 shortcut, 2 channel tiles
+    (1, 9, 11, 64, 9, 11, 64, 1, 768, 1, 1),         # 3 channel tiles, ragged pixels
 ]
 
 
@@ -373,9 +377,11 @@ def test_fused_projection_parity(torch, case):
     assert_same(got, _run_proj(torch, main, proj, fused=False), f"fused vs separate {case}")
 
 
-def test_fused_projection_general_requant(torch):
-    """Levels with shift < 2 take the 64-bit requantisation in the fused launch."""
-    main, proj = _proj_case(PROJ_CASES[1], seed=23, general=True)
+@pytest.mark.parametrize("which", [1, 4])
+def test_fused_projection_general_requant(torch, which):
+    """Levels with shift < 2 take the 64-bit requantisation in the fused launch
+    (tiled kernel and streaming kernel)."""
+    main, proj = _proj_case(PROJ_CASES[which], seed=23, general=True)
     assert_same(_run_proj(torch, main, proj), oracle_conv(main), "fused projection, shift < 2")
 
 
