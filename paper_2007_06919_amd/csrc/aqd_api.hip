@@ -506,6 +506,14 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
             tile_cfg = TILE_256x64;
             blk_px = 64;
         }
+    } else if ((h0.tile_cfg == TILE_128x256 || h0.tile_cfg == TILE_64x512) && h0.ksteps <= 4 &&
+               h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_in == 4 && h0.d.bits_out == 4 &&
+               h0.d.skip_bits == 0 && h0.d.kh == 1 && h0.d.kw == 1 && h0.d.pad == 0 &&
+               h0.d.cout % h0.blk_co == 0) {
+        // 1x1 convolutions with cin <= 256 on 128- or 64-channel handles:
+        // persistent streaming tiles (weights resident in LDS)
+        tile_cfg = h0.tile_cfg == TILE_128x256 ? TILE_STREAM_C128 : TILE_STREAM_C64;
+        blk_px = h0.tile_cfg == TILE_128x256 ? 64 : 128;
     }
     int tiles = 0;
     for (int i = 0; i < count; ++i) {
@@ -566,7 +574,8 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
 // when the model gains 20%.
 void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
 {
-    if (a.tile_cfg == TILE_256x64S || a.tile_cfg == TILE_256x64 || a.tile_cfg == TILE_STREAM) {  // never split
+    if (a.tile_cfg == TILE_256x64S || a.tile_cfg == TILE_256x64 || a.tile_cfg == TILE_STREAM ||
+        a.tile_cfg == TILE_STREAM_C128 || a.tile_cfg == TILE_STREAM_C64) {  // never split
         *nparts = 1;
         *kchunk = a.ksteps;
         return;

@@ -15,7 +15,10 @@ enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
        // launch-time choices for handles laid out for 256x128 (same weight layout):
        TILE_256x64S = 3,   // short K, code outputs: three workgroups per CU
        TILE_256x64 = 4,    // launches with too few 256x128 tiles to fill the GPU
-       TILE_STREAM = 5 };  // 1x1, cin <= 128, code outputs: persistent 256 x 64 tiles
+       TILE_STREAM = 5,    // 1x1, cin <= 128, code outputs: persistent 256 x 64 tiles
+       // 1x1, cin <= 256, code outputs, no skip, for handles laid out for 128-
+       // and 64-channel tiles: persistent 128 x 64 and 64 x 128 tiles
+       TILE_STREAM_C128 = 6, TILE_STREAM_C64 = 7 };
 constexpr int KC = 64;
 
 // tile shape of a configuration, and the channels one lane holds per pixel

@@ -760,13 +760,18 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
 // fused in (1x1 of x2 with one K step, int32, aligned with v as in Eq. 7-8;
 // the main convolution then has one K step too): its weights and codes use
 // the second K-step slots of the weight and code buffers.
-constexpr int ST_KMAX = 2;
-
-template <int SKK, int FAST>
+// Shapes (4 waves, two workgroups per CU, 32 pixels per wave): MI = 8, WC = 2:
+// 256 channels x 64 pixels, up to 2 K steps (handles laid out for 256-channel
+// tiles); MI = 4, WC = 2: 128 x 64, up to 4 K steps; MI = 4, WC = 1: 64 x 128,
+// up to 4 K steps (the latter two without skip).
+template <int SKK, int FAST, int MI = 8, int WC = 2>
 __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
 {
-    constexpr int BI = 4, MI = 8, NJ = 2, WPC = 2, NT = 256;
-    constexpr int TM = 128, TN = 32, BCO = 256, BPX = 64, PB = KC * BI / 8;
+    constexpr int BI = 4, NJ = 2, WPC = 4 / WC, NT = 256;
+    constexpr int TM = 16 * MI, TN = 32, BCO = WC * TM, BPX = TN * WPC, PB = KC * BI / 8;
+    constexpr int ST_KMAX = BCO == 256 ? 2 : 4;
+    constexpr int PPW = BPX / 4;                   // pixels each wave copies (16 or 32)
+    static_assert(SKK == 0 || BCO == 256, "skips on 256-channel tiles only");
     constexpr int CPL = 4 * MI, OW = CPL * BI / 32, QMAX = (1 << BI) - 1;
     constexpr int A_STEP = BCO * KC;               // int8 weight rows of one K step (16 KiB)
     constexpr int B_STEP = BPX * PB;               // packed codes of one K step (2 KiB)
@@ -813,7 +818,7 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
         const int pq = q - S.tile_begin / A.co_tiles;
         const int hw = S.ho * S.wo;
         {
-            const int ploc = 16 * wave + (lane >> 1);
+            const int ploc = PPW * wave + (lane >> 1);
             const long long p = (long long)pq * BPX + ploc;
             const uint8_t *src = nullptr;
             if (p < S.P) {  // P < 2^31 (host): 32-bit index arithmetic
@@ -824,8 +829,9 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
                       16 * ((lane & 1) ^ swz_b4(ploc));
             }
             for (int k = 0; k < K; ++k)
-                if (lane < 32)
-                    dma16(src ? src + k * PB : A.zero, lbase + OFF_B + (b * ST_KMAX + k) * B_STEP + wave * 512);
+                if (PPW == 32 || lane < 2 * PPW)
+                    dma16(src ? src + k * PB : A.zero,
+                          lbase + OFF_B + (b * ST_KMAX + k) * B_STEP + wave * (PPW * PB));
             if constexpr (SKK == 2) {
                 // the shortcut's input pixel (1x1, stride A.stride2, always inside x2)
                 const uint8_t *src2 = A.zero;
@@ -881,7 +887,7 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
             // the segment's weights (every K step) and tables
             for (int k = 0; k < K; ++k)
 #pragma unroll
-                for (int t = 0; t < 4; ++t) {
+                for (int t = 0; t < BCO / 64; ++t) {
                     const int row = 16 * (4 * t + wave) + (lane >> 2);
                     dma16(S.wt + ((long long)co_tile * A.ksteps + k) * A_STEP + row * KC +
                               16 * ((lane & 3) ^ swz_a(row)),
@@ -1108,6 +1114,8 @@ void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane)
     case TILE_256x64S:
     case TILE_256x64:
     case TILE_STREAM: *blk_co = 256; *blk_px = 64; *chan_per_lane = 32; return;
+    case TILE_STREAM_C128: *blk_co = 128; *blk_px = 64; *chan_per_lane = 16; return;
+    case TILE_STREAM_C64: *blk_co = 64; *blk_px = 128; *chan_per_lane = 16; return;
     case TILE_128x256: *blk_co = 128; *blk_px = 256; *chan_per_lane = 16; return;
     default: *blk_co = 64; *blk_px = 512; *chan_per_lane = 16; return;
     }
@@ -1144,19 +1152,36 @@ hipError_t launch_qconv_stream(const MfmaArgs &a, hipStream_t stream)
 {
     // skip_bits 32: the fused projection shortcut, one K step each
     const bool dual = a.skip_bits == 32;
-    if (a.ksteps > ST_KMAX || a.bits_out != 4 || (a.skip_bits != 0 && a.skip_bits != 4 && !dual) ||
+    const int bco = a.tile_cfg == TILE_STREAM ? 256 : a.tile_cfg == TILE_STREAM_C128 ? 128 : 64;
+    const int kmax = bco == 256 ? 2 : 4;
+    if (a.ksteps > kmax || a.bits_out != 4 || (a.skip_bits != 0 && a.skip_bits != 4 && !dual) ||
+        (bco != 256 && a.skip_bits != 0) ||
         (dual && (a.ksteps != 1 || a.ksteps2 != 1 || a.cin2 != KC || a.up2)) || a.kh != 1 || a.kw != 1 ||
-        a.pad != 0 || a.cout % 256 != 0 || a.co_tiles < 1 || a.co_tiles > 256)
+        a.pad != 0 || a.cout % bco != 0 || a.co_tiles < 1 || a.co_tiles > 256)
         return hipErrorInvalidValue;
     const int qtiles = a.total_tiles / a.co_tiles;
     if (qtiles <= 0)
         return hipSuccess;
-    const int nstream = qtiles < 512 / a.co_tiles ? qtiles : 512 / a.co_tiles;
+    // workgroups per CU: two on 256-channel tiles (LDS), three on the smaller ones
+    const int slots = bco == 256 ? 512 : 768;
+    const int nstream = qtiles < slots / a.co_tiles ? qtiles : slots / a.co_tiles;
     dim3 grid(nstream * a.co_tiles), block(256);
     bool fast = true;
     for (int i = 0; i < a.nseg; ++i)
         fast = fast && a.seg[i].fast;
-    if (dual) {
+    if (bco != 256) {
+        if (bco == 128) {
+            if (fast)
+                hipLaunchKernelGGL((qconv_stream_kernel<0, 1, 4, 2>), grid, block, 0, stream, a);
+            else
+                hipLaunchKernelGGL((qconv_stream_kernel<0, 0, 4, 2>), grid, block, 0, stream, a);
+        } else {
+            if (fast)
+                hipLaunchKernelGGL((qconv_stream_kernel<0, 1, 4, 1>), grid, block, 0, stream, a);
+            else
+                hipLaunchKernelGGL((qconv_stream_kernel<0, 0, 4, 1>), grid, block, 0, stream, a);
+        }
+    } else if (dual) {
         if (fast)
             hipLaunchKernelGGL((qconv_stream_kernel<2, 1>), grid, block, 0, stream, a);
         else
@@ -1199,7 +1224,9 @@ hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
         case TILE_256x128: return launch_modes<4, 8, 4, 2, 2>(a, stream);
         case TILE_256x64S: return launch_qconv_short(a, stream);
         case TILE_256x64: return launch_modes<4, 8, 2, 2, 2>(a, stream);
-        case TILE_STREAM: return launch_qconv_stream(a, stream);
+        case TILE_STREAM:
+        case TILE_STREAM_C128:
+        case TILE_STREAM_C64: return launch_qconv_stream(a, stream);
         case TILE_128x256: return launch_modes<4, 4, 8, 2, 2>(a, stream);
         case TILE_64x512: return launch_modes<4, 4, 8, 1, 4>(a, stream);
         }

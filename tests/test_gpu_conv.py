@@ -123,6 +123,13 @@ STREAM_CASES = [
     (1, 25, 21, 128, 256, 1, 2, 4, 4, 1, 4, 0, False),      # stride 2, no skip
     (8, 120, 161, 64, 256, 1, 1, 4, 4, 1, 4, 4, False),     # ~4.7 tiles per workgroup
     (3, 70, 90, 128, 768, 1, 1, 4, 4, 0, 4, 4, False),      # 3 channel tiles, 2 tiles per workgroup
+    # handles laid out for 128- and 64-channel tiles, up to 4 K steps, no skip
+    (2, 41, 52, 256, 128, 1, 1, 4, 4, 0, 4, 0, False),      # 128 x 64 tiles, 4 K steps
+    (4, 60, 90, 192, 128, 1, 1, 4, 4, 1, 4, 0, False),      # 3 K steps, several tiles per workgroup
+    (1, 45, 41, 128, 128, 1, 2, 4, 4, 0, 4, 0, False),      # stride 2
+    (2, 41, 52, 256, 64, 1, 1, 4, 4, 1, 4, 0, False),       # 64 x 128 tiles, 4 K steps
+    (1, 33, 37, 64, 64, 1, 1, 4, 4, 0, 4, 0, False),        # 1 K step
+    (8, 200, 168, 256, 64, 1, 1, 4, 4, 1, 4, 0, False),     # ~2.7 tiles per workgroup
 ]
 
 
