@@ -45,7 +45,7 @@ def _conv_key(net: NetSpec, conv) -> tuple:
 
 class Net:
     def __init__(self, net: NetSpec, params: NetParams, device="cuda:0", stream=None,
-                 split_k: bool = True, fuse_proj: bool = True):
+                 split_k: bool = True, fuse_proj: bool = True, side_streams: int = 2):
         import torch
 
         self.torch = torch
@@ -76,6 +76,23 @@ class Net:
                                 for g in self.schedule)
         self.ws = (torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
                    if self.ws_bytes else None)
+        # independent launches (FPN side branches, the box prediction next to
+        # the class prediction) run on side streams; each stream has its own
+        # split-K workspace
+        self.side = [torch.cuda.Stream(device=self.device) for _ in range(side_streams)]
+        self.side_ws = [torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+                        if self.ws_bytes else None for _ in self.side]
+        self.deps, self.lane = self._plan_streams(len(self.side) + 1)
+        # groups whose completion another stream waits for, and each side
+        # stream's last group (the main stream joins it at the end of a pass)
+        self.signal = {d for gi, ds in enumerate(self.deps) for d in ds
+                       if self.lane[gi] is not None and self.lane[d] is not None
+                       and self.lane[d] != self.lane[gi]}
+        for k in range(1, len(self.side) + 1):
+            mine = [gi for gi, l in enumerate(self.lane) if l == k]
+            if mine:
+                self.signal.add(mine[-1])
+        self._calls = self._marshal()
         self.graph = None
         self.graph_stream = None
 
@@ -105,6 +122,86 @@ class Net:
                 continue
             out[conv.name] = d
         return out
+
+    def _marshal(self):
+        """Per group, the C-ABI calls of one pass with their arguments
+        converted once (the tensors never move): a forward pass then costs
+        one foreign call per launch."""
+        L = aqd.lib()
+        wss = [self.ws] + self.side_ws
+        calls = []
+        for gi, group in enumerate(self.schedule):
+            k = self.lane[gi]
+            cs = []
+            if k is not None:
+                plain = [(c, si) for c, si in group
+                         if c.name not in self._fused_away and c.name not in self.fused]
+                if plain:
+                    arr = aqd._seg_array([self._seg_args(conv, si) for conv, si in plain])
+                    if wss[k] is not None:
+                        cs.append((L.qconv_run_group_ws,
+                                   (len(plain), arr, wss[k].data_ptr(), self.ws_bytes)))
+                    else:
+                        cs.append((L.qconv_run_group, (len(plain), arr)))
+                for conv, si in group:
+                    if conv.name in self.fused:
+                        proj = self.fused[conv.name]
+                        x, _, y = conv.segs[0]
+                        xp = proj.segs[0][0]
+                        tx, tp = self.net.tensors[x], self.net.tensors[xp]
+                        cs.append((L.qconv_run_proj,
+                                   (self.handles[conv.name], self.handles[proj.name], 0, tx.n, tx.h,
+                                    tx.w, self.bufs[x].data_ptr(), tp.h, tp.w,
+                                    self.bufs[xp].data_ptr(), self.bufs[y].data_ptr())))
+            calls.append(cs)
+        return calls
+
+    def _group_inputs(self, group):
+        """Tensors a launch of this group reads (codes, skips, fused shortcut inputs)."""
+        ins = []
+        for conv, si in group:
+            if conv.name in self._fused_away:
+                continue
+            x, skip, _ = conv.segs[si]
+            ins.append(x)
+            if conv.name in self.fused:
+                ins.append(self.fused[conv.name].segs[0][0])  # the shortcut's input
+            elif skip is not None:
+                ins.append(skip)
+        return ins
+
+    def _plan_streams(self, nstreams):
+        """Per group: the groups it depends on, and its stream (0 = the main
+        stream). A group continues the stream whose last group it depends on
+        (latest first); otherwise it opens on the side stream least recently
+        used. Groups that launch nothing (fused-away shortcuts) get no stream."""
+        producer = {}
+        for gi, group in enumerate(self.schedule):
+            for conv, si in group:
+                if conv.name not in self._fused_away:
+                    producer[conv.segs[si][2]] = gi
+        deps, lane, last = [], [], [None] * nstreams
+        used = [0] * nstreams
+        for gi, group in enumerate(self.schedule):
+            d = sorted({producer[t] for t in self._group_inputs(group) if t in producer} - {gi})
+            deps.append(d)
+            if not self._group_inputs(group):
+                lane.append(None)
+                continue
+            pick = None
+            for dep in sorted(d, reverse=True):
+                if lane[dep] is not None and last[lane[dep]] == dep:
+                    pick = lane[dep]
+                    break
+            if pick is None:
+                if gi == 0 or not d:
+                    pick = 0
+                else:
+                    pick = min(range(1, nstreams), key=lambda k: used[k]) if nstreams > 1 else 0
+            lane.append(pick)
+            last[pick] = gi
+            used[pick] = gi + 1
+        return deps, lane
 
     def launches_per_forward(self) -> int:
         n = 0
@@ -228,23 +325,46 @@ class Net:
     def forward(self, stream=None, launch_hook=None):
         """Enqueue the whole network on the stream. launch_hook(group_index,
         'before'|'after') is called around each grouped launch (for timing)."""
-        s = self.stream if stream is None else stream
+        torch = self.torch
+        main = self.stream if stream is None else stream
+        streams = [main] + self.side
+        done = {}          # group -> event recorded after its launch
+        tail = {}          # side stream -> event after its last launch
+        # side streams start after the work already enqueued on the main stream
+        start = None
+        if len(self.side):
+            start = torch.cuda.Event()
+            start.record(main)
+        started = set()
         for gi, group in enumerate(self.schedule):
+            k = self.lane[gi]
+            if k is None:
+                continue
+            s = streams[k]
+            if k and k not in started:
+                s.wait_event(start)
+                started.add(k)
+            for d in self.deps[gi]:
+                if self.lane[d] is not None and self.lane[d] != k:
+                    s.wait_event(done[d])
             if launch_hook:
                 launch_hook(gi, "before")
-            plain = [(c, si) for c, si in group
-                     if c.name not in self._fused_away and c.name not in self.fused]
-            if plain:
-                segs = [self._seg_args(conv, si) for conv, si in plain]
-                if self.ws is not None:
-                    aqd.qconv_run_group_ws(segs, self.ws, self.ws_bytes, s)
-                else:
-                    aqd.qconv_run_group(segs, s)
-            for conv, si in group:
-                if conv.name in self.fused:
-                    self._run_fused(conv, self.fused[conv.name], s)
+            sh = s.cuda_stream
+            for fn, args in self._calls[gi]:
+                st = fn(*args, sh)
+                if st != aqd.AQD_OK:
+                    raise aqd.AqdError(st, aqd.last_error())
             if launch_hook:
                 launch_hook(gi, "after")
+            if gi in self.signal:
+                ev = torch.cuda.Event()
+                ev.record(s)
+                done[gi] = ev
+                if k:
+                    tail[k] = ev
+        # the pass ends on the main stream once every side stream is done
+        for k in sorted(tail):
+            main.wait_event(tail[k])
 
     def capture(self, stream=None):
         """Record one forward pass on the (non-null) stream into a HIP graph;
@@ -269,13 +389,6 @@ class Net:
     def replay(self, stream=None):
         assert self.graph is not None, "capture() first"
         aqd.graph_launch(self.graph, self.graph_stream if stream is None else stream)
-
-    def _run_fused(self, conv, proj, stream):
-        x, _, y = conv.segs[0]
-        xp = proj.segs[0][0]
-        tx, tp = self.net.tensors[x], self.net.tensors[xp]
-        aqd.qconv_run_proj(self.handles[conv.name], self.handles[proj.name], 0, tx.n, tx.h, tx.w,
-                           self.bufs[x], tp.h, tp.w, self.bufs[xp], self.bufs[y], stream)
 
     def group_macs(self, group) -> int:
         tot = 0

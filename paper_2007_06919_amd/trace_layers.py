@@ -46,7 +46,7 @@ def layer_table(trace_csv, workload=4, top=30, passes=5):
     launches = launch_list(net)
     rows = sorted((r for r in csv.DictReader(open(trace_csv))
                    if any(k in r["Kernel_Name"] for k in ("qconv_mfma", "qconv_stream", "qconv_direct", "splitk"))),
-                  key=lambda r: int(r["Start_Timestamp"]))
+                  key=lambda r: int(r["Dispatch_Id"]))  # enqueue order (launches on several streams overlap)
     # one entry per launch; a combining kernel belongs to the launch before it
     seq = []
     for r in rows:
