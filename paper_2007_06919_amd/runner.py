@@ -43,6 +43,65 @@ def _conv_key(net: NetSpec, conv) -> tuple:
             ty.bits, net.tensors[skip].bits if skip else 0, conv.skip_up2)
 
 
+def group_inputs(group, fused, fused_away):
+    """Tensors a launch of this group reads (codes, skips, fused shortcut inputs)."""
+    ins = []
+    for conv, si in group:
+        if conv.name in fused_away:
+            continue
+        x, skip, _ = conv.segs[si]
+        ins.append(x)
+        if conv.name in fused:
+            ins.append(fused[conv.name].segs[0][0])  # the shortcut's input
+        elif skip is not None:
+            ins.append(skip)
+    return ins
+
+
+def plan_streams(schedule, fused, fused_away, nstreams):
+    """Stream plan of a pass: per group, the groups it depends on (producers
+    of the tensors it reads) and its stream (0 = the main stream; None for
+    groups that launch nothing, the fused-away shortcuts); and the set of
+    groups after which an event is recorded (those another stream waits for,
+    and each side stream's last group, which the main stream joins at the end
+    of a pass). A group continues the stream whose last group it depends on
+    (latest first); otherwise it opens on the side stream least recently used."""
+    producer = {}
+    for gi, group in enumerate(schedule):
+        for conv, si in group:
+            if conv.name not in fused_away:
+                producer[conv.segs[si][2]] = gi
+    deps, lane, last = [], [], [None] * nstreams
+    used = [0] * nstreams
+    for gi, group in enumerate(schedule):
+        ins = group_inputs(group, fused, fused_away)
+        d = sorted({producer[t] for t in ins if t in producer} - {gi})
+        deps.append(d)
+        if not ins:
+            lane.append(None)
+            continue
+        pick = None
+        for dep in sorted(d, reverse=True):
+            if lane[dep] is not None and last[lane[dep]] == dep:
+                pick = lane[dep]
+                break
+        if pick is None:
+            if gi == 0 or not d or nstreams == 1:
+                pick = 0
+            else:
+                pick = min(range(1, nstreams), key=lambda k: used[k])
+        lane.append(pick)
+        last[pick] = gi
+        used[pick] = gi + 1
+    signal = {d for gi, ds in enumerate(deps) for d in ds
+              if lane[gi] is not None and lane[d] is not None and lane[d] != lane[gi]}
+    for k in range(1, nstreams):
+        mine = [gi for gi, l in enumerate(lane) if l == k]
+        if mine:
+            signal.add(mine[-1])
+    return deps, lane, signal
+
+
 class Net:
     def __init__(self, net: NetSpec, params: NetParams, device="cuda:0", stream=None,
                  split_k: bool = True, fuse_proj: bool = True, side_streams: int = 2):
@@ -82,16 +141,8 @@ class Net:
         self.side = [torch.cuda.Stream(device=self.device) for _ in range(side_streams)]
         self.side_ws = [torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
                         if self.ws_bytes else None for _ in self.side]
-        self.deps, self.lane = self._plan_streams(len(self.side) + 1)
-        # groups whose completion another stream waits for, and each side
-        # stream's last group (the main stream joins it at the end of a pass)
-        self.signal = {d for gi, ds in enumerate(self.deps) for d in ds
-                       if self.lane[gi] is not None and self.lane[d] is not None
-                       and self.lane[d] != self.lane[gi]}
-        for k in range(1, len(self.side) + 1):
-            mine = [gi for gi, l in enumerate(self.lane) if l == k]
-            if mine:
-                self.signal.add(mine[-1])
+        self.deps, self.lane, self.signal = plan_streams(self.schedule, self.fused,
+                                                         self._fused_away, len(self.side) + 1)
         self._calls = self._marshal()
         self.graph = None
         self.graph_stream = None
@@ -155,53 +206,6 @@ class Net:
                                     self.bufs[xp].data_ptr(), self.bufs[y].data_ptr())))
             calls.append(cs)
         return calls
-
-    def _group_inputs(self, group):
-        """Tensors a launch of this group reads (codes, skips, fused shortcut inputs)."""
-        ins = []
-        for conv, si in group:
-            if conv.name in self._fused_away:
-                continue
-            x, skip, _ = conv.segs[si]
-            ins.append(x)
-            if conv.name in self.fused:
-                ins.append(self.fused[conv.name].segs[0][0])  # the shortcut's input
-            elif skip is not None:
-                ins.append(skip)
-        return ins
-
-    def _plan_streams(self, nstreams):
-        """Per group: the groups it depends on, and its stream (0 = the main
-        stream). A group continues the stream whose last group it depends on
-        (latest first); otherwise it opens on the side stream least recently
-        used. Groups that launch nothing (fused-away shortcuts) get no stream."""
-        producer = {}
-        for gi, group in enumerate(self.schedule):
-            for conv, si in group:
-                if conv.name not in self._fused_away:
-                    producer[conv.segs[si][2]] = gi
-        deps, lane, last = [], [], [None] * nstreams
-        used = [0] * nstreams
-        for gi, group in enumerate(self.schedule):
-            d = sorted({producer[t] for t in self._group_inputs(group) if t in producer} - {gi})
-            deps.append(d)
-            if not self._group_inputs(group):
-                lane.append(None)
-                continue
-            pick = None
-            for dep in sorted(d, reverse=True):
-                if lane[dep] is not None and last[lane[dep]] == dep:
-                    pick = lane[dep]
-                    break
-            if pick is None:
-                if gi == 0 or not d:
-                    pick = 0
-                else:
-                    pick = min(range(1, nstreams), key=lambda k: used[k]) if nstreams > 1 else 0
-            lane.append(pick)
-            last[pick] = gi
-            used[pick] = gi + 1
-        return deps, lane
 
     def launches_per_forward(self) -> int:
         n = 0
