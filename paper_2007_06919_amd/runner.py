@@ -15,6 +15,9 @@ A network description (``workloads.NetSpec``) becomes a list of grouped
   pass (it is written once, at set-up, by the calibration pass);
 * ``capture()`` records one forward pass into a HIP graph (``aqd_graph_*``)
   and ``replay()`` enqueues the whole network as one graph launch;
+* launches that do not continue the main chain of dependencies (the FPN's
+  P6/P7 branch and P4/P5 output convolutions, the box prediction) run on two
+  side streams, joined by events (``plan_streams``);
 * one workspace, sized for the largest group's split-K need
   (``qconv_group_workspace``), lets small launches split their K reduction
   over more workgroups (``qconv_run_group_ws``);
