@@ -231,6 +231,21 @@ typedef struct {
 aqd_status_t qadd_run(const qadd_desc_t *desc, const void *a, const void *b, void *y,
                       const qadd_params_t *dev_params, aqd_stream_t stream);
 
+/* Max-pooling of a code tensor (Sec. 3.2.4: the layer leaves its input's
+ * scale factor unchanged, so the codes are pooled directly):
+ *   y[n][i][j][c] = max of x[n][i*stride - pad + dy][j*stride - pad + dx][c]
+ *   over 0 <= dy, dx < k, skipping positions outside the input,
+ * ho = (h + 2*pad - k) / stride + 1, wo likewise (both >= 1; pad < k, so
+ * every window holds an input position). x: device [n][h][w][c] codes of
+ * `bits` in {2, 4, 8}; y: device [n][ho][wo][c], same width; c * bits a
+ * multiple of 8; y must not overlap x. 1 <= k <= 7, 1 <= stride <= 4. */
+typedef struct {
+    int n, h, w, c, bits, k, stride, pad;
+} aqd_maxpool_desc_t;
+
+aqd_status_t aqd_maxpool_run(const aqd_maxpool_desc_t *desc, const void *x, void *y,
+                             aqd_stream_t stream);
+
 /* Exact per-channel sums of an int32 tensor [rows][c] on the device:
  * sums[ch] += sum_r v[r][ch], sums[c + ch] += sum_r v[r][ch]^2 (int64,
  * accumulated into the caller's zeroed array). These are the statistics a

@@ -199,6 +199,34 @@ def qadd(a, b, up2, skip_c, skip_d, skip_side, mult, shift, bits_out):
     return out
 
 
+def maxpool(x, k, stride, pad):
+    """Max-pooling of codes (Sec. 3.2.4: the layer leaves the scale factor
+    unchanged, so the codes are pooled as they are). x: [n, h, w, c] codes;
+    y[n, i, j, c] = max of x over the k x k window whose top-left input
+    position is (i * stride - pad, j * stride - pad); positions outside the
+    input are skipped. Returns int64 [n, ho, wo, c]."""
+    x = _i64(x)
+    n, h, w, c = x.shape
+    ho = (h + 2 * pad - k) // stride + 1
+    wo = (w + 2 * pad - k) // stride + 1
+    assert ho >= 1 and wo >= 1
+    out = np.full((n, ho, wo, c), -1, dtype=np.int64)
+    for dy in range(k):
+        ih = np.arange(ho) * stride - pad + dy
+        vi = (ih >= 0) & (ih < h)
+        for dx in range(k):
+            iw = np.arange(wo) * stride - pad + dx
+            vj = (iw >= 0) & (iw < w)
+            if not vi.any() or not vj.any():
+                continue
+            win = x[:, ih[vi]][:, :, iw[vj]]               # [n, |vi|, |vj|, c]
+            sub = out[:, vi][:, :, vj]
+            out[np.ix_(np.arange(n), np.nonzero(vi)[0], np.nonzero(vj)[0], np.arange(c))] = \
+                np.maximum(sub, win)
+    assert (out >= 0).all(), "every window holds at least one input position"
+    return out
+
+
 def rsm_array(a, c, d):
     """RSM over arrays via the C code; returns Python ints (exact)."""
     a, c = _i64(a).ravel(), _i64(c).ravel()

@@ -53,6 +53,10 @@ class QaddDesc(ctypes.Structure):
                                      "hb", "wb")]
 
 
+class MaxpoolDesc(ctypes.Structure):
+    _fields_ = [(n, c_int) for n in ("n", "h", "w", "c", "bits", "k", "stride", "pad")]
+
+
 class QaddParams(ctypes.Structure):
     _fields_ = [(n, c_void_p) for n in ("skip_c", "skip_d", "skip_side", "mult", "shift")]
 
@@ -78,6 +82,7 @@ def lib():
             "qconv_destroy": ([vp], None),
             "qadd_run": ([POINTER(QaddDesc), vp, vp, vp, POINTER(QaddParams), vp], st),
             "aqd_channel_sums": ([vp, c_int64, i, vp, vp], st),
+            "aqd_maxpool_run": ([POINTER(MaxpoolDesc), vp, vp, vp], st),
             "aqd_graph_begin": ([vp], st),
             "aqd_graph_end": ([vp, POINTER(c_void_p)], st),
             "aqd_graph_launch": ([vp, vp], st),
@@ -103,7 +108,7 @@ def lib():
 def exported_symbols():
     return ["qconv_create", "qconv_out_shape", "qconv_run", "qconv_run_group",
             "qconv_group_workspace", "qconv_run_group_ws", "qconv_run_proj", "qconv_destroy",
-            "qadd_run", "aqd_channel_sums", "aqd_graph_begin", "aqd_graph_end",
+            "qadd_run", "aqd_maxpool_run", "aqd_channel_sums", "aqd_graph_begin", "aqd_graph_end",
             "aqd_graph_launch", "aqd_graph_destroy", "aqd_last_error", "aqd_pack_codes",
             "aqd_unpack_codes", "aqd_approx_ratio", "aqd_normalize_multiplier",
             "aqd_bn_stats_from_sums", "aqd_fold_bn", "aqd_skip_params", "aqd_requant_params"]
@@ -220,6 +225,12 @@ def qadd_run(n, h, w, c, bits_a, bits_b, bits_out, up2, hb, wb, a, b, y, params,
 
 def channel_sums(v, rows, c, sums, stream=None):
     _check(lib().aqd_channel_sums(_addr(v), rows, c, _addr(sums), _stream(stream)))
+
+
+def maxpool_run(n, h, w, c, bits, k, stride, pad, x, y, stream=None):
+    """Max-pooling of a code tensor (see aqd.h)."""
+    d = MaxpoolDesc(n, h, w, c, bits, k, stride, pad)
+    _check(lib().aqd_maxpool_run(ctypes.byref(d), _addr(x), _addr(y), _stream(stream)))
 
 
 def graph_begin(stream):

@@ -886,6 +886,45 @@ aqd_status_t aqd_channel_sums(const int32_t *v, int64_t rows, int c, int64_t *su
     return AQD_OK;
 }
 
+aqd_status_t aqd_maxpool_run(const aqd_maxpool_desc_t *desc, const void *x, void *y,
+                             aqd_stream_t stream)
+{
+    REQUIRE(desc, "null argument");
+    const aqd_maxpool_desc_t d = *desc;
+    REQUIRE(d.n >= 0 && d.h >= 1 && d.w >= 1 && d.c >= 1, "bad tensor shape");
+    REQUIRE(code_bits(d.bits), "bits must be 2, 4 or 8");
+    REQUIRE((d.c * d.bits) % 8 == 0, "c * bits must be a multiple of 8");
+    REQUIRE(d.k >= 1 && d.k <= 7 && d.stride >= 1 && d.stride <= 4 && d.pad >= 0 && d.pad < d.k,
+            "k must be in 1..7, stride in 1..4, pad in 0..k-1");
+    const int ho = (d.h + 2 * d.pad - d.k) / d.stride + 1;
+    const int wo = (d.w + 2 * d.pad - d.k) / d.stride + 1;
+    REQUIRE(d.h + 2 * d.pad >= d.k && d.w + 2 * d.pad >= d.k && ho >= 1 && wo >= 1,
+            "input smaller than the window");
+    REQUIRE((long long)d.n * d.h * d.w < (1LL << 31), "too many pixels for one call");
+    if (d.n == 0)
+        return AQD_OK;
+    REQUIRE(x && y, "null tensor");
+    const size_t xb = (size_t)d.n * d.h * d.w * d.c * d.bits / 8;
+    const size_t yb = (size_t)d.n * ho * wo * d.c * d.bits / 8;
+    REQUIRE(!overlap(y, yb, x, xb), "output overlaps the input");
+    PoolArgs a{};
+    a.x = (const uint8_t *)x;
+    a.y = (uint8_t *)y;
+    a.n = d.n;
+    a.h = d.h;
+    a.w = d.w;
+    a.c = d.c;
+    a.bits = d.bits;
+    a.k = d.k;
+    a.stride = d.stride;
+    a.pad = d.pad;
+    a.ho = ho;
+    a.wo = wo;
+    if (launch_maxpool(a, (hipStream_t)stream) != hipSuccess)
+        return fail(AQD_ERR_DEVICE, "max-pooling launch failed");
+    return AQD_OK;
+}
+
 // ------------------------------------------------------------------ graph capture
 aqd_status_t aqd_graph_begin(aqd_stream_t stream)
 {

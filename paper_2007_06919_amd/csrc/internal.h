@@ -118,6 +118,14 @@ struct QaddArgs {
 };
 hipError_t launch_qadd(const QaddArgs &a, hipStream_t stream);
 
+// ---- max-pooling (qpool.hip) --------------------------------------------------
+struct PoolArgs {
+    const uint8_t *x;
+    uint8_t *y;
+    int n, h, w, c, bits, k, stride, pad, ho, wo;
+};
+hipError_t launch_maxpool(const PoolArgs &a, hipStream_t stream);
+
 // ---- per-channel sums (qadd.hip) ----------------------------------------------
 hipError_t launch_channel_sums(const int32_t *v, long long rows, int c, long long *sums,
                                hipStream_t stream);

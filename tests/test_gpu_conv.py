@@ -191,6 +191,44 @@ def test_stream_grouped_segments(torch):
             aqd.qconv_destroy(h)
 
 
+@pytest.mark.parametrize("bits,k,stride,pad,shape", [
+    (4, 3, 2, 1, (2, 37, 41, 64)),      # ResNet stem pooling on 4-bit codes
+    (8, 3, 2, 1, (1, 25, 30, 16)),
+    (2, 2, 2, 0, (3, 17, 19, 32)),
+    (4, 5, 1, 2, (1, 9, 8, 6)),         # 6 channels: three bytes per pixel
+    (8, 7, 3, 3, (1, 20, 22, 3)),       # 3-channel 8-bit input
+])
+def test_maxpool_parity(torch, bits, k, stride, pad, shape):
+    dev = torch.device("cuda:0")
+    rng = np.random.Generator(np.random.PCG64(bits * 1000 + k * 10 + stride))
+    n, h, w, c = shape
+    x = rng.integers(0, 1 << bits, size=shape)
+    want = ref.pack_codes(ref.maxpool(x, k, stride, pad), bits)
+    xd = torch.from_numpy(aqd.pack_codes(x, bits)).to(dev)
+    yd = torch.full(want.shape, 0xA5, dtype=torch.uint8, device=dev)
+    aqd.maxpool_run(n, h, w, c, bits, k, stride, pad, xd, yd)
+    torch.cuda.synchronize()
+    assert_same(yd.cpu().numpy(), want, f"maxpool {bits} {k} {stride} {pad} {shape}")
+
+
+def test_stem_8bit_conv_then_pool(torch):
+    """The 8-bit input layer of a fully quantized ResNet: 7x7 stride 2 conv of a
+    3-channel 8-bit image (direct kernel) to 4-bit codes, then 3x3 stride 2
+    max-pooling, against the oracle's conv and pooling."""
+    dev = torch.device("cuda:0")
+    case = workloads.random_conv_case(seed=31, n=1, h=67, w=81, cin=3, cout=64, k=7, stride=2,
+                                      bits_in=8, bits_w=8, bits_out=4)
+    conv = gpu_conv(case, torch)[0]
+    assert_same(conv, oracle_conv(case, 0), "stem conv")
+    ho, wo = case.out_hw
+    want = ref.pack_codes(ref.maxpool(ref.unpack_codes(oracle_conv(case, 0), 4, 64).reshape(
+        1, ho, wo, 64), 3, 2, 1), 4)
+    yd = torch.full(want.shape, 0xA5, dtype=torch.uint8, device=dev)
+    aqd.maxpool_run(1, ho, wo, 64, 4, 3, 2, 1, torch.from_numpy(conv).to(dev), yd)
+    torch.cuda.synchronize()
+    assert_same(yd.cpu().numpy(), want, "stem pooling")
+
+
 DIRECT_CASES = [
     (1, 9, 10, 32, 16, 3, 1, 4, 4, 0, 4, 0, False),         # cin not a multiple of 64
     (2, 8, 7, 16, 12, 3, 2, 8, 4, 0, 8, 0, False),          # 8-bit activations

@@ -412,3 +412,30 @@ def test_bn_stats_from_sums():
     flat = acc.reshape(-1, 24).astype(np.float64)
     assert np.allclose(mean, 0.25 * flat.mean(0), rtol=1e-12, atol=1e-9)
     assert np.allclose(var, 0.0625 * flat.var(0), rtol=1e-9)
+
+
+# ---- max-pooling (Sec. 3.2.4) -------------------------------------------------
+@pytest.mark.parametrize("k,stride,pad", [(3, 2, 1), (2, 2, 0), (3, 1, 1), (5, 3, 2), (1, 1, 0)])
+def test_maxpool_equals_torch_max_pool2d(k, stride, pad):
+    """The library routine (float64 on the CPU, padding ignored as -inf) on
+    integer codes is exact."""
+    rng = np.random.default_rng(k * 100 + stride * 10 + pad)
+    x = rng.integers(0, 256, size=(2, 13, 11, 6))
+    want = torch.nn.functional.max_pool2d(torch.from_numpy(x).permute(0, 3, 1, 2).double(), k,
+                                          stride, pad).permute(0, 2, 3, 1).numpy().astype(np.int64)
+    assert np.array_equal(ref.maxpool(x, k, stride, pad), want)
+
+
+def test_maxpool_brute_force_tiny_and_identity():
+    rng = np.random.default_rng(7)
+    x = rng.integers(0, 16, size=(1, 5, 4, 3))
+    got = ref.maxpool(x, 3, 2, 1)
+    ho, wo = (5 + 2 - 3) // 2 + 1, (4 + 2 - 3) // 2 + 1
+    assert got.shape == (1, ho, wo, 3)
+    for i in range(ho):
+        for j in range(wo):
+            for c in range(3):
+                vals = [x[0, i * 2 - 1 + dy, j * 2 - 1 + dx, c] for dy in range(3) for dx in range(3)
+                        if 0 <= i * 2 - 1 + dy < 5 and 0 <= j * 2 - 1 + dx < 4]
+                assert got[0, i, j, c] == max(vals)
+    assert np.array_equal(ref.maxpool(x, 1, 1, 0), x)
