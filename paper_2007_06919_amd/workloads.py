@@ -205,6 +205,41 @@ def add_retina_heads(net: NetSpec, levels, bits, towers=("cls", "box")):
         net.outputs.extend(ys)
 
 
+def add_fcos_heads(net: NetSpec, levels, bits):
+    """FCOS heads (the paper's second detector, Table 4), shared over the
+    pyramid levels with a private epilogue table per level: a class tower and
+    a box tower of four 3x3 256->256 convs each; predictions (int32) of the
+    per-location class scores (NUM_CLASSES), box distances (4) and
+    centerness (1, from the box tower)."""
+    tops = {}
+    for tower in ("cls", "box"):
+        xs = list(levels)
+        for i in range(1, 5):
+            ys = [f"{tower}{i}.{lv}" for lv in levels]
+            net.conv_levels(f"{tower}.t{i}", xs, ys, 256, 3, bits, bits)
+            xs = ys
+        tops[tower] = xs
+    for name, tower, cout in (("cls.pred", "cls", NUM_CLASSES), ("box.pred", "box", 4),
+                              ("ctr.pred", "box", 1)):
+        ys = [f"{name.split('.')[0]}_out.{lv}" for lv in levels]
+        net.conv_levels(name, tops[tower], ys, cout, 3, bits, 32)
+        net.outputs.extend(ys)
+
+
+def fcos_r50_net(n, h, w, bits, wenc=WENC_PAPER_ODD) -> NetSpec:
+    """ResNet-50 + FPN (as retinanet_r50_net) with the FCOS heads."""
+    net = retinanet_r50_net(n, h, w, bits, heads=False, wenc=wenc)
+    net.outputs.clear()
+    add_fcos_heads(net, LEVELS, bits)
+    return net
+
+
+def fcos_config(n, h, w, bits=4, seed=5):
+    """(NetSpec, NetParams) of the FCOS network, calibrated recipe."""
+    net = fcos_r50_net(n, h, w, bits)
+    return net, make_params(net, seed, "calibrated")
+
+
 def head_tower_net(n, h, w, bits, wenc=WENC_PAPER_ODD) -> NetSpec:
     """Class tower of the RetinaNet head on the five pyramid levels of an
     h x w image: four 3x3 256->256 convs and the 3x3 256->720 prediction."""

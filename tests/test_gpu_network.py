@@ -117,3 +117,11 @@ def test_graph_replay_matches_eager(torch):
                     assert_same(gpu.raw(n), want[n], f"replay {r}: {n}")
     finally:
         gpu.close()
+
+
+def test_fcos_scaled(torch):
+    """The FCOS heads (the paper's second detector) on ResNet-50 + FPN at a
+    reduced image size: every tensor and epilogue table against the oracle
+    (the 1-channel centerness prediction runs on the direct kernel)."""
+    net, params = workloads.fcos_config(1, 192, 256)
+    compare_network(torch, net, params)

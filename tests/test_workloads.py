@@ -65,3 +65,17 @@ def test_calibrated_network_keeps_codes_spread_and_bn_centered():
         q = (1 << t.bits) - 1
         interior = np.mean((a > 0) & (a < q))
         assert interior > 0.2, (name, interior)
+
+
+def test_fcos_wiring():
+    """FCOS heads on the ResNet-50 + FPN network: two towers of four 3x3
+    256-channel convs over P3-P7, int32 predictions of 80 class scores, 4 box
+    distances and 1 centerness per location."""
+    net = W.fcos_r50_net(1, 192, 256, 4)
+    preds = {c.name: c for c in net.convs if c.name.endswith(".pred")}
+    assert {n: c.cout for n, c in preds.items()} == {"cls.pred": 80, "box.pred": 4, "ctr.pred": 1}
+    assert all(len(c.segs) == 5 and c.k == 3 for c in preds.values())
+    assert all(net.tensors[y].bits == 32 for c in preds.values() for _, _, y in c.segs)
+    towers = [c for c in net.convs if ".t" in c.name]
+    assert len(towers) == 8 and all(c.cin == c.cout == 256 and len(c.segs) == 5 for c in towers)
+    assert len(net.outputs) == 15 and len(net.convs) == 60 + 11
