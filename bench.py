@@ -29,8 +29,8 @@ COPY_PROBE_BYTES = 256 << 20
 # HBM traffic of one head-tower launch, from two rocprofv3 counter runs
 # (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain copy of
 # COPY_PROBE_BYTES; valid only for the kernel source it was measured on.
-HEAD_TRAFFIC = {"kernel_sha256": "ff28c3fc2fcfc2af28c28cfd1eb9802018f86e0ffb12fa1a1c42f05c186f8c43",
-                "fetch_bytes": 50970624, "write_bytes": 45670400}
+HEAD_TRAFFIC = {"kernel_sha256": "f0ef2a4cabea8514d4443af953175ec73499b7084a3b7171fee3709ae9566ef2",
+                "fetch_bytes": 50956902, "write_bytes": 45670400}
 
 
 def kernel_sha256():

@@ -489,6 +489,9 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
     // splitting K is the better cure) on 256 x 64 tiles two to a CU (measured:
     // from ~260 tiles on, the larger tile is faster)
     int tile_cfg = h0.tile_cfg, blk_px = h0.blk_px;
+    long long t_handle = 0;  // tiles at the handle's own tile shape
+    for (int i = 0; i < count; ++i)
+        t_handle += ((long long)segs[i].n * chk[i].ho * chk[i].wo + h0.blk_px - 1) / h0.blk_px * h0.co_tiles;
     if (h0.tile_cfg == TILE_256x128) {
         long long t128 = 0;
         for (int i = 0; i < count; ++i)
@@ -514,6 +517,10 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         // persistent streaming tiles (weights resident in LDS)
         tile_cfg = h0.tile_cfg == TILE_128x256 ? TILE_STREAM_C128 : TILE_STREAM_C64;
         blk_px = h0.tile_cfg == TILE_128x256 ? 64 : 128;
+    } else if ((h0.tile_cfg == TILE_128x256 || h0.tile_cfg == TILE_64x512) && t_handle > 256 && h0.d.bits_in == 4 &&
+               h0.d.skip_bits == 0 && (h0.d.out_mode == AQD_OUT_INT32 || h0.d.bits_out == 4)) {
+        tile_cfg = h0.tile_cfg == TILE_128x256 ? TILE_128x128_O3 : TILE_64x256_O3;
+        blk_px = h0.tile_cfg == TILE_128x256 ? 128 : 256;
     }
     int tiles = 0;
     for (int i = 0; i < count; ++i) {
@@ -575,7 +582,8 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
 void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
 {
     if (a.tile_cfg == TILE_256x64S || a.tile_cfg == TILE_256x64 || a.tile_cfg == TILE_STREAM ||
-        a.tile_cfg == TILE_STREAM_C128 || a.tile_cfg == TILE_STREAM_C64) {  // never split
+        a.tile_cfg == TILE_STREAM_C128 || a.tile_cfg == TILE_STREAM_C64 || a.tile_cfg == TILE_128x128_O3 ||
+        a.tile_cfg == TILE_64x256_O3) {  // never split
         *nparts = 1;
         *kchunk = a.ksteps;
         return;

@@ -18,7 +18,9 @@ enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
        TILE_STREAM = 5,    // 1x1, cin <= 128, code outputs: persistent 256 x 64 tiles
        // 1x1, cin <= 256, code outputs, no skip, for handles laid out for 128-
        // and 64-channel tiles: persistent 128 x 64 and 64 x 128 tiles
-       TILE_STREAM_C128 = 6, TILE_STREAM_C64 = 7 };
+       TILE_STREAM_C128 = 6, TILE_STREAM_C64 = 7,
+       // half-width pixel tiles, three workgroups per CU, on 128/64-channel handles
+       TILE_128x128_O3 = 8, TILE_64x256_O3 = 9 };
 constexpr int KC = 64;
 
 // tile shape of a configuration, and the channels one lane holds per pixel

@@ -1075,7 +1075,7 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
     }
 }
 
-template <int BI, int MI, int NJ, int WC, int WP, int OUTK, int SKK>
+template <int BI, int MI, int NJ, int WC, int WP, int OUTK, int SKK, int OCC = 0>
 hipError_t launch_t(const MfmaArgs &a, hipStream_t stream)
 {
     dim3 grid(8 * a.tiles_per_xcd), block(64 * WC * WP);
@@ -1083,10 +1083,24 @@ hipError_t launch_t(const MfmaArgs &a, hipStream_t stream)
     for (int i = 0; i < a.nseg; ++i)
         fast = fast && a.seg[i].fast;
     if (OUTK == 1 || fast)
-        hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, WP, OUTK, SKK, 1>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, WP, OUTK, SKK, 1, 0, OCC>), grid, block, 0, stream, a);
     else
-        hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, WP, OUTK, SKK, 0>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((qconv_mfma_kernel<BI, MI, NJ, WC, WP, OUTK, SKK, 0, 0, OCC>), grid, block, 0, stream, a);
     return hipGetLastError();
+}
+
+// half-width pixel tiles, three workgroups per CU, for handles laid out for
+// 128- and 64-channel tiles (same weight layout): outputs without skip
+template <int MI, int NJ, int WC, int WP>
+hipError_t launch_occ3(const MfmaArgs &a, hipStream_t stream)
+{
+    if (a.skip_bits != 0)
+        return hipErrorInvalidValue;
+    if (a.bits_out == 32)
+        return launch_t<4, MI, NJ, WC, WP, 1, 0, 3>(a, stream);
+    if (a.bits_out != 4)
+        return hipErrorInvalidValue;
+    return launch_t<4, MI, NJ, WC, WP, 0, 0, 3>(a, stream);
 }
 
 template <int BI, int MI, int NJ, int WC, int WP>
@@ -1116,6 +1130,8 @@ void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane)
     case TILE_STREAM: *blk_co = 256; *blk_px = 64; *chan_per_lane = 32; return;
     case TILE_STREAM_C128: *blk_co = 128; *blk_px = 64; *chan_per_lane = 16; return;
     case TILE_STREAM_C64: *blk_co = 64; *blk_px = 128; *chan_per_lane = 16; return;
+    case TILE_128x128_O3: *blk_co = 128; *blk_px = 128; *chan_per_lane = 16; return;
+    case TILE_64x256_O3: *blk_co = 64; *blk_px = 256; *chan_per_lane = 16; return;
     case TILE_128x256: *blk_co = 128; *blk_px = 256; *chan_per_lane = 16; return;
     default: *blk_co = 64; *blk_px = 512; *chan_per_lane = 16; return;
     }
@@ -1227,6 +1243,8 @@ hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
         case TILE_STREAM:
         case TILE_STREAM_C128:
         case TILE_STREAM_C64: return launch_qconv_stream(a, stream);
+        case TILE_128x128_O3: return launch_occ3<4, 4, 2, 2>(a, stream);
+        case TILE_64x256_O3: return launch_occ3<4, 4, 1, 4>(a, stream);
         case TILE_128x256: return launch_modes<4, 4, 8, 2, 2>(a, stream);
         case TILE_64x512: return launch_modes<4, 4, 8, 1, 4>(a, stream);
         }

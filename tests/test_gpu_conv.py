@@ -153,6 +153,37 @@ def test_conv_stream_parity(torch, case, variant):
         assert_same(got, oracle_conv(c, level), f"stream {variant} {case} level {level}")
 
 
+# Launches of more than one round of 128 x 256 or 64 x 512 tiles without a
+# skip run on tiles half as wide, three workgroups to a CU: 1x1 and 3x3,
+# stride 2, int32 and code outputs, ragged pixel tails.
+OCC3_CASES = [
+    # (n, h, w, cin, cout, k, stride, bits_out)
+    (1, 363, 363, 64, 64, 1, 1, 32),        # 64 x 256 tiles, 258 handle tiles
+    (1, 257, 257, 64, 128, 1, 1, 32),       # 128 x 128 tiles, 259 handle tiles
+    (4, 182, 182, 64, 64, 3, 1, 4),         # 3x3 codes, 64-channel handle
+    (2, 182, 182, 64, 128, 3, 1, 4),        # 3x3 codes, 128-channel handle
+    (2, 363, 363, 64, 128, 3, 2, 4),        # stride 2
+    (4, 182, 182, 256, 36, 3, 1, 32),       # a box predictor: 36 of 64 channels
+    (1, 300, 500, 320, 64, 1, 1, 4),        # 1x1 with 5 K steps (not streamed)
+]
+
+
+@pytest.mark.parametrize("case", OCC3_CASES, ids=lambda c: "x".join(map(str, c)))
+@pytest.mark.parametrize("variant", ["plain", "small_shifts"])
+def test_conv_three_per_cu_parity(torch, case, variant):
+    """Shifts < 2 take the 64-bit requantisation."""
+    n, h, w, cin, cout, k, s, bo = case
+    c = workloads.random_conv_case(seed=hash(case) % 1000 + 41, n=n, h=h, w=w, cin=cin, cout=cout,
+                                   k=k, stride=s, bits_in=4, bits_w=4, wenc=1, bits_out=bo)
+    if variant == "small_shifts" and bo != 32:
+        rng = np.random.Generator(np.random.PCG64(23))
+        for lv in c.levels:
+            lv["shift"] = rng.integers(-2, 2, size=cout).astype(np.int32)
+            lv["mult"] = rng.integers(1 << 24, 1 << 27, size=cout).astype(np.int32)
+    for level, got in enumerate(gpu_conv(c, torch)):
+        assert_same(got, oracle_conv(c, level), f"three per CU {variant} {case} level {level}")
+
+
 def test_stream_grouped_segments(torch):
     """One launch over segments of two handles (weights and tables reloaded at
     each segment change) and two levels, with code skips."""
