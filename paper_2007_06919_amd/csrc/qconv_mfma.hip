@@ -822,11 +822,15 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
             const long long p = (long long)pq * BPX + ploc;
             const uint8_t *src = nullptr;
             if (p < S.P) {  // P < 2^31 (host): 32-bit index arithmetic
-                const int n_ = (int)p / hw;
-                const int rem = (int)p - n_ * hw;
-                const int oh = rem / S.wo, ow = rem - oh * S.wo;
-                src = S.x + (((long long)n_ * S.h + oh * A.stride) * S.w + ow * A.stride) * (A.cin * BI / 8) +
-                      16 * ((lane & 1) ^ swz_b4(ploc));
+                if (A.stride == 1) {  // 1x1, no padding: input pixel p
+                    src = S.x + p * (A.cin * BI / 8) + 16 * ((lane & 1) ^ swz_b4(ploc));
+                } else {
+                    const int n_ = (int)p / hw;
+                    const int rem = (int)p - n_ * hw;
+                    const int oh = rem / S.wo, ow = rem - oh * S.wo;
+                    src = S.x + (((long long)n_ * S.h + oh * A.stride) * S.w + ow * A.stride) * (A.cin * BI / 8) +
+                          16 * ((lane & 1) ^ swz_b4(ploc));
+                }
             }
             for (int k = 0; k < K; ++k)
                 if (PPW == 32 || lane < 2 * PPW)
@@ -836,11 +840,15 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
                 // the shortcut's input pixel (1x1, stride A.stride2, always inside x2)
                 const uint8_t *src2 = A.zero;
                 if (p < S.P) {
-                    const int n_ = (int)p / hw;
-                    const int rem = (int)p - n_ * hw;
-                    const int oh = rem / S.wo, ow = rem - oh * S.wo;
-                    src2 = S.x2 + (((long long)n_ * S.h2 + oh * A.stride2) * S.w2 + ow * A.stride2) *
-                                      (A.cin2 * BI / 8) + 16 * ((lane & 1) ^ swz_b4(ploc));
+                    if (A.stride2 == 1) {  // x2 has the output's size: pixel p
+                        src2 = S.x2 + p * (A.cin2 * BI / 8) + 16 * ((lane & 1) ^ swz_b4(ploc));
+                    } else {
+                        const int n_ = (int)p / hw;
+                        const int rem = (int)p - n_ * hw;
+                        const int oh = rem / S.wo, ow = rem - oh * S.wo;
+                        src2 = S.x2 + (((long long)n_ * S.h2 + oh * A.stride2) * S.w2 + ow * A.stride2) *
+                                          (A.cin2 * BI / 8) + 16 * ((lane & 1) ^ swz_b4(ploc));
+                    }
                 }
                 if (lane < 32)
                     dma16(src2, lbase + OFF_B + (b * ST_KMAX + 1) * B_STEP + wave * 512);
