@@ -160,6 +160,24 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p)
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t *)p;
 }
 
+// a + byte b of w (b a constant once unrolled), one SDWA add: kept out of the
+// compiler's reach, which otherwise rebuilds the byte as a shift and a mask
+__device__ __forceinline__ uint32_t add_byte(uint32_t a, uint32_t w, int b)
+{
+    uint32_t r;
+    switch (b) {
+    case 0: asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
+                : "=v"(r) : "v"(a), "v"(w)); break;
+    case 1: asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
+                : "=v"(r) : "v"(a), "v"(w)); break;
+    case 2: asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2"
+                : "=v"(r) : "v"(a), "v"(w)); break;
+    default: asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
+                 : "=v"(r) : "v"(a), "v"(w)); break;
+    }
+    return r;
+}
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt()
 {
@@ -520,6 +538,7 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
     constexpr int QMAX = (1 << BI) - 1;
     int32_t *prm = (int32_t *)lds_stages;
     int32_t *lut = prm + EPI_FIELDS * C::BCO;            // [BCO][2^BI]: RSM(k, c, d)
+    const int32_t *lut_l = lut + (co_loc << BI);         // this lane's channels
     const bool use_lut = SKK == 1 && S.side0;            // uniform over the workgroup
     // skip codes: issued before the table goes to LDS, so that the two overlap
     uint32_t skw[NJ][C::OW];
@@ -665,7 +684,7 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const int bit = (4 * i + e) * BI;
-                        kv[e] = (int)((skw[j][bit >> 5] >> (bit & 31)) & QMAX);
+                        kv[e] = (int)__builtin_amdgcn_ubfe(skw[j][bit >> 5], bit & 31, BI);
                     }
                 }
 #pragma unroll
@@ -676,7 +695,7 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
                         int u = v;
                         // u fits in int32, so the sum modulo 2^32 is exact
                         if constexpr (LUT) {
-                            u = (int)((unsigned)v + (unsigned)lut[((cl + e) << BI) | kv[e]]);
+                            u = (int)((unsigned)v + (unsigned)lut_l[((4 * i + e) << BI) + kv[e]]);
                         } else if constexpr (SKK != 0) {
                             const int scaled = rsm32(sside[e] ? v : kv[e], sc[e], sd[e]);
                             u = (int)((unsigned)scaled + (unsigned)(sside[e] ? kv[e] : v));
@@ -686,7 +705,7 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
                     } else {
                         long long u = v;
                         if constexpr (LUT)
-                            u = (int)((unsigned)v + (unsigned)lut[((cl + e) << BI) | kv[e]]);
+                            u = (int)((unsigned)v + (unsigned)lut_l[((4 * i + e) << BI) + kv[e]]);
                         else if constexpr (SKK != 0)
                             u = align_add(v, kv[e], sc[e], sd[e], sside[e]);
                         y = (int)requant_clamp(u, mult[e], shf[e], QMAX);
@@ -995,6 +1014,8 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
         const long long px0 = (long long)pq * BPX + wp * TN + (lane & 15);
         const bool co_ok = co_glob < A.cout;
         const bool use_lut = SKK == 1 && S.side0;
+        const int32_t *lut_l = lut + (co_loc << BI);  // this lane's channels
+        const uint32_t lut_base = (uint32_t)(OFF_L + (co_loc << (BI + 2)));
         uint32_t outw[NJ][OW];
         uint32_t skw[NJ][OW];
 #pragma unroll
@@ -1014,6 +1035,16 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
         }
         auto body = [&](auto lut_c) {
             constexpr bool LUT = decltype(lut_c)::value;
+            // table byte offsets 4k of the skip codes, one per byte: even
+            // nibbles of each word in kev, odd ones in kod
+            uint32_t kev[NJ][OW], kod[NJ][OW];
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                for (int u = 0; u < OW; ++u) {
+                    kev[j][u] = (skw[j][u] << 2) & 0x3C3C3C3Cu;
+                    kod[j][u] = (skw[j][u] >> 2) & 0x3C3C3C3Cu;
+                }
             static_for<MI>([&](auto ic) {
                 constexpr int i = decltype(ic)::value;
                 const int cl = co_loc + 4 * i;
@@ -1043,16 +1074,23 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
                         const int v = acc[i][j][e];  // acc + bias
                         const int bit = (4 * i + e) * BI;
                         int kv = 0;
-                        if constexpr (SKK == 1)
-                            kv = (int)((skw[j][bit >> 5] >> (bit & 31)) & QMAX);
+                        if constexpr (SKK == 1 && !LUT)
+                            kv = (int)__builtin_amdgcn_ubfe(skw[j][bit >> 5], bit & 31, BI);
                         else if constexpr (SKK == 2)
                             kv = acc2[i][j][e];  // v2 = acc2 + bias2
+                        // the table entry of this channel and code (LUT)
+                        auto lut_at = [&]() {
+                            const int n = (4 * i + e) & 7;  // nibble in its word (a constant once unrolled)
+                            const uint32_t w = (n & 1) ? kod[j][bit >> 5] : kev[j][bit >> 5];
+                            const uint32_t a = add_byte(lut_base, w, n >> 1);
+                            return *(const int32_t *)((const uint8_t *)lds + a + ((4 * i + e) << (BI + 2)));
+                        };
                         int y;
                         if constexpr (FAST) {
                             int u = v;
                             // u fits in int32, so the sum modulo 2^32 is exact
                             if constexpr (LUT) {
-                                u = (int)((unsigned)v + (unsigned)lut[((cl + e) << BI) | kv]);
+                                u = (int)((unsigned)v + (unsigned)lut_at());
                             } else if constexpr (SKK != 0) {
                                 const int scaled = rsm32(sside[e] ? v : kv, sc[e], sd[e]);
                                 u = (int)((unsigned)scaled + (unsigned)(sside[e] ? kv : v));
@@ -1062,7 +1100,7 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
                         } else {
                             long long u = v;
                             if constexpr (LUT)
-                                u = (int)((unsigned)v + (unsigned)lut[((cl + e) << BI) | kv]);
+                                u = (int)((unsigned)v + (unsigned)lut_at());
                             else if constexpr (SKK != 0)
                                 u = align_add(v, kv, sc[e], sd[e], sside[e]);
                             y = (int)requant_clamp(u, mult[e], shf[e], QMAX);
