@@ -16,8 +16,12 @@
  * occupies bits (c*b) mod 8 .. (c*b) mod 8 + b - 1 of byte (c*b) div 8
  * (little-endian within a byte). Activation codes are unsigned, in
  * [0, 2^b - 1] (Eq. 2: the zero point is 0, so code 0 is the real 0 and zero
- * padding is code 0). An int32 tensor ("bits" = 32) stores one int32 per
- * element.
+ * padding is code 0). Bitwidth 3 (the paper's 3-bit networks, Tables 2 and 4)
+ * is stored like bitwidth 4, one code per 4-bit container (C/2 bytes per
+ * pixel, codes in [0, 7]); every width field below accepts 3 with that
+ * layout, and an output of width 3 is clamped to [0, 7]. Weight fields of
+ * width 3 sit in 4-bit containers too. An int32 tensor ("bits" = 32) stores
+ * one int32 per element.
  *
  * Integer rounding: RSM(a, c, d) = floor((a*c + 2^(d-1)) / 2^d) for d >= 1
  * and a*c for d = 0, i.e. a*c/2^d rounded to nearest with ties toward
@@ -89,16 +93,16 @@ enum { AQD_OUT_CODES = 0, AQD_OUT_INT32 = 1 };
 /* Description of one convolution layer (shared weights, one epilogue table
  * per level: multi-level BN, Sec. 3.2.2, Fig. 3). */
 typedef struct {
-    int cin, cout;     /* >= 1; cin*bits_in and cin*bits_w multiples of 8 */
+    int cin, cout;     /* >= 1; cin*bits_in and cin*bits_w multiples of 8 (stored widths) */
     int kh, kw;        /* 1..7 */
     int stride;        /* 1..4 */
     int pad;           /* 0..kh-1 (same for both axes) */
-    int bits_in;       /* activation code width: 2, 4 or 8 */
-    int bits_w;        /* weight field width: 2, 4 or 8 */
+    int bits_in;       /* activation code width: 2, 3, 4 or 8 */
+    int bits_w;        /* weight field width: 2, 3, 4 or 8 */
     int wenc;          /* AQD_WENC_* */
     int out_mode;      /* AQD_OUT_* */
-    int bits_out;      /* 2, 4 or 8 for AQD_OUT_CODES (cout*bits_out multiple of 8) */
-    int skip_bits;     /* 0: no skip; 2/4/8: code skip; 32: int32 skip (codes out only) */
+    int bits_out;      /* 2, 3, 4 or 8 for AQD_OUT_CODES (cout*bits_out multiple of 8) */
+    int skip_bits;     /* 0: no skip; 2/3/4/8: code skip; 32: int32 skip (codes out only) */
     int skip_up2;      /* 1: skip is the coarser map of a nearest 2x upsample */
     int num_levels;    /* number of epilogue tables, 1..64 */
 } qconv_desc_t;
@@ -214,8 +218,8 @@ void qconv_destroy(qconv_t conv);
  *   y[n][i][j][c] = clamp(RSM(u_, mult[c], 31 + shift[c]), 0, 2^bits_out - 1)
  *   u_ = side 0: a + RSM(b, c_[c], d[c]);  side 1: RSM(a, c_[c], d[c]) + b
  *   with b read at (i >> 1, j >> 1) when up2 (nearest 2x upsample, Sec. 3.2.4).
- * a: device [n][h][w][c] (bits_a in {2, 4, 8, 32}); b: device
- * [n][hb][wb][c] (bits_b in {2, 4, 8, 32}); y: device [n][h][w][c] codes.
+ * a: device [n][h][w][c] (bits_a in {2, 3, 4, 8, 32}); b: device
+ * [n][hb][wb][c] (bits_b in {2, 3, 4, 8, 32}); y: device [n][h][w][c] codes.
  * Without up2, hb == h and wb == w; with up2, (h-1)/2 < hb, (w-1)/2 < wb. */
 typedef struct {
     int n, h, w, c;
@@ -237,7 +241,7 @@ aqd_status_t qadd_run(const qadd_desc_t *desc, const void *a, const void *b, voi
  *   over 0 <= dy, dx < k, skipping positions outside the input,
  * ho = (h + 2*pad - k) / stride + 1, wo likewise (both >= 1; pad < k, so
  * every window holds an input position). x: device [n][h][w][c] codes of
- * `bits` in {2, 4, 8}; y: device [n][ho][wo][c], same width; c * bits a
+ * `bits` in {2, 3, 4, 8}; y: device [n][ho][wo][c], same width; c * bits a
  * multiple of 8; y must not overlap x. 1 <= k <= 7, 1 <= stride <= 4. */
 typedef struct {
     int n, h, w, c, bits, k, stride, pad;
@@ -286,7 +290,7 @@ const char *aqd_last_error(void);
  * order written. */
 
 /* Pack `rows` x c codes (one byte each, values < 2^bits) into the code tensor
- * layout; out has rows * c * bits / 8 bytes. */
+ * layout; out has rows * c * bits / 8 bytes (rows * c / 2 for bits 3). */
 aqd_status_t aqd_pack_codes(const uint8_t *codes, int64_t rows, int c, int bits, uint8_t *out);
 /* Inverse of aqd_pack_codes. */
 aqd_status_t aqd_unpack_codes(const uint8_t *packed, int64_t rows, int c, int bits, uint8_t *out);

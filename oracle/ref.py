@@ -98,30 +98,40 @@ def decode_weights(fields, bits, wenc=WENC_TWOS):
 
 
 # ----------------------------------------------------------------- packing
+def container_bits(bits):
+    """Bits one code occupies in a tensor: 3-bit codes (the paper's 3-bit
+    networks, Tables 2 and 4) sit in 4-bit containers, the others fill their
+    width."""
+    return 4 if bits == 3 else bits
+
+
 def pack_codes(codes, bits):
     """Pack b-bit codes along the last (channel) axis, little-endian within a
-    byte: channel j of a group of 8/b sits at bits j*b .. j*b+b-1."""
+    byte: channel j of a group of 8/s sits at bits j*s .. j*s+b-1, where s is
+    the container width (s = b, or 4 for b = 3)."""
     codes = np.asarray(codes)
     if bits == 8:
         return codes.astype(np.uint8)
-    per = 8 // bits
+    s = container_bits(bits)
+    per = 8 // s
     c = codes.shape[-1]
     assert c % per == 0, "channels * bits must be a multiple of 8"
     grp = codes.astype(np.uint32).reshape(codes.shape[:-1] + (c // per, per))
     out = np.zeros(grp.shape[:-1], dtype=np.uint32)
     for j in range(per):
-        out |= (grp[..., j] & qmax(bits)) << (j * bits)
+        out |= (grp[..., j] & qmax(bits)) << (j * s)
     return out.astype(np.uint8)
 
 
 def unpack_codes(packed, bits, c):
-    """Inverse of ``pack_codes``: [..., c*b/8] bytes -> [..., c] codes."""
+    """Inverse of ``pack_codes``: [..., c*s/8] bytes -> [..., c] codes."""
     packed = np.asarray(packed, dtype=np.uint8)
     if bits == 8:
         return packed.astype(np.int64)
-    per = 8 // bits
+    s = container_bits(bits)
+    per = 8 // s
     b = packed.astype(np.int64)
-    parts = [(b >> (j * bits)) & qmax(bits) for j in range(per)]
+    parts = [(b >> (j * s)) & qmax(bits) for j in range(per)]
     out = np.stack(parts, axis=-1)
     return out.reshape(packed.shape[:-1] + (c,))
 

@@ -254,18 +254,24 @@ def graph_destroy(graph):
 
 
 # ----------------------------------------------------------- host helpers
+def stored_bits(bits):
+    """Bits a code of width ``bits`` takes in a tensor (3-bit codes sit in
+    4-bit containers; int32 tensors: 32)."""
+    return 4 if bits == 3 else bits
+
+
 def pack_codes(codes, bits):
     codes = _host(codes, np.uint8)
     c = codes.shape[-1]
     rows = codes.size // c
-    out = np.empty(codes.shape[:-1] + (c * bits // 8,), np.uint8)
+    out = np.empty(codes.shape[:-1] + (c * stored_bits(bits) // 8,), np.uint8)
     _check(lib().aqd_pack_codes(codes.ctypes.data, rows, c, bits, out.ctypes.data))
     return out
 
 
 def unpack_codes(packed, bits, c):
     packed = _host(packed, np.uint8)
-    rows = packed.size // (c * bits // 8)
+    rows = packed.size // (c * stored_bits(bits) // 8)
     out = np.empty(packed.shape[:-1] + (c,), np.uint8)
     _check(lib().aqd_unpack_codes(packed.ctypes.data, rows, c, bits, out.ctypes.data))
     return out

@@ -34,7 +34,10 @@ aqd_status_t fail(aqd_status_t st, const std::string &msg)
             return fail(AQD_ERR_INVALID, (msg));      \
     } while (0)
 
-bool code_bits(int b) { return b == 2 || b == 4 || b == 8; }
+// code widths; 3-bit codes (Tables 2 and 4 of the paper) are stored one per
+// 4-bit container, so that every kernel reads them as 4-bit codes
+bool code_bits(int b) { return b == 2 || b == 3 || b == 4 || b == 8; }
+int stored_bits(int b) { return b == 3 ? 4 : b; }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -106,7 +109,8 @@ int weight_value(int field, int bits, int wenc)
 }  // namespace
 
 struct qconv_s {
-    qconv_desc_t d;
+    qconv_desc_t d;     // widths as stored (3-bit codes in 4-bit containers)
+    int qmax;           // largest output code, 2^bits_out - 1 of the caller's bits_out
     bool mfma;
     int tile_cfg, blk_co, blk_px;
     int co_tiles, ksteps, cout_pad;
@@ -129,21 +133,21 @@ static aqd_status_t validate_desc(const qconv_desc_t *d)
     REQUIRE(d->kh >= 1 && d->kh <= 7 && d->kw >= 1 && d->kw <= 7, "kh and kw must be in 1..7");
     REQUIRE(d->stride >= 1 && d->stride <= 4, "stride must be in 1..4");
     REQUIRE(d->pad >= 0 && d->pad < d->kh && d->pad < d->kw, "pad must be in 0..k-1");
-    REQUIRE(code_bits(d->bits_in), "bits_in must be 2, 4 or 8");
-    REQUIRE(code_bits(d->bits_w), "bits_w must be 2, 4 or 8");
+    REQUIRE(code_bits(d->bits_in), "bits_in must be 2, 3, 4 or 8");
+    REQUIRE(code_bits(d->bits_w), "bits_w must be 2, 3, 4 or 8");
     REQUIRE(d->wenc == AQD_WENC_TWOS || d->wenc == AQD_WENC_PAPER_ODD, "unknown weight grid");
     REQUIRE(d->out_mode == AQD_OUT_CODES || d->out_mode == AQD_OUT_INT32, "unknown output mode");
-    REQUIRE((d->cin * d->bits_in) % 8 == 0, "cin * bits_in must be a multiple of 8");
-    REQUIRE((d->cin * d->bits_w) % 8 == 0, "cin * bits_w must be a multiple of 8");
+    REQUIRE((d->cin * stored_bits(d->bits_in)) % 8 == 0, "cin * bits_in must be a multiple of 8");
+    REQUIRE((d->cin * stored_bits(d->bits_w)) % 8 == 0, "cin * bits_w must be a multiple of 8");
     if (d->out_mode == AQD_OUT_CODES) {
-        REQUIRE(code_bits(d->bits_out), "bits_out must be 2, 4 or 8");
-        REQUIRE((d->cout * d->bits_out) % 8 == 0, "cout * bits_out must be a multiple of 8");
+        REQUIRE(code_bits(d->bits_out), "bits_out must be 2, 3, 4 or 8");
+        REQUIRE((d->cout * stored_bits(d->bits_out)) % 8 == 0, "cout * bits_out must be a multiple of 8");
     }
     REQUIRE(d->skip_bits == 0 || code_bits(d->skip_bits) || d->skip_bits == 32,
-            "skip_bits must be 0, 2, 4, 8 or 32");
+            "skip_bits must be 0, 2, 3, 4, 8 or 32");
     if (d->skip_bits) {
         REQUIRE(d->out_mode == AQD_OUT_CODES, "a skip add needs code output");
-        REQUIRE((d->cout * d->skip_bits) % 8 == 0, "cout * skip_bits must be a multiple of 8");
+        REQUIRE((d->cout * stored_bits(d->skip_bits)) % 8 == 0, "cout * skip_bits must be a multiple of 8");
     }
     REQUIRE(d->skip_up2 == 0 || (d->skip_up2 == 1 && d->skip_bits), "skip_up2 needs a skip");
     REQUIRE(d->num_levels >= 1 && d->num_levels <= 64, "num_levels must be in 1..64");
@@ -158,8 +162,15 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
     aqd_status_t st = validate_desc(desc);
     if (st != AQD_OK)
         return st;
-    const qconv_desc_t d = *desc;
-    const bool codes = d.out_mode == AQD_OUT_CODES;
+    const qconv_desc_t dc = *desc;  // the caller's widths
+    const bool codes = dc.out_mode == AQD_OUT_CODES;
+    qconv_desc_t d = dc;             // stored widths
+    d.bits_in = stored_bits(dc.bits_in);
+    d.bits_w = stored_bits(dc.bits_w);
+    if (codes)
+        d.bits_out = stored_bits(dc.bits_out);
+    if (dc.skip_bits && dc.skip_bits != 32)
+        d.skip_bits = stored_bits(dc.skip_bits);
     for (int l = 0; l < d.num_levels; ++l) {
         const qconv_epilogue_t &e = levels[l];
         REQUIRE(e.bias, "epilogue bias is null");
@@ -179,8 +190,8 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
     }
     // accumulator bound: K * max code * max |weight| < 2^31
     const long long K = (long long)d.kh * d.kw * d.cin;
-    const long long wmax = d.wenc == AQD_WENC_PAPER_ODD ? (1 << d.bits_w) - 1 : (1 << (d.bits_w - 1));
-    if (K * ((1 << d.bits_in) - 1) * wmax >= (1LL << 31))
+    const long long wmax = dc.wenc == AQD_WENC_PAPER_ODD ? (1 << dc.bits_w) - 1 : (1 << (dc.bits_w - 1));
+    if (K * ((1 << dc.bits_in) - 1) * wmax >= (1LL << 31))
         return fail(AQD_ERR_UNSUPPORTED, "accumulator could exceed int32 for this K and bitwidths");
 
     // decode weight fields
@@ -192,21 +203,22 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
             const uint8_t *row = w_packed + ((size_t)co * taps + t) * wrow;
             for (int ci = 0; ci < d.cin; ++ci) {
                 int bit = ci * d.bits_w;
-                int f = (row[bit >> 3] >> (bit & 7)) & ((1 << d.bits_w) - 1);
-                wv[((size_t)co * taps + t) * d.cin + ci] = (int16_t)weight_value(f, d.bits_w, d.wenc);
+                int f = (row[bit >> 3] >> (bit & 7)) & ((1 << dc.bits_w) - 1);
+                wv[((size_t)co * taps + t) * d.cin + ci] = (int16_t)weight_value(f, dc.bits_w, d.wenc);
             }
         }
 
     // MFMA kernel: 2/4-bit activations, weights that fit int8, 64-channel K
     // steps, output and skip codes of the input's width; the direct kernel
     // takes everything else
-    const bool w_fits_i8 = d.bits_w <= 4 || d.wenc == AQD_WENC_TWOS;
+    const bool w_fits_i8 = dc.bits_w <= 4 || d.wenc == AQD_WENC_TWOS;
     const bool mfma = (d.bits_in == 2 || d.bits_in == 4) && d.cin % KC == 0 && w_fits_i8 &&
                       (codes ? (d.cout % 16 == 0 && d.bits_out == d.bits_in &&
                                 (d.skip_bits == 0 || d.skip_bits == d.bits_in || d.skip_bits == 32))
                              : d.cout % 4 == 0);
     qconv_s h{};
     h.d = d;
+    h.qmax = codes ? (1 << dc.bits_out) - 1 : 0;
     h.mfma = mfma;
     int cpl = 0;
     h.tile_cfg = pick_tile(d.cout, codes, d.bits_in);
@@ -217,7 +229,7 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
     h.ksteps = mfma ? taps * (d.cin / KC) : 0;
     h.fast.assign(d.num_levels, 0);
     h.side0.assign(d.num_levels, 0);
-    for (int l = 0; l < d.num_levels && d.skip_bits; ++l) {
+    for (int l = 0; l < d.num_levels && d.skip_bits; ++l) {  // (stored widths from here on)
         int ok = 1;
         for (int c = 0; c < d.cout; ++c)
             ok &= levels[l].skip_side[c] == 0;
@@ -437,6 +449,7 @@ aqd_status_t launch_direct(const qconv_seg_t &s, const SegCheck &c, hipStream_t 
     a.pad = h.d.pad;
     a.bits_in = h.d.bits_in;
     a.out_bits = h.d.out_mode == AQD_OUT_INT32 ? 32 : h.d.bits_out;
+    a.qmax = h.qmax;
     a.skip_bits = h.d.skip_bits;
     a.up2 = h.d.skip_up2;
     if (launch_qconv_direct(a, stream) != hipSuccess)
@@ -463,7 +476,7 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         aqd_status_t st = check_seg(segs[i], &chk[i]);
         if (st != AQD_OK)
             return st;
-        REQUIRE(same_config(segs[0].conv->d, segs[i].conv->d),
+        REQUIRE(same_config(segs[0].conv->d, segs[i].conv->d) && segs[0].conv->qmax == segs[i].conv->qmax,
                 "grouped handles must share shapes, bitwidths and modes");
     }
     for (int i = 0; i < count; ++i)
@@ -567,6 +580,7 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
     a.up2 = h0.d.skip_up2;
     a.tile_cfg = tile_cfg;
     a.bits_out = h0.d.out_mode == AQD_OUT_INT32 ? 32 : h0.d.bits_out;
+    a.qmax = h0.qmax;
     a.skip_bits = h0.d.skip_bits;
     a.zero = h0.zero;
     return AQD_OK;
@@ -689,6 +703,7 @@ aqd_status_t qconv_run_group_ws(int count, const qconv_seg_t *segs, void *worksp
     e.cout = a.cout;
     e.cout_pad = a.cout_pad;
     e.bits_out = a.bits_out;
+    e.qmax = a.qmax;
     e.skip_bits = a.skip_bits;
     e.up2 = a.up2;
     const int cpt = a.bits_out == 32 ? 4 : 32 / a.bits_out;
@@ -809,6 +824,7 @@ aqd_status_t qconv_run_proj(qconv_t conv, qconv_t proj, int level, int n, int h,
     a.up2 = 0;
     a.tile_cfg = conv->tile_cfg;
     a.bits_out = d.bits_out;
+    a.qmax = conv->qmax;
     a.skip_bits = 32;
     a.zero = conv->zero;
     a.cin2 = e.cin;
@@ -836,11 +852,15 @@ aqd_status_t qadd_run(const qadd_desc_t *desc, const void *a, const void *b, voi
                       const qadd_params_t *p, aqd_stream_t stream)
 {
     REQUIRE(desc && p, "null argument");
-    const qadd_desc_t d = *desc;
+    qadd_desc_t d = *desc;
     REQUIRE(d.n >= 0 && d.h >= 1 && d.w >= 1 && d.c >= 1, "bad tensor shape");
-    REQUIRE(code_bits(d.bits_a) || d.bits_a == 32, "bits_a must be 2, 4, 8 or 32");
-    REQUIRE(code_bits(d.bits_b) || d.bits_b == 32, "bits_b must be 2, 4, 8 or 32");
-    REQUIRE(code_bits(d.bits_out), "bits_out must be 2, 4 or 8");
+    REQUIRE(code_bits(d.bits_a) || d.bits_a == 32, "bits_a must be 2, 3, 4, 8 or 32");
+    REQUIRE(code_bits(d.bits_b) || d.bits_b == 32, "bits_b must be 2, 3, 4, 8 or 32");
+    REQUIRE(code_bits(d.bits_out), "bits_out must be 2, 3, 4 or 8");
+    const int qmax = (1 << d.bits_out) - 1;
+    d.bits_a = stored_bits(d.bits_a);  // widths as stored from here on
+    d.bits_b = stored_bits(d.bits_b);
+    d.bits_out = stored_bits(d.bits_out);
     REQUIRE((d.c * d.bits_a) % 8 == 0 && (d.c * d.bits_b) % 8 == 0 && (d.c * d.bits_out) % 8 == 0,
             "c * bits must be a multiple of 8");
     if (d.up2)
@@ -876,6 +896,7 @@ aqd_status_t qadd_run(const qadd_desc_t *desc, const void *a, const void *b, voi
     q.bits_a = d.bits_a;
     q.bits_b = d.bits_b;
     q.bits_out = d.bits_out;
+    q.qmax = qmax;
     q.up2 = d.up2;
     if (launch_qadd(q, (hipStream_t)stream) != hipSuccess)
         return fail(AQD_ERR_DEVICE, "qadd launch failed");
@@ -898,9 +919,10 @@ aqd_status_t aqd_maxpool_run(const aqd_maxpool_desc_t *desc, const void *x, void
                              aqd_stream_t stream)
 {
     REQUIRE(desc, "null argument");
-    const aqd_maxpool_desc_t d = *desc;
+    aqd_maxpool_desc_t d = *desc;
     REQUIRE(d.n >= 0 && d.h >= 1 && d.w >= 1 && d.c >= 1, "bad tensor shape");
-    REQUIRE(code_bits(d.bits), "bits must be 2, 4 or 8");
+    REQUIRE(code_bits(d.bits), "bits must be 2, 3, 4 or 8");
+    d.bits = stored_bits(d.bits);
     REQUIRE((d.c * d.bits) % 8 == 0, "c * bits must be a multiple of 8");
     REQUIRE(d.k >= 1 && d.k <= 7 && d.stride >= 1 && d.stride <= 4 && d.pad >= 0 && d.pad < d.k,
             "k must be in 1..7, stride in 1..4, pad in 0..k-1");
@@ -981,9 +1003,10 @@ void aqd_graph_destroy(void *graph_exec)
 // ------------------------------------------------------------------ host helpers
 aqd_status_t aqd_pack_codes(const uint8_t *codes, int64_t rows, int c, int bits, uint8_t *out)
 {
-    REQUIRE(codes && out && rows >= 0 && c >= 1 && code_bits(bits) && (c * bits) % 8 == 0,
+    REQUIRE(codes && out && rows >= 0 && c >= 1 && code_bits(bits) && (c * stored_bits(bits)) % 8 == 0,
             "bad arguments");
-    const int rb = c * bits / 8;
+    const int sb = stored_bits(bits);
+    const int rb = c * sb / 8;
     const int mask = (1 << bits) - 1;
     for (int64_t r = 0; r < rows; ++r) {
         uint8_t *o = out + r * rb;
@@ -991,7 +1014,7 @@ aqd_status_t aqd_pack_codes(const uint8_t *codes, int64_t rows, int c, int bits,
         for (int ch = 0; ch < c; ++ch) {
             const int v = codes[r * c + ch];
             REQUIRE(v <= mask, "code out of range for the bitwidth");
-            const int bit = ch * bits;
+            const int bit = ch * sb;
             o[bit >> 3] |= (uint8_t)(v << (bit & 7));
         }
     }
@@ -1000,12 +1023,13 @@ aqd_status_t aqd_pack_codes(const uint8_t *codes, int64_t rows, int c, int bits,
 
 aqd_status_t aqd_unpack_codes(const uint8_t *packed, int64_t rows, int c, int bits, uint8_t *out)
 {
-    REQUIRE(packed && out && rows >= 0 && c >= 1 && code_bits(bits) && (c * bits) % 8 == 0,
+    REQUIRE(packed && out && rows >= 0 && c >= 1 && code_bits(bits) && (c * stored_bits(bits)) % 8 == 0,
             "bad arguments");
-    const int rb = c * bits / 8;
+    const int sb = stored_bits(bits);
+    const int rb = c * sb / 8;
     for (int64_t r = 0; r < rows; ++r)
         for (int ch = 0; ch < c; ++ch) {
-            const int bit = ch * bits;
+            const int bit = ch * sb;
             out[r * c + ch] = (packed[r * rb + (bit >> 3)] >> (bit & 7)) & ((1 << bits) - 1);
         }
     return AQD_OK;

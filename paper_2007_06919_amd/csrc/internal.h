@@ -65,7 +65,8 @@ struct MfmaArgs {
     int cin, cout, cout_pad;
     int kh, kw, stride, pad;
     int co_tiles, ksteps;
-    int bits_out;        // 2, 4, 8 or 32 (int32 output)
+    int bits_out;        // 2, 4, 8 or 32 (int32 output), as stored
+    int qmax;            // largest output code (7 for 3-bit codes in 4-bit containers)
     int skip_bits;       // 0, 2, 4, 8 or 32
     int up2;
     const uint8_t *zero; // >= 16 zero bytes in device memory (source of padding taps)
@@ -94,6 +95,7 @@ struct SplitArgs {
     long long total_items;
     int nparts, cout, cout_pad;
     int bits_out, skip_bits, up2;  // bits_out 32: int32 output
+    int qmax;                      // largest output code
 };
 hipError_t launch_splitk_epilogue(const SplitArgs &a, hipStream_t stream);
 
@@ -107,6 +109,7 @@ struct DirectArgs {
     int n, h, w, ho, wo, hs, ws;
     int cin, cout, kh, kw, stride, pad;
     int bits_in, out_bits, skip_bits, up2;
+    int qmax;  // largest output code
 };
 hipError_t launch_qconv_direct(const DirectArgs &a, hipStream_t stream);
 
@@ -117,6 +120,7 @@ struct QaddArgs {
     const int32_t *skip_c, *skip_d, *skip_side, *mult, *shift;
     int n, h, w, c, hb, wb;
     int bits_a, bits_b, bits_out, up2;
+    int qmax;  // largest output code
 };
 hipError_t launch_qadd(const QaddArgs &a, hipStream_t stream);
 

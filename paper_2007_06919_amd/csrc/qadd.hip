@@ -34,7 +34,7 @@ __global__ void __launch_bounds__(256) qadd_kernel(QaddArgs A)
         const int y = rem / A.w, x = rem - y * A.w;
         bpix = ((long long)n * A.hb + (y >> 1)) * A.wb + (x >> 1);
     }
-    const int qmax = (1 << A.bits_out) - 1;
+    const int qmax = A.qmax;
     uint32_t packed = 0;
     for (int e = 0; e < per; ++e) {
         const int ch = grp * per + e;

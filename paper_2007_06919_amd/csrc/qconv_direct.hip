@@ -30,7 +30,7 @@ __global__ void __launch_bounds__(256) qconv_direct_kernel(DirectArgs A)
     const int row_bytes = A.cin * A.bits_in / 8;
     const int32_t *bias = A.epi, *mult = A.epi + A.cout, *shift = A.epi + 2 * A.cout;
     const int32_t *sc = A.epi + 3 * A.cout, *sd = A.epi + 4 * A.cout, *sside = A.epi + 5 * A.cout;
-    const int qmax = A.out_bits == 32 ? 0 : (1 << A.out_bits) - 1;
+    const int qmax = A.out_bits == 32 ? 0 : A.qmax;
 
     uint32_t packed = 0;
     for (int e = 0; e < per; ++e) {

@@ -178,6 +178,14 @@ __device__ __forceinline__ uint32_t add_byte(uint32_t a, uint32_t w, int b)
     return r;
 }
 
+// 3-bit outputs in 4-bit containers: min(code, 7) in each nibble of a word
+// of 4-bit codes already clamped to [0, 15] (a nibble >= 8 has bit 3 set)
+__device__ __forceinline__ uint32_t sat7_nibbles(uint32_t w)
+{
+    const uint32_t m = (w >> 3) & 0x11111111u;
+    return (w & ~((m << 4) - m)) | ((m << 3) - m);  // m * 15, m * 7 without carries
+}
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt()
 {
@@ -757,6 +765,13 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
         body(std::false_type{}, I0{}, INJ{});
     }
 
+    if (BI == 4 && A.qmax == 7) {  // 3-bit codes (the epilogue clamped to 15)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+            for (int u = 0; u < C::OW; ++u)
+                outw[j][u] = sat7_nibbles(outw[j][u]);
+    }
     static_for<NJ>([&](auto jc) {
         constexpr int j = decltype(jc)::value;
         if (okj[j])
@@ -1114,6 +1129,13 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
             body(std::true_type{});
         else
             body(std::false_type{});
+        if (A.qmax == 7) {  // 3-bit codes (the epilogue clamped to 15)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                for (int u = 0; u < OW; ++u)
+                    outw[j][u] = sat7_nibbles(outw[j][u]);
+        }
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
             if (co_ok && px0 + j * 16 < S.P)

@@ -63,7 +63,6 @@ __global__ void __launch_bounds__(256) splitk_epilogue_kernel(SplitArgs A)
             const int oh = rem / S.wo, ow = rem - oh * S.wo;
             spix = ((long long)n_ * S.hs + (oh >> 1)) * S.ws + (ow >> 1);
         }
-        constexpr int QMAX = (1 << BO) - 1;
         uint32_t word = 0;
 #pragma unroll
         for (int e = 0; e < CPT; ++e) {
@@ -79,7 +78,7 @@ __global__ void __launch_bounds__(256) splitk_epilogue_kernel(SplitArgs A)
                 u = align_add(v, k, S.epi[EPI_SKIP_C * A.cout_pad + c], S.epi[EPI_SKIP_D * A.cout_pad + c],
                               S.epi[EPI_SKIP_SIDE * A.cout_pad + c]);
             }
-            const uint32_t y = requant_clamp(u, S.epi[EPI_MULT * A.cout_pad + c], S.epi[EPI_SHIFT * A.cout_pad + c], QMAX);
+            const uint32_t y = requant_clamp(u, S.epi[EPI_MULT * A.cout_pad + c], S.epi[EPI_SHIFT * A.cout_pad + c], A.qmax);
             word |= y << (e * BO);
         }
         *(uint32_t *)((uint8_t *)S.y + px * (A.cout * BO / 8) + c0 * BO / 8) = word;

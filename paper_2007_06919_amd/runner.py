@@ -119,7 +119,7 @@ class Net:
             if t.bits == 32:
                 self.bufs[name] = torch.empty(t.shape, dtype=torch.int32, device=self.device)
             else:
-                self.bufs[name] = torch.empty((t.n, t.h, t.w, t.c * t.bits // 8), dtype=torch.uint8,
+                self.bufs[name] = torch.empty((t.n, t.h, t.w, t.c * aqd.stored_bits(t.bits) // 8), dtype=torch.uint8,
                                               device=self.device)
         for name in net.inputs:
             t = net.tensors[name]
@@ -171,8 +171,9 @@ class Net:
             d = producer.get(skip)
             if d is None or len(d.segs) != 1 or d.k != 1 or consumers.get(skip) != 1:
                 continue
-            if (net.tensors[x].bits != 4 or net.tensors[y].bits != 4 or conv.cout % 256 or
-                    net.tensors[d.segs[0][0]].bits != 4 or d.cin % 64 or conv.cin % 64):
+            sb = aqd.stored_bits
+            if (sb(net.tensors[x].bits) != 4 or sb(net.tensors[y].bits) != 4 or conv.cout % 256 or
+                    sb(net.tensors[d.segs[0][0]].bits) != 4 or d.cin % 64 or conv.cin % 64):
                 continue
             out[conv.name] = d
         return out

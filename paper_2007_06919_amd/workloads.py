@@ -422,6 +422,13 @@ def scaled_config(idx: int, n: int, h: int, w: int, seed: Optional[int] = None):
     return net, make_params(net, seed, "calibrated")
 
 
+def retinanet_config(n: int, h: int, w: int, bits: int, seed: int = 6):
+    """ResNet-50 + FPN + RetinaNet heads at any code width (3: the paper's
+    3-bit networks, Tables 2 and 4), calibrated, same recipe as workload 4."""
+    net = retinanet_r50_net(n, h, w, bits, heads=True)
+    return net, make_params(net, seed, "calibrated")
+
+
 # --------------------------------------------------------------------------
 # random single-conv cases (parity fuzzing)
 # --------------------------------------------------------------------------

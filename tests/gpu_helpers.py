@@ -31,7 +31,7 @@ def gpu_conv(case, torch, stream=None, split=False):
         if case.bits_out == 32:
             y = torch.full((case.n, ho, wo, case.cout), -7, dtype=torch.int32, device=dev)
         else:
-            y = torch.full((case.n, ho, wo, case.cout * case.bits_out // 8), 0xA5,
+            y = torch.full((case.n, ho, wo, case.cout * aqd.stored_bits(case.bits_out) // 8), 0xA5,
                            dtype=torch.uint8, device=dev)
         outs = []
         for level in range(len(case.levels)):

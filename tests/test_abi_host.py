@@ -62,7 +62,8 @@ def _create(desc, levels, w=None):
 
 
 @pytest.mark.parametrize("bad", [
-    dict(cin=0), dict(kh=9), dict(stride=0), dict(pad=3), dict(bits_in=3), dict(bits_w=1),
+    dict(cin=0), dict(kh=9), dict(stride=0), dict(pad=3), dict(bits_in=5), dict(bits_w=1),
+    dict(cin=3, bits_in=3), dict(bits_out=6),
     dict(wenc=5), dict(out_mode=2), dict(bits_out=16), dict(cin=3, bits_in=4),
     dict(cout=3, bits_out=2), dict(skip_bits=5), dict(skip_bits=4, out_mode=1, bits_out=0),
     dict(skip_up2=1), dict(num_levels=0), dict(num_levels=65),
@@ -111,7 +112,7 @@ def test_qadd_rejects_bad_descriptor():
 
 
 # ----------------------------------------------- packers and host helpers
-@pytest.mark.parametrize("bits", [2, 4, 8])
+@pytest.mark.parametrize("bits", [2, 3, 4, 8])
 def test_packers_agree_with_oracle(bits):
     rng = np.random.Generator(np.random.PCG64(bits))
     codes = rng.integers(0, 1 << bits, size=(5, 7, 64)).astype(np.uint8)

@@ -184,6 +184,56 @@ def test_conv_three_per_cu_parity(torch, case, variant):
         assert_same(got, oracle_conv(c, level), f"three per CU {variant} {case} level {level}")
 
 
+# 3-bit codes (stored in 4-bit containers, outputs clamped to 7) on every
+# launch path: 256 x 128 tiles with a code skip, 128- and 64-channel handles,
+# the streaming 1x1 kernel, the three-per-CU tiles, int32 predictions,
+# split K, the direct kernel, and 3-bit inputs with 4-bit outputs.
+THREE_BIT_CASES = [
+    # (n, h, w, cin, cout, k, stride, bits_in, bits_w, wenc, bits_out, skip_bits, up2)
+    (1, 19, 23, 128, 256, 3, 1, 3, 3, 1, 3, 3, False),      # 256 x 128, code skip
+    (2, 17, 13, 64, 512, 1, 2, 3, 3, 1, 3, 3, True),        # upsampled skip, stride 2
+    (1, 21, 18, 64, 128, 3, 1, 3, 3, 1, 3, 0, False),       # 128-channel handle
+    (1, 15, 22, 128, 64, 3, 2, 3, 3, 0, 3, 0, False),       # 64-channel handle
+    (2, 41, 52, 64, 256, 1, 1, 3, 3, 1, 3, 3, False),       # streaming 1x1 with skip
+    (2, 41, 52, 256, 128, 1, 1, 3, 3, 1, 3, 0, False),      # streaming 128 x 64
+    (1, 363, 363, 64, 64, 1, 1, 3, 3, 1, 3, 0, False),      # three per CU, 64 x 256
+    (1, 19, 23, 256, 720, 3, 1, 3, 3, 1, 32, 0, False),     # int32 class predictor
+    (1, 16, 18, 64, 256, 3, 1, 3, 3, 0, 3, 32, False),      # int32 skip
+    (1, 21, 19, 48, 96, 3, 1, 3, 3, 1, 3, 3, False),        # direct kernel (cin 48)
+    (1, 19, 23, 128, 256, 3, 1, 3, 3, 1, 4, 4, False),      # 3-bit in, 4-bit out
+]
+
+
+@pytest.mark.parametrize("case", THREE_BIT_CASES, ids=lambda c: "x".join(map(str, c)))
+@pytest.mark.parametrize("variant", ["random_sides", "side0", "small_shifts"])
+def test_three_bit_parity(torch, case, variant):
+    n, h, w, cin, cout, k, s, bi, bw, wenc, bo, sb, up2 = case
+    c = workloads.random_conv_case(seed=hash(case) % 1000 + 61, n=n, h=h, w=w, cin=cin, cout=cout,
+                                   k=k, stride=s, bits_in=bi, bits_w=bw, wenc=wenc, bits_out=bo,
+                                   skip_bits=sb, skip_up2=up2)
+    rng = np.random.Generator(np.random.PCG64(29))
+    for lv in c.levels:
+        if variant == "side0" and sb and sb != 32:
+            lv["skip_side"][:] = 0
+        if variant == "small_shifts" and bo != 32:
+            lv["shift"] = rng.integers(-2, 2, size=cout).astype(np.int32)
+            lv["mult"] = rng.integers(1 << 24, 1 << 27, size=cout).astype(np.int32)
+    for level, got in enumerate(gpu_conv(c, torch)):
+        want = oracle_conv(c, level)
+        assert_same(got, want, f"3-bit {variant} {case} level {level}")
+        if bo == 3 and variant != "small_shifts":  # the clamp at 7 is reached
+            codes = ref.unpack_codes(got, 4, cout)
+            assert codes.max() == 7
+
+
+def test_three_bit_split_k(torch):
+    """Split K with 3-bit codes: the combining epilogue clamps at 7."""
+    c = workloads.random_conv_case(seed=71, n=1, h=6, w=7, cin=448, cout=64, k=3, bits_in=3,
+                                   bits_w=3, wenc=1, bits_out=3, skip_bits=3)
+    got = gpu_conv(c, torch, split=True)
+    assert_same(got[0], oracle_conv(c, 0), "3-bit split K")
+
+
 def test_stream_grouped_segments(torch):
     """One launch over segments of two handles (weights and tables reloaded at
     each segment change) and two levels, with code skips."""
@@ -228,6 +278,7 @@ def test_stream_grouped_segments(torch):
     (2, 2, 2, 0, (3, 17, 19, 32)),
     (4, 5, 1, 2, (1, 9, 8, 6)),         # 6 channels: three bytes per pixel
     (8, 7, 3, 3, (1, 20, 22, 3)),       # 3-channel 8-bit input
+    (3, 3, 2, 1, (2, 21, 17, 32)),      # 3-bit codes in 4-bit containers
 ])
 def test_maxpool_parity(torch, bits, k, stride, pad, shape):
     dev = torch.device("cuda:0")
@@ -341,7 +392,8 @@ def test_run_is_deterministic_and_leaves_guard_bytes(torch):
 
 @pytest.mark.parametrize("bits_a,bits_b,bits_out,up2", [(4, 4, 4, True), (2, 2, 2, False),
                                                         (32, 4, 4, False), (4, 32, 8, True),
-                                                        (8, 2, 4, True)])
+                                                        (8, 2, 4, True), (3, 3, 3, True),
+                                                        (32, 3, 3, False)])
 def test_qadd_parity(torch, bits_a, bits_b, bits_out, up2):
     dev = torch.device("cuda:0")
     rng = np.random.Generator(np.random.PCG64(bits_a * 100 + bits_b))
@@ -366,7 +418,7 @@ def test_qadd_parity(torch, bits_a, bits_b, bits_out, up2):
         return torch.from_numpy(aqd.pack_codes(v, bits)).to(dev)
 
     pd = {k: torch.from_numpy(v.astype(np.int32)).to(dev) for k, v in p.items()}
-    y = torch.zeros((n, h, w, c * bits_out // 8), dtype=torch.uint8, device=dev)
+    y = torch.zeros((n, h, w, c * aqd.stored_bits(bits_out) // 8), dtype=torch.uint8, device=dev)
     aqd.qadd_run(n, h, w, c, bits_a, bits_b, bits_out, up2, hb, wb, dev_t(a, bits_a),
                  dev_t(b, bits_b), y, pd)
     torch.cuda.synchronize()

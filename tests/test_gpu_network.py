@@ -89,6 +89,15 @@ def test_config4_bench_configuration(torch):
     assert gpu.fused and gpu.ws_bytes > 0
 
 
+def test_three_bit_retinanet_scaled(torch):
+    """The RetinaNet-R50 network with 3-bit codes (4-bit containers, every
+    requantisation clamped at 7), calibrated: fused shortcuts, streaming and
+    three-per-CU tiles, side streams; every tensor and table."""
+    net, params = workloads.retinanet_config(2, 192, 256, 3)
+    gpu, _ = compare_network(torch, net, params)
+    assert gpu.fused
+
+
 def test_graph_replay_matches_eager(torch):
     """The network recorded once into a HIP graph (aqd_graph_*): three
     replays, each after the output buffers were overwritten by eager work and

@@ -60,15 +60,19 @@ def test_pack_layout_known_bytes():
     assert ref.pack_codes(np.array([[1, 2]]), 4).tolist() == [[0x21]]
     assert ref.pack_codes(np.array([[1, 2, 3, 0]]), 2).tolist() == [[0b00111001]]
     assert ref.pack_codes(np.array([[200, 7]]), 8).tolist() == [[200, 7]]
+    # 3-bit codes sit in 4-bit containers
+    assert ref.pack_codes(np.array([[1, 7, 5, 0]]), 3).tolist() == [[0x71, 0x05]]
 
 
-@pytest.mark.parametrize("bits", [2, 4, 8])
+@pytest.mark.parametrize("bits", [2, 3, 4, 8])
 def test_pack_roundtrip(bits):
     rng = _rng(bits)
     codes = rng.integers(0, 1 << bits, size=(3, 5, 7, 64))
     packed = ref.pack_codes(codes, bits)
-    assert packed.shape == (3, 5, 7, 64 * bits // 8)
+    assert packed.shape == (3, 5, 7, 64 * (4 if bits == 3 else bits) // 8)
     assert np.array_equal(ref.unpack_codes(packed, bits, 64), codes)
+    if bits == 3:  # the same bytes as 4-bit codes of the same values
+        assert np.array_equal(packed, ref.pack_codes(codes, 4))
 
 
 def test_weight_decode():
@@ -78,6 +82,9 @@ def test_weight_decode():
     # Eq. 3-4: the paper's odd grid 2*eta - (2^b - 1); b = 2 -> {-3, -1, 1, 3}
     assert ref.decode_weights(np.arange(4), 2, ref.WENC_PAPER_ODD).tolist() == [-3, -1, 1, 3]
     assert ref.decode_weights(f, 4, ref.WENC_PAPER_ODD).tolist() == list(range(-15, 16, 2))
+    # 3 bits: {-7, -5, ..., 7} on the odd grid, [-4, 3] in two's complement
+    assert ref.decode_weights(np.arange(8), 3, ref.WENC_PAPER_ODD).tolist() == list(range(-7, 8, 2))
+    assert ref.decode_weights(np.arange(8), 3, ref.WENC_TWOS).tolist() == [0, 1, 2, 3, -4, -3, -2, -1]
 
 
 # ------------------------------------------------------ Eq. 2 / 3 / 4
@@ -217,7 +224,7 @@ def _literal(rng, cout, skip=False):
     return p
 
 
-@pytest.mark.parametrize("bits_out", [2, 4, 8])
+@pytest.mark.parametrize("bits_out", [2, 3, 4, 8])
 def test_requant_matches_float_brute_force(bits_out):
     rng = _rng(20 + bits_out)
     x = rng.integers(0, 4, size=(1, 6, 7, 16))
@@ -336,6 +343,27 @@ def test_qadd_matches_float_brute_force():
     want = _float_epilogue(a, 0, p["mult"], p["shift"] - 8, 15, full, p["skip_c"], p["skip_d"],
                            p["skip_side"])
     assert np.array_equal(got, want)
+
+
+def test_three_bit_output_is_the_four_bit_output_clamped_to_7():
+    """Clamping is idempotent and monotone: with the same tables, a 3-bit
+    output (Eq. 2, codes in [0, 7]) is min(4-bit output, 7), for convs with
+    either skip side and for the standalone add."""
+    rng = _rng(47)
+    x = rng.integers(0, 8, size=(2, 7, 9, 32))
+    wf = rng.integers(0, 8, size=(16, 3, 3, 32))
+    skip = rng.integers(0, 8, size=(2, 7, 9, 16))
+    p = _literal(rng, 16, skip=True)
+    kw = dict(mult=p["mult"], shift=p["shift"] - 4, skip=skip, skip_c=p["skip_c"],
+              skip_d=p["skip_d"], skip_side=p["skip_side"], wenc=ref.WENC_PAPER_ODD)
+    y3 = ref.qconv(x, wf, 3, 1, 1, p["bias"], bits_out=3, **kw)
+    y4 = ref.qconv(x, wf, 3, 1, 1, p["bias"], bits_out=4, **kw)
+    assert np.array_equal(y3, np.minimum(y4, 7)) and 0 < (y3 == 7).mean() < 1
+    a3 = ref.qadd(x[..., :16], skip, False, p["skip_c"], p["skip_d"], p["skip_side"],
+                  p["mult"], p["shift"] - 8, 3)
+    a4 = ref.qadd(x[..., :16], skip, False, p["skip_c"], p["skip_d"], p["skip_side"],
+                  p["mult"], p["shift"] - 8, 4)
+    assert np.array_equal(a3, np.minimum(a4, 7))
 
 
 def test_int32_range_is_enforced():
