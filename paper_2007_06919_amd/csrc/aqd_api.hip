@@ -515,6 +515,11 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
             h0.d.cout % 256 == 0) {
             tile_cfg = TILE_STREAM;
             blk_px = 64;
+        } else if (short_codes && h0.d.kh == 1 && h0.d.kw == 1 && h0.d.pad == 0 && h0.d.cout % 256 == 0) {
+            // 3-4 K steps: the weights of a 256-row tile do not fit twice in
+            // LDS, its 128-row halves do (persistent 128 x 64 tiles)
+            tile_cfg = TILE_STREAM_H128;
+            blk_px = 64;
         } else if (short_codes) {
             tile_cfg = TILE_256x64S;
             blk_px = 64;
@@ -535,6 +540,8 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         tile_cfg = h0.tile_cfg == TILE_128x256 ? TILE_128x128_O3 : TILE_64x256_O3;
         blk_px = h0.tile_cfg == TILE_128x256 ? 128 : 256;
     }
+    // the half view splits each 256-channel tile in two
+    const int co_tiles = tile_cfg == TILE_STREAM_H128 ? 2 * h0.co_tiles : h0.co_tiles;
     int tiles = 0;
     for (int i = 0; i < count; ++i) {
         const qconv_seg_t &s = segs[i];
@@ -560,8 +567,8 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         m.lut = s.conv->lut_dev ? s.conv->lut_dev + (size_t)s.level * s.conv->cout_pad * (1 << h0.d.skip_bits)
                                 : nullptr;
         const long long px_tiles = (m.P + blk_px - 1) / blk_px;
-        REQUIRE(tiles + px_tiles * h0.co_tiles < (1LL << 26), "too many tiles for one launch");
-        tiles += (int)(px_tiles * h0.co_tiles);
+        REQUIRE(tiles + px_tiles * co_tiles < (1LL << 26), "too many tiles for one launch");
+        tiles += (int)(px_tiles * co_tiles);
     }
     a.total_tiles = tiles;
     a.tiles_per_xcd = (tiles + 7) / 8;
@@ -575,7 +582,7 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
     a.kw = h0.d.kw;
     a.stride = h0.d.stride;
     a.pad = h0.d.pad;
-    a.co_tiles = h0.co_tiles;
+    a.co_tiles = co_tiles;
     a.ksteps = h0.ksteps;
     a.up2 = h0.d.skip_up2;
     a.tile_cfg = tile_cfg;
@@ -597,7 +604,7 @@ void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
 {
     if (a.tile_cfg == TILE_256x64S || a.tile_cfg == TILE_256x64 || a.tile_cfg == TILE_STREAM ||
         a.tile_cfg == TILE_STREAM_C128 || a.tile_cfg == TILE_STREAM_C64 || a.tile_cfg == TILE_128x128_O3 ||
-        a.tile_cfg == TILE_64x256_O3) {  // never split
+        a.tile_cfg == TILE_64x256_O3 || a.tile_cfg == TILE_STREAM_H128) {  // never split
         *nparts = 1;
         *kchunk = a.ksteps;
         return;

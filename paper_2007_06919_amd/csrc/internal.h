@@ -20,7 +20,11 @@ enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
        // and 64-channel tiles: persistent 128 x 64 and 64 x 128 tiles
        TILE_STREAM_C128 = 6, TILE_STREAM_C64 = 7,
        // half-width pixel tiles, three workgroups per CU, on 128/64-channel handles
-       TILE_128x128_O3 = 8, TILE_64x256_O3 = 9 };
+       TILE_128x128_O3 = 8, TILE_64x256_O3 = 9,
+       // 1x1, 3-4 K steps, code outputs, no skip or a code skip, on handles laid
+       // out for 256-channel tiles: persistent 128 x 64 tiles reading each
+       // 256-row weight tile as two halves
+       TILE_STREAM_H128 = 10 };
 constexpr int KC = 64;
 
 // tile shape of a configuration, and the channels one lane holds per pixel

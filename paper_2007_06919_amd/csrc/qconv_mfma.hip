@@ -798,18 +798,23 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
 // 256 channels x 64 pixels, up to 2 K steps (handles laid out for 256-channel
 // tiles); MI = 4, WC = 2: 128 x 64, up to 4 K steps; MI = 4, WC = 1: 64 x 128,
 // up to 4 K steps (the latter two without skip).
-template <int SKK, int FAST, int MI = 8, int WC = 2>
+// HV = 1 (MI = 4, WC = 2): a handle laid out for 256-channel tiles read as two
+// 128-channel tiles (weights of a 256-row tile: rows 128h .. 128h+127 of
+// each K step), up to 4 K steps, with or without a code skip: a lane of
+// lane group g in wave wc holds channels 32g + 16wc .. 32g + 16wc + 15.
+template <int SKK, int FAST, int MI = 8, int WC = 2, int HV = 0>
 __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
 {
     constexpr int BI = 4, NJ = 2, WPC = 4 / WC, NT = 256;
     constexpr int TM = 16 * MI, TN = 32, BCO = WC * TM, BPX = TN * WPC, PB = KC * BI / 8;
     constexpr int ST_KMAX = BCO == 256 ? 2 : 4;
     constexpr int PPW = BPX / 4;                   // pixels each wave copies (16 or 32)
-    static_assert(SKK == 0 || BCO == 256, "skips on 256-channel tiles only");
+    static_assert(!HV || (MI == 4 && WC == 2), "the half view reads 128-row halves of 256-row tiles");
+    static_assert(SKK == 0 || BCO == 256 || (HV && SKK == 1), "skips on 256-channel tiles or the half view");
     constexpr int CPL = 4 * MI, OW = CPL * BI / 32, QMAX = (1 << BI) - 1;
     constexpr int A_STEP = BCO * KC;               // int8 weight rows of one K step (16 KiB)
     constexpr int B_STEP = BPX * PB;               // packed codes of one K step (2 KiB)
-    constexpr int SK_TILE = BPX * BCO * BI / 8;    // skip codes of one tile (8 KiB)
+    constexpr int SK_TILE = BPX * BCO * BI / 8;    // skip codes of one tile (8 KiB; 4 KiB for the half view)
     constexpr int OFF_B = ST_KMAX * A_STEP;
     constexpr int OFF_S = OFF_B + 2 * ST_KMAX * B_STEP;
     constexpr int OFF_P = OFF_S + (SKK == 1 ? 2 * SK_TILE : 0);
@@ -888,7 +893,25 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
                     dma16(src2, lbase + OFF_B + (b * ST_KMAX + 1) * B_STEP + wave * 512);
             }
         }
-        if constexpr (SKK == 1) {
+        if constexpr (SKK == 1 && HV) {
+            // 64 B per pixel: 4 lanes per pixel, 16 pixels per wave, 16-byte
+            // chunk c of pixel p at position c ^ (p & 3)
+            const int ploc = wave * 16 + (lane >> 2);
+            const long long p = (long long)pq * BPX + ploc;
+            const uint8_t *src = A.zero;
+            if (p < S.P) {
+                long long spix = p;
+                if (A.up2) {
+                    const int n_ = (int)p / hw;
+                    const int rem = (int)p - n_ * hw;
+                    const int oh = rem / S.wo, ow = rem - oh * S.wo;
+                    spix = ((long long)n_ * S.hs + (oh >> 1)) * S.ws + (ow >> 1);
+                }
+                src = (const uint8_t *)S.skip + spix * (A.cout * BI / 8) + co_tile * (BCO * BI / 8) +
+                      16 * ((lane & 3) ^ (ploc & 3));
+            }
+            dma16(src, lbase + OFF_S + b * SK_TILE + wave * 1024);
+        } else if constexpr (SKK == 1) {
 #pragma unroll
             for (int c = 0; c < 2; ++c) {
                 const int ploc = (2 * wave + c) * 8 + (lane >> 3);
@@ -913,7 +936,8 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
     // fragment addresses (the main kernel's swizzles)
     const int a_off = (wc * TM + (lane & 15)) * KC + 16 * ((lane >> 4) ^ swz_a(lane & 15));
     const int b_off = OFF_B + (wp * TN + (lane & 15)) * PB + 8 * ((lane >> 4) ^ (swz_b4(lane & 15) << 1));
-    const int co_loc = wc * TM + CPL * g;           // first of this lane's CPL channels (in the tile)
+    // first of this lane's CPL channels (in the tile)
+    const int co_loc = HV ? 32 * g + 16 * wc : wc * TM + CPL * g;
     const int co_glob = co_tile * BCO + co_loc;
 
     int q = blockIdx.x / A.co_tiles;
@@ -931,8 +955,11 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
 #pragma unroll
                 for (int t = 0; t < BCO / 64; ++t) {
                     const int row = 16 * (4 * t + wave) + (lane >> 2);
-                    dma16(S.wt + ((long long)co_tile * A.ksteps + k) * A_STEP + row * KC +
-                              16 * ((lane & 3) ^ swz_a(row)),
+                    // the half view: half (co_tile & 1) of a 256-row tile (the row
+                    // swizzle depends on the row modulo 8 only)
+                    const long long step = HV ? ((long long)(co_tile >> 1) * A.ksteps + k) * 2 + (co_tile & 1)
+                                              : (long long)co_tile * A.ksteps + k;
+                    dma16(S.wt + step * A_STEP + row * KC + 16 * ((lane & 3) ^ swz_a(row)),
                           lbase + k * A_STEP + (4 * t + wave) * 1024);
                 }
 #pragma unroll
@@ -1038,7 +1065,14 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
 #pragma unroll
             for (int u = 0; u < OW; ++u)
                 outw[j][u] = skw[j][u] = 0;
-            if constexpr (SKK == 1) {
+            if constexpr (SKK == 1 && HV) {
+                // this lane's 16 channels: logical chunk g, half wc
+                const int ploc = wp * TN + j * 16 + (lane & 15);
+                const uint2 t = *(const uint2 *)(lds + OFF_S + buf * SK_TILE + ploc * (BCO * BI / 8) +
+                                                 16 * (g ^ (ploc & 3)) + 8 * wc);
+                skw[j][0] = t.x;
+                skw[j][1] = t.y;
+            } else if constexpr (SKK == 1) {
                 const int ploc = wp * TN + j * 16 + (lane & 15);
                 const uint4 t = *(const uint4 *)(lds + OFF_S + buf * SK_TILE + ploc * (BCO * BI / 8) +
                                                  16 * ((wc * 4 + g) ^ (ploc & 7)));
@@ -1197,6 +1231,7 @@ void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane)
     case TILE_256x64:
     case TILE_STREAM: *blk_co = 256; *blk_px = 64; *chan_per_lane = 32; return;
     case TILE_STREAM_C128: *blk_co = 128; *blk_px = 64; *chan_per_lane = 16; return;
+    case TILE_STREAM_H128: *blk_co = 128; *blk_px = 64; *chan_per_lane = 32; return;
     case TILE_STREAM_C64: *blk_co = 64; *blk_px = 128; *chan_per_lane = 16; return;
     case TILE_128x128_O3: *blk_co = 128; *blk_px = 128; *chan_per_lane = 16; return;
     case TILE_64x256_O3: *blk_co = 64; *blk_px = 256; *chan_per_lane = 16; return;
@@ -1236,24 +1271,37 @@ hipError_t launch_qconv_stream(const MfmaArgs &a, hipStream_t stream)
 {
     // skip_bits 32: the fused projection shortcut, one K step each
     const bool dual = a.skip_bits == 32;
-    const int bco = a.tile_cfg == TILE_STREAM ? 256 : a.tile_cfg == TILE_STREAM_C128 ? 128 : 64;
+    const bool hv = a.tile_cfg == TILE_STREAM_H128;
+    const int bco = a.tile_cfg == TILE_STREAM ? 256 : (a.tile_cfg == TILE_STREAM_C128 || hv) ? 128 : 64;
     const int kmax = bco == 256 ? 2 : 4;
     if (a.ksteps > kmax || a.bits_out != 4 || (a.skip_bits != 0 && a.skip_bits != 4 && !dual) ||
-        (bco != 256 && a.skip_bits != 0) ||
+        (bco != 256 && a.skip_bits != 0 && !(hv && a.skip_bits == 4)) ||
         (dual && (a.ksteps != 1 || a.ksteps2 != 1 || a.cin2 != KC || a.up2)) || a.kh != 1 || a.kw != 1 ||
         a.pad != 0 || a.cout % bco != 0 || a.co_tiles < 1 || a.co_tiles > 256)
         return hipErrorInvalidValue;
     const int qtiles = a.total_tiles / a.co_tiles;
     if (qtiles <= 0)
         return hipSuccess;
-    // workgroups per CU: two on 256-channel tiles (LDS), three on the smaller ones
-    const int slots = bco == 256 ? 512 : 768;
+    // workgroups per CU: two on 256-channel tiles and the half view (LDS), three on the others
+    const int slots = (bco == 256 || hv) ? 512 : 768;
     const int nstream = qtiles < slots / a.co_tiles ? qtiles : slots / a.co_tiles;
     dim3 grid(nstream * a.co_tiles), block(256);
     bool fast = true;
     for (int i = 0; i < a.nseg; ++i)
         fast = fast && a.seg[i].fast;
-    if (bco != 256) {
+    if (hv) {
+        if (a.skip_bits == 0) {
+            if (fast)
+                hipLaunchKernelGGL((qconv_stream_kernel<0, 1, 4, 2, 1>), grid, block, 0, stream, a);
+            else
+                hipLaunchKernelGGL((qconv_stream_kernel<0, 0, 4, 2, 1>), grid, block, 0, stream, a);
+        } else {
+            if (fast)
+                hipLaunchKernelGGL((qconv_stream_kernel<1, 1, 4, 2, 1>), grid, block, 0, stream, a);
+            else
+                hipLaunchKernelGGL((qconv_stream_kernel<1, 0, 4, 2, 1>), grid, block, 0, stream, a);
+        }
+    } else if (bco != 256) {
         if (bco == 128) {
             if (fast)
                 hipLaunchKernelGGL((qconv_stream_kernel<0, 1, 4, 2>), grid, block, 0, stream, a);
@@ -1309,6 +1357,7 @@ hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
         case TILE_256x64S: return launch_qconv_short(a, stream);
         case TILE_256x64: return launch_modes<4, 8, 2, 2, 2>(a, stream);
         case TILE_STREAM:
+        case TILE_STREAM_H128:
         case TILE_STREAM_C128:
         case TILE_STREAM_C64: return launch_qconv_stream(a, stream);
         case TILE_128x128_O3: return launch_occ3<4, 4, 2, 2>(a, stream);

@@ -130,6 +130,13 @@ STREAM_CASES = [
     (2, 41, 52, 256, 64, 1, 1, 4, 4, 1, 4, 0, False),       # 64 x 128 tiles, 4 K steps
     (1, 33, 37, 64, 64, 1, 1, 4, 4, 0, 4, 0, False),        # 1 K step
     (8, 200, 168, 256, 64, 1, 1, 4, 4, 1, 4, 0, False),     # ~2.7 tiles per workgroup
+    # handles laid out for 256-channel tiles with 3-4 K steps: 128 x 64 tiles
+    # reading each 256-row weight tile as two halves, with or without a skip
+    (2, 41, 52, 256, 512, 1, 1, 4, 4, 1, 4, 4, False),      # 4 K steps, code skip
+    (1, 33, 37, 192, 256, 1, 1, 4, 4, 0, 4, 0, False),      # 3 K steps, no skip
+    (2, 16, 18, 256, 256, 1, 1, 4, 4, 0, 4, 4, True),       # upsampled code skip
+    (1, 25, 21, 256, 256, 1, 2, 4, 4, 1, 4, 4, False),      # stride 2
+    (8, 50, 84, 256, 1024, 1, 1, 4, 4, 1, 4, 4, False),     # ResNet-50 res4 conv3 at batch 8
 ]
 
 
@@ -197,6 +204,7 @@ THREE_BIT_CASES = [
     (2, 41, 52, 64, 256, 1, 1, 3, 3, 1, 3, 3, False),       # streaming 1x1 with skip
     (2, 41, 52, 256, 128, 1, 1, 3, 3, 1, 3, 0, False),      # streaming 128 x 64
     (1, 363, 363, 64, 64, 1, 1, 3, 3, 1, 3, 0, False),      # three per CU, 64 x 256
+    (2, 41, 52, 256, 512, 1, 1, 3, 3, 1, 3, 3, False),      # streaming halves of 256-row tiles
     (1, 19, 23, 256, 720, 3, 1, 3, 3, 1, 32, 0, False),     # int32 class predictor
     (1, 16, 18, 64, 256, 3, 1, 3, 3, 0, 3, 32, False),      # int32 skip
     (1, 21, 19, 48, 96, 3, 1, 3, 3, 1, 3, 3, False),        # direct kernel (cin 48)
