@@ -29,8 +29,8 @@ COPY_PROBE_BYTES = 256 << 20
 # HBM traffic of one head-tower launch, from two rocprofv3 counter runs
 # (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain copy of
 # COPY_PROBE_BYTES; valid only for the kernel source it was measured on.
-HEAD_TRAFFIC = {"kernel_sha256": "805689725a23b4fc04d4384da0042495091f541056b1af629682ffc110913ac0",
-                "fetch_bytes": 50967317, "write_bytes": 45670400}
+HEAD_TRAFFIC = {"kernel_sha256": "73fe7bae65181170d6e8b36f82f623e5bf55fbb9a8e17f1ec27d51190f8c6efb",
+                "fetch_bytes": 50980075, "write_bytes": 45670400}
 
 
 def kernel_sha256():
