@@ -105,12 +105,20 @@ typedef struct {
     int skip_bits;     /* 0: no skip; 2/3/4/8: code skip; 32: int32 skip (codes out only) */
     int skip_up2;      /* 1: skip is the coarser map of a nearest 2x upsample */
     int num_levels;    /* number of epilogue tables, 1..64 */
+    /* Step sizes alpha of the uniform quantizers (Sec. 3.1.1, Eq. 1): real
+     * input = step_in * code, real weight = step_w * decoded weight value
+     * (for the odd grid of Eq. 3 that is nu_w / (2^b - 1)), real output =
+     * step_out * code. Metadata for the host-side derivation of the integer
+     * parameters (qconv_scales); stored on the handle, never used on the
+     * device. 0 means "not given"; otherwise finite and > 0. */
+    double step_in, step_w, step_out;
 } qconv_desc_t;
 
 /* One epilogue table; host arrays of length cout, copied at create.
  * mult/shift are ignored (may be NULL) for AQD_OUT_INT32; skip_* are ignored
- * (may be NULL) without a skip. Ranges: shift in [-31, 31]; skip_c >= 0;
- * skip_d in [0, 31]; skip_side in {0, 1}. */
+ * (may be NULL) without a skip. Ranges: shift in [-31, 31]; skip_c any
+ * int32 (negative when the two scales of Eq. 7 have opposite signs, see
+ * aqd_skip_params); skip_d in [0, 31]; skip_side in {0, 1}. */
 typedef struct {
     const int32_t *bias;      /* round(s) of the folded BN, Eq. 6 */
     const int32_t *mult;      /* requantisation multiplier M */
@@ -135,6 +143,13 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
 
 /* Output spatial size for an h x w input: floor((h + 2p - kh)/s) + 1. */
 aqd_status_t qconv_out_shape(qconv_t conv, int h, int w, int *ho, int *wo);
+
+/* Scales of a handle's integer tensors, from its step sizes (Sec. 3.2.1,
+ * Eq. 4: the accumulator acc = sum eta_x * w_value has the scale
+ * alpha_conv = step_in * step_w). *alpha_conv receives step_in * step_w and
+ * *step_out the output step (0 if not given; either pointer may be NULL).
+ * INVALID if the handle was created without step_in or step_w. */
+aqd_status_t qconv_scales(qconv_t conv, double *alpha_conv, double *step_out);
 
 /* Run the convolution with epilogue table `level` on n images of h x w.
  * x:    device, [n][h][w][cin] codes (bits_in).
@@ -318,15 +333,26 @@ aqd_status_t aqd_fold_bn(int cout, const double *gamma, const double *beta, cons
                          const double *var, double eps, double alpha_conv, int32_t *bias,
                          double *alpha_z);
 
-/* Eq. 7-8 per channel: side 0 and (c, d) = F(alpha_k / alpha_z) when
- * alpha_k >= alpha_z, else side 1 and (c, d) = F(alpha_z / alpha_k);
- * scale = min(alpha_z, alpha_k), the scale of the sum.
- * alpha_k has cout entries if alpha_k_per_channel, else one. */
+/* Eq. 7-8 per channel: the operand with the larger scale is rescaled to the
+ * smaller one, and the sum carries the smaller scale:
+ *   |alpha_k| >= |alpha_z|: side 0, (c, d) = F(|alpha_k / alpha_z|), scale = alpha_z;
+ *   otherwise:              side 1, (c, d) = F(|alpha_z / alpha_k|), scale = alpha_k;
+ * with c negated when alpha_z and alpha_k have opposite signs (a folded
+ * normalisation with gamma < 0 has alpha_z < 0; for positive scales this is
+ * the paper's rule, and scale = min(alpha_z, alpha_k)).
+ * alpha_k has cout entries if alpha_k_per_channel, else one. INVALID for a
+ * zero or non-finite scale, or a ratio outside aqd_approx_ratio's domain. */
 aqd_status_t aqd_skip_params(int cout, const double *alpha_z, const double *alpha_k,
                              int alpha_k_per_channel, int32_t *c, int32_t *d, int32_t *side,
                              double *scale);
 
-/* Requantisation to codes of step alpha_out: (mult, shift) of scale/alpha_out. */
+/* Requantisation to codes of step alpha_out (Eq. 2 applied to a sum of scale
+ * `scale`): (mult, shift) = aqd_normalize_multiplier(scale / alpha_out), so
+ * that RSM(u, mult, 31 + shift) is u * scale / alpha_out rounded to nearest
+ * up to the dyadic error |mult / 2^(31+shift) - scale / alpha_out| <=
+ * 2^-(32+shift). The split from aqd_fold_bn (which returns alpha_z, not a
+ * multiplier) lets a skip add (aqd_skip_params) choose the sum's scale
+ * between the fold and the requantisation. */
 aqd_status_t aqd_requant_params(int cout, const double *scale, double alpha_out, int32_t *mult,
                                 int32_t *shift);
 

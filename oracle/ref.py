@@ -342,9 +342,17 @@ def bn_stats_from_sums(s1, s2, count, alpha_conv):
 
 
 def skip_params(alpha_z, alpha_k):
-    """Per channel (Eq. 7): side 0 when the skip scale alpha_k >= alpha_z
-    (skip operand scaled by F(alpha_k, alpha_z)), else side 1 (conv operand
-    scaled by F(alpha_z, alpha_k)); returns c, d, side and the sum's scale."""
+    """Per channel, Eq. 7-8: the operand whose scale is larger in magnitude is
+    rescaled to the other one's scale, and the sum carries the smaller scale.
+
+    side 0 (|alpha_k| >= |alpha_z|): the skip operand is multiplied by
+        c / 2^d ~ alpha_k / alpha_z, the sum's scale is alpha_z;
+    side 1 (|alpha_k| < |alpha_z|): the conv operand is multiplied by
+        c / 2^d ~ alpha_z / alpha_k, the sum's scale is alpha_k.
+    (c, d) = F of the magnitude of the ratio (Eq. 8, ratio >= 1), with c
+    negated when the two scales have opposite signs (a normalisation with
+    gamma < 0 gives a negative alpha_z; the paper's scales are positive, where
+    this is exactly its rule). Returns c, d, side and the sum's scale."""
     alpha_z = np.asarray(alpha_z, np.float64)
     alpha_k = np.broadcast_to(np.asarray(alpha_k, np.float64), alpha_z.shape)
     c = np.zeros(alpha_z.shape, np.int64)
@@ -353,12 +361,16 @@ def skip_params(alpha_z, alpha_k):
     scale = np.zeros(alpha_z.shape, np.float64)
     for i in range(alpha_z.size):
         az, ak = float(alpha_z[i]), float(alpha_k[i])
-        if ak >= az:
-            c[i], d[i] = approx_ratio(ak / az)
+        if az == 0.0 or ak == 0.0:
+            raise ValueError("skip_params: scales must be non-zero")
+        sign = -1 if (az < 0) != (ak < 0) else 1
+        if abs(ak) >= abs(az):
+            ci, d[i] = approx_ratio(abs(ak / az))
             side[i], scale[i] = 0, az
         else:
-            c[i], d[i] = approx_ratio(az / ak)
+            ci, d[i] = approx_ratio(abs(az / ak))
             side[i], scale[i] = 1, ak
+        c[i] = sign * ci
     return c, d, side, scale
 
 

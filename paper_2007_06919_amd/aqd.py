@@ -35,7 +35,8 @@ class AqdError(RuntimeError):
 class QconvDesc(ctypes.Structure):
     _fields_ = [(n, c_int) for n in ("cin", "cout", "kh", "kw", "stride", "pad", "bits_in",
                                      "bits_w", "wenc", "out_mode", "bits_out", "skip_bits",
-                                     "skip_up2", "num_levels")]
+                                     "skip_up2", "num_levels")] + \
+               [(n, c_double) for n in ("step_in", "step_w", "step_out")]
 
 
 class QconvEpilogue(ctypes.Structure):
@@ -74,6 +75,7 @@ def lib():
         sig = {
             "qconv_create": ([POINTER(QconvDesc), vp, POINTER(QconvEpilogue), POINTER(c_void_p)], st),
             "qconv_out_shape": ([vp, i, i, POINTER(c_int), POINTER(c_int)], st),
+            "qconv_scales": ([vp, POINTER(c_double), POINTER(c_double)], st),
             "qconv_run": ([vp, i, i, i, i, vp, vp, i, i, vp, vp], st),
             "qconv_run_group": ([i, POINTER(QconvSeg), vp], st),
             "qconv_group_workspace": ([i, POINTER(QconvSeg), POINTER(ctypes.c_size_t)], st),
@@ -106,7 +108,7 @@ def lib():
 
 
 def exported_symbols():
-    return ["qconv_create", "qconv_out_shape", "qconv_run", "qconv_run_group",
+    return ["qconv_create", "qconv_out_shape", "qconv_scales", "qconv_run", "qconv_run_group",
             "qconv_group_workspace", "qconv_run_group_ws", "qconv_run_proj", "qconv_destroy",
             "qadd_run", "aqd_maxpool_run", "aqd_channel_sums", "aqd_graph_begin", "aqd_graph_end",
             "aqd_graph_launch", "aqd_graph_destroy", "aqd_last_error", "aqd_pack_codes",
@@ -148,11 +150,14 @@ def _host(a, dtype):
 
 # ------------------------------------------------------------------ qconv
 def qconv_create(cin, cout, k, stride, pad, bits_in, bits_w, w_packed, levels, *,
-                 wenc=WENC_TWOS, out_mode=OUT_CODES, bits_out=4, skip_bits=0, skip_up2=0):
+                 wenc=WENC_TWOS, out_mode=OUT_CODES, bits_out=4, skip_bits=0, skip_up2=0,
+                 step_in=0.0, step_w=0.0, step_out=0.0):
     """levels: list of dicts with int32 arrays 'bias' and, as the mode needs,
-    'mult', 'shift', 'skip_c', 'skip_d', 'skip_side'. Returns the handle."""
+    'mult', 'shift', 'skip_c', 'skip_d', 'skip_side'. step_*: the step sizes
+    (0: not given). Returns the handle."""
     d = QconvDesc(cin, cout, k, k, stride, pad, bits_in, bits_w, wenc, out_mode, bits_out,
-                  skip_bits, int(skip_up2), len(levels))
+                  skip_bits, int(skip_up2), len(levels), float(step_in), float(step_w),
+                  float(step_out))
     keep = []
     eps = (QconvEpilogue * len(levels))()
     for i, lv in enumerate(levels):
@@ -171,6 +176,13 @@ def qconv_out_shape(conv, h, w):
     ho, wo = c_int(), c_int()
     _check(lib().qconv_out_shape(conv, h, w, ctypes.byref(ho), ctypes.byref(wo)))
     return ho.value, wo.value
+
+
+def qconv_scales(conv):
+    """(alpha_conv, step_out) of a handle created with its step sizes."""
+    a, o = c_double(), c_double()
+    _check(lib().qconv_scales(conv, ctypes.byref(a), ctypes.byref(o)))
+    return a.value, o.value
 
 
 def qconv_run(conv, level, n, h, w, x, skip, hs, ws, y, stream=None):

@@ -151,6 +151,9 @@ static aqd_status_t validate_desc(const qconv_desc_t *d)
     }
     REQUIRE(d->skip_up2 == 0 || (d->skip_up2 == 1 && d->skip_bits), "skip_up2 needs a skip");
     REQUIRE(d->num_levels >= 1 && d->num_levels <= 64, "num_levels must be in 1..64");
+    const double steps[3] = {d->step_in, d->step_w, d->step_out};
+    for (double st : steps)
+        REQUIRE(std::isfinite(st) && st >= 0.0, "step sizes must be finite and >= 0 (0: not given)");
     return AQD_OK;
 }
 
@@ -182,7 +185,6 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
         if (d.skip_bits) {
             REQUIRE(e.skip_c && e.skip_d && e.skip_side, "skip parameters are null");
             for (int c = 0; c < d.cout; ++c) {
-                REQUIRE(e.skip_c[c] >= 0, "skip_c must be >= 0");
                 REQUIRE(e.skip_d[c] >= 0 && e.skip_d[c] <= 31, "skip_d outside [0, 31]");
                 REQUIRE(e.skip_side[c] == 0 || e.skip_side[c] == 1, "skip_side must be 0 or 1");
             }
@@ -369,6 +371,18 @@ aqd_status_t qconv_out_shape(qconv_t conv, int h, int w, int *ho, int *wo)
     return AQD_OK;
 }
 
+aqd_status_t qconv_scales(qconv_t conv, double *alpha_conv, double *step_out)
+{
+    REQUIRE(conv, "null handle");
+    REQUIRE(conv->d.step_in > 0.0 && conv->d.step_w > 0.0,
+            "the handle was created without step_in / step_w");
+    if (alpha_conv)
+        *alpha_conv = conv->d.step_in * conv->d.step_w;
+    if (step_out)
+        *step_out = conv->d.step_out;
+    return AQD_OK;
+}
+
 }  // extern "C"
 
 namespace {
@@ -459,10 +473,6 @@ aqd_status_t launch_direct(const qconv_seg_t &s, const SegCheck &c, hipStream_t 
 
 }  // namespace
 
-extern "C" {
-
-}  // extern "C"
-
 namespace {
 
 // Checks a group and fills the MFMA launch description (everything but the
@@ -515,9 +525,11 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
             h0.d.cout % 256 == 0) {
             tile_cfg = TILE_STREAM;
             blk_px = 64;
-        } else if (short_codes && h0.d.kh == 1 && h0.d.kw == 1 && h0.d.pad == 0 && h0.d.cout % 256 == 0) {
+        } else if (short_codes && h0.d.kh == 1 && h0.d.kw == 1 && h0.d.pad == 0 && h0.d.cout % 256 == 0 &&
+                   h0.co_tiles <= 128) {
             // 3-4 K steps: the weights of a 256-row tile do not fit twice in
-            // LDS, its 128-row halves do (persistent 128 x 64 tiles)
+            // LDS, its 128-row halves do (persistent 128 x 64 tiles; the
+            // streaming launch takes at most 256 channel tiles)
             tile_cfg = TILE_STREAM_H128;
             blk_px = 64;
         } else if (short_codes) {
@@ -530,7 +542,7 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
     } else if ((h0.tile_cfg == TILE_128x256 || h0.tile_cfg == TILE_64x512) && h0.ksteps <= 4 &&
                h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_in == 4 && h0.d.bits_out == 4 &&
                h0.d.skip_bits == 0 && h0.d.kh == 1 && h0.d.kw == 1 && h0.d.pad == 0 &&
-               h0.d.cout % h0.blk_co == 0) {
+               h0.d.cout % h0.blk_co == 0 && h0.co_tiles <= 256) {
         // 1x1 convolutions with cin <= 256 on 128- or 64-channel handles:
         // persistent streaming tiles (weights resident in LDS)
         tile_cfg = h0.tile_cfg == TILE_128x256 ? TILE_STREAM_C128 : TILE_STREAM_C64;
@@ -1126,19 +1138,24 @@ aqd_status_t aqd_skip_params(int cout, const double *alpha_z, const double *alph
     for (int i = 0; i < cout; ++i) {
         const double az = alpha_z[i];
         const double ak = alpha_k_per_channel ? alpha_k[i] : alpha_k[0];
-        REQUIRE(az > 0.0 && ak > 0.0, "scales must be positive");
+        REQUIRE(std::isfinite(az) && std::isfinite(ak) && az != 0.0 && ak != 0.0,
+                "scales must be finite and non-zero");
+        // opposite signs (a normalisation with gamma < 0): the numerator is negated
+        const bool neg = (az < 0.0) != (ak < 0.0);
         aqd_status_t st;
-        if (ak >= az) {
-            st = aqd_approx_ratio(ak / az, &c[i], &d[i]);
+        if (std::fabs(ak) >= std::fabs(az)) {
+            st = aqd_approx_ratio(std::fabs(ak / az), &c[i], &d[i]);
             side[i] = 0;
             scale[i] = az;
         } else {
-            st = aqd_approx_ratio(az / ak, &c[i], &d[i]);
+            st = aqd_approx_ratio(std::fabs(az / ak), &c[i], &d[i]);
             side[i] = 1;
             scale[i] = ak;
         }
         if (st != AQD_OK)
             return st;
+        if (neg)
+            c[i] = -c[i];
     }
     return AQD_OK;
 }

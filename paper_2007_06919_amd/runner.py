@@ -247,12 +247,15 @@ class Net:
         return sched
 
     def _create(self, conv, levels, out_mode, bits_out, skip_bits, skip_up2):
-        x = conv.segs[0][0]
+        x, _, y = conv.segs[0]
+        p = self.params
         return aqd.qconv_create(conv.cin, conv.cout, conv.k, conv.stride, conv.pad,
                                 self.net.tensors[x].bits, conv.bits_w,
                                 self._packed_weights(conv), levels, wenc=conv.wenc,
                                 out_mode=out_mode, bits_out=bits_out, skip_bits=skip_bits,
-                                skip_up2=skip_up2)
+                                skip_up2=skip_up2, step_in=p.alpha[x],
+                                step_w=p.alpha_w[conv.name],
+                                step_out=p.alpha[y] if out_mode == aqd.OUT_CODES else 0.0)
 
     def _packed_weights(self, conv):
         return aqd.pack_codes(self.params.weights[conv.name], conv.bits_w)
@@ -287,7 +290,7 @@ class Net:
         aqd.channel_sums(acc, len(imgs) * ho * wo, conv.cout, sums, self.stream)
         self.stream.synchronize()
         s = sums.cpu().numpy()
-        alpha_conv = p.alpha[x] * p.alpha_w[conv.name]
+        alpha_conv, _ = aqd.qconv_scales(stats_handle)   # Eq. 4, from the handle's steps
         mean, var = aqd.bn_stats_from_sums(s[:conv.cout], s[conv.cout:], len(imgs) * ho * wo,
                                            alpha_conv)
         sp = p.segs[conv.name][si]

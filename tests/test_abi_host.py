@@ -67,6 +67,7 @@ def _create(desc, levels, w=None):
     dict(wenc=5), dict(out_mode=2), dict(bits_out=16), dict(cin=3, bits_in=4),
     dict(cout=3, bits_out=2), dict(skip_bits=5), dict(skip_bits=4, out_mode=1, bits_out=0),
     dict(skip_up2=1), dict(num_levels=0), dict(num_levels=65),
+    dict(step_in=-1.0), dict(step_w=float("nan")), dict(step_out=float("inf")),
 ])
 def test_create_rejects_bad_descriptors(bad):
     d = _desc(**bad)
@@ -149,7 +150,9 @@ def test_bn_fold_chain_agrees_with_oracle():
         m1, v1 = ref.bn_stats_from_sums(s1, s2, cnt, alpha_conv)
         m2, v2 = aqd.bn_stats_from_sums(s1, s2, cnt, alpha_conv)
         assert np.array_equal(m1, m2) and np.array_equal(v1, v2)
-        g, b = rng.uniform(0.5, 1.5, c), rng.uniform(0, 1, c)
+        # gamma < 0 on some channels: alpha_z < 0 and the signed rule of Eq. 7
+        g = rng.uniform(0.5, 1.5, c) * np.where(rng.random(c) < 0.3, -1.0, 1.0)
+        b = rng.uniform(0, 1, c)
         b1, az1 = ref.fold_bn(g, b, m1, v1, 1e-5, alpha_conv)
         b2, az2 = aqd.fold_bn(g, b, m2, v2, 1e-5, alpha_conv)
         assert np.array_equal(b1, b2) and np.array_equal(az1, az2)

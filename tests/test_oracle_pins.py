@@ -467,3 +467,215 @@ def test_maxpool_brute_force_tiny_and_identity():
                         if 0 <= i * 2 - 1 + dy < 5 and 0 <= j * 2 - 1 + dx < 4]
                 assert got[0, i, j, c] == max(vals)
     assert np.array_equal(ref.maxpool(x, 1, 1, 0), x)
+
+
+# ------------------------------------- Eq. 7 side/scale rule, requant scale
+# These pin the oracle's host derivation of the skip alignment (side, c, d,
+# the sum's scale) and of the requantisation multiplier to what Eq. 7-8 and
+# Eq. 2 mean: the integer result must track the real-valued sum of the two
+# dequantized operands, quantized to the output step. A derivation with the
+# wrong side, the larger scale or an inverted ratio fails these checks (each
+# such mistake is planted below and must be caught).
+
+def _frac(x):
+    return Fraction(float(x))
+
+
+def test_skip_params_hand_worked_channels():
+    az = np.array([0.25, 0.75, 0.5, 0.125, -0.25, -0.75, 0.375])
+    ak = np.array([0.75, 0.25, 0.5, 0.3125, 0.75, 0.25, -0.375])
+    c, d, side, scale = ref.skip_params(az, ak)
+    # 3 = 6/2^1, 1 = 2/2^1, 2.5 = 5/2^1 (dyadic ratios are exact, smallest d)
+    assert c.tolist() == [6, 6, 2, 5, -6, -6, -2]
+    assert d.tolist() == [1, 1, 1, 1, 1, 1, 1]
+    assert side.tolist() == [0, 1, 0, 0, 0, 1, 0]
+    assert scale.tolist() == [0.25, 0.25, 0.5, 0.125, -0.25, 0.25, 0.375]
+
+
+def test_skip_params_rule_with_exact_rationals():
+    rng = _rng(71)
+    m = 600
+    az = np.exp(rng.uniform(np.log(1e-3), np.log(10.0), m)) * rng.choice([-1.0, 1.0], m, p=[0.2, 0.8])
+    ak = np.exp(rng.uniform(np.log(1e-3), np.log(10.0), m))
+    ak[:50] = np.abs(az[:50])                       # equal magnitudes: side 0, ratio 1
+    c, d, side, scale = ref.skip_params(az, ak)
+    for i in range(m):
+        Z, K = _frac(az[i]), _frac(ak[i])
+        big, small = (K, Z) if abs(K) >= abs(Z) else (Z, K)
+        assert side[i] == (0 if abs(K) >= abs(Z) else 1)
+        assert _frac(scale[i]) == small                       # the smaller scale, signed
+        assert abs(_frac(scale[i])) == min(abs(Z), abs(K))
+        R = big / small                                       # exact ratio (signed)
+        assert (c[i] < 0) == (R < 0)
+        assert 1 <= d[i] <= 31 and abs(int(c[i])) < (1 << 31)
+        # as good as the largest exponent Eq. 8 allows for this ratio (the
+        # ratio itself was rounded once to a double: relative 2^-52)
+        dmax = max(e for e in range(1, 32) if abs(R) * (1 << e) + Fraction(1, 2) < (1 << 31))
+        err = abs(Fraction(int(c[i]), 1 << int(d[i])) - R)
+        assert err <= Fraction(1, 1 << (dmax + 1)) + abs(R) * Fraction(1, 1 << 52)
+        if i < 50:
+            assert side[i] == 0 and Fraction(int(c[i]), 1 << int(d[i])) == (1 if az[i] > 0 else -1)
+
+
+def test_requant_params_dyadic_bound():
+    rng = _rng(72)
+    m = 600
+    scale = np.exp(rng.uniform(np.log(1e-6), np.log(50.0), m)) * rng.choice([-1.0, 1.0], m)
+    alpha_out = np.exp(rng.uniform(np.log(1e-2), np.log(2.0), m))
+    for i in range(m):
+        M, sh = ref.requant_params(np.array([scale[i]]), float(alpha_out[i]))
+        M, sh = int(M[0]), int(sh[0])
+        r = _frac(scale[i]) / _frac(alpha_out[i])
+        assert (1 << 30) <= abs(M) < (1 << 31) and -31 <= sh <= 31
+        assert (M < 0) == (r < 0)
+        err = abs(Fraction(M, 1 << (31 + sh)) - r)
+        assert err <= Fraction(1, 1 << (32 + sh)) + abs(r) * Fraction(1, 1 << 52)
+
+
+_skip_params = ref.skip_params   # the oracle's own, for the planted mistakes below
+
+
+def _mut_swapped_side(alpha_z, alpha_k):
+    c, d, side, scale = _skip_params(alpha_z, alpha_k)
+    return c, d, 1 - side, scale
+
+
+def _mut_max_scale(alpha_z, alpha_k):
+    c, d, side, scale = _skip_params(alpha_z, alpha_k)
+    az = np.asarray(alpha_z, np.float64)
+    ak = np.broadcast_to(np.asarray(alpha_k, np.float64), az.shape)
+    return c, d, side, np.where(side == 0, ak, az)
+
+
+def _mut_inverted_ratio(alpha_z, alpha_k):
+    c, d, side, scale = _skip_params(alpha_z, alpha_k)
+    inv = [int(round(2.0 ** 30 * (1 << int(di)) / ci)) for ci, di in zip(c, d)]
+    return np.array(inv, np.int64), np.full(c.shape, 30, np.int64), side, scale
+
+
+def _skip_add_violations(derive, rng, m=4000):
+    """Integer skip add + requantisation (the oracle's qadd) against the real
+    sum of the dequantized operands; returns the number of outputs outside
+    the error bound of Eq. 7-8 and Eq. 2."""
+    qm = 15
+    az = np.exp(rng.uniform(np.log(0.02), np.log(0.2), m))
+    ratio = np.exp(rng.uniform(np.log(1.5), np.log(8.0), m))
+    flip = rng.random(m) < 0.5
+    ak = np.where(flip, az * ratio, az / ratio)                    # both sides
+    az = az * np.where(rng.random(m) < 0.25, -1.0, 1.0)           # gamma < 0 channels
+    alpha_out = 0.2
+    v = rng.integers(-200, 201, m)
+    k = rng.integers(0, 16, m)
+    c, d, side, scale = derive(az, ak)
+    mult, shift = ref.requant_params(scale, alpha_out)
+    # one channel per element
+    out = ref.qadd(v.reshape(1, 1, 1, m), k.reshape(1, 1, 1, m), False, c, d, side, mult, shift,
+                   4).reshape(m)
+    real = (az * v + ak * k) / alpha_out
+    small = np.minimum(np.abs(az), np.abs(ak))
+    # alignment rounding (1/2 of the smaller scale) + dyadic approximations
+    # (below 1e-6 here) + the final rounding
+    bound = 0.5 * small / alpha_out + 1e-6 + 0.5
+    return int(np.sum(np.abs(out - np.clip(real, 0, qm)) > bound))
+
+
+def test_skip_add_requant_tracks_the_real_sum():
+    assert _skip_add_violations(ref.skip_params, _rng(73)) == 0
+
+
+@pytest.mark.parametrize("mutant", [_mut_swapped_side, _mut_max_scale, _mut_inverted_ratio])
+def test_skip_add_real_sum_check_catches_planted_mistakes(mutant):
+    assert _skip_add_violations(mutant, _rng(73)) > 400
+
+
+def _tiny_residual_net():
+    """Identity code skip, int32 projection skip and an upsampled code skip,
+    every conv calibrated (odd weight grid, 4-bit codes)."""
+    from paper_2007_06919_amd import workloads as wl
+    net = wl.NetSpec(wenc=wl.WENC_PAPER_ODD)
+    net.add_tensor("x", 1, 8, 9, 64, 4)
+    net.add_tensor("u", 1, 4, 5, 64, 4)
+    net.inputs += ["x", "u"]
+    net.conv("c1", "x", "a", 64, 3, 1, 4, 4)
+    net.conv("c2", "a", "b", 64, 3, 1, 4, 4, skip="x")
+    net.conv("dn", "x", "ds", 64, 1, 1, 4, 32)
+    net.conv("c3", "b", "o", 64, 1, 1, 4, 4, skip="ds")
+    net.conv("lat", "o", "p", 64, 1, 1, 4, 4, skip="u", skip_up2=True)
+    net.outputs.append("p")
+    params = wl.make_params(net, 74, "calibrated")
+    rng = _rng(75)
+    for segs in params.segs.values():       # a quarter of the channels with gamma < 0
+        for sp in segs:
+            sp["gamma"] = sp["gamma"] * np.where(rng.random(sp["gamma"].size) < 0.25, -1.0, 1.0)
+    return net, params
+
+
+def _float_layer_violations(net, params, vals):
+    """Each layer in float64 from the oracle's integer inputs to it:
+    dequantize (Eq. 1), convolve, batch-normalise with the calibration
+    image's statistics, add the dequantized skip, quantize to the output
+    step (Eq. 2). Returns the number of outputs outside the error bound of
+    the integer path (folded-bias rounding, Eq. 6; alignment rounding, Eq. 7;
+    final rounding)."""
+    bad = 0
+    real, az_of = {}, {}
+    for conv in net.convs:
+        x, skip, y = conv.segs[0]
+        ax = params.alpha[x]
+        aw = 1.0 / 15.0
+        wv = 2.0 * params.weights[conv.name].astype(np.float64) - 15.0       # Eq. 3 grid
+        xr = torch.from_numpy(ax * vals[x].astype(np.float64)).permute(0, 3, 1, 2)
+        wr = torch.from_numpy(aw * wv).permute(0, 3, 1, 2)
+        z = torch.nn.functional.conv2d(xr, wr, padding=conv.pad, stride=conv.stride)
+        z = z.permute(0, 2, 3, 1).numpy()
+        zz = z.reshape(-1, conv.cout)
+        mu = zz.mean(axis=0)
+        var = (zz * zz).mean(axis=0) - mu * mu
+        sp = params.segs[conv.name][0]
+        sd = np.sqrt(var + params.bn_eps)
+        bn = sp["gamma"] * (z - mu) / sd + sp["beta"]
+        az = (ax * aw) * sp["gamma"] / sd
+        if net.tensors[y].bits == 32:
+            # v = acc + round(s) carries the scale alpha_z (Eq. 6): within alpha_z / 2
+            assert np.all(np.abs(az * vals[y] - bn) <= np.abs(az) / 2 + 1e-9)
+            real[y], az_of[y] = bn, az
+            continue
+        ay = params.alpha[y]
+        extra = np.abs(az)                                   # this conv's bias rounding
+        pre = bn
+        if skip is not None:
+            if net.tensors[skip].bits == 32:
+                sk, ak = real[skip], az_of[skip]
+                extra = extra + np.abs(ak)                   # the skip's own bias rounding
+            else:
+                ks = vals[skip]
+                if conv.skip_up2:
+                    ks = ks[:, np.arange(z.shape[1]) >> 1][:, :, np.arange(z.shape[2]) >> 1]
+                ak = params.alpha[skip]
+                sk = ak * ks
+            pre = bn + sk
+            extra = extra + np.minimum(np.abs(az), np.abs(ak))   # alignment rounding
+        target = np.clip(pre / ay, 0, 15)
+        bound = 0.5 + extra / (2 * ay) + 1e-6
+        bad += int(np.sum(np.abs(vals[y] - target) > bound))
+    return bad
+
+
+def test_calibrated_residual_network_tracks_float64():
+    from oracle import network
+    net, params = _tiny_residual_net()
+    vals, tables = network.run(net, params)
+    assert any(int(c) < 0 for t in tables.values() for s in t for c in s.get("skip_c", []))
+    assert any(int(m) < 0 for t in tables.values() for s in t for m in s.get("mult", []))
+    interior = [np.mean((vals[t] > 0) & (vals[t] < 15)) for t in ("a", "b", "o", "p")]
+    assert min(interior) > 0.2, interior
+    assert _float_layer_violations(net, params, vals) == 0
+
+
+@pytest.mark.parametrize("mutant", [_mut_swapped_side, _mut_max_scale, _mut_inverted_ratio])
+def test_float64_network_check_catches_planted_mistakes(mutant, monkeypatch):
+    from oracle import network
+    net, params = _tiny_residual_net()
+    monkeypatch.setattr(ref, "skip_params", mutant)
+    vals, _ = network.run(net, params)
+    assert _float_layer_violations(net, params, vals) > 100
