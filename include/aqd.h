@@ -206,6 +206,21 @@ aqd_status_t qconv_group_workspace(int count, const qconv_seg_t *segs, size_t *b
 aqd_status_t qconv_run_group_ws(int count, const qconv_seg_t *segs, void *workspace,
                                 size_t ws_bytes, aqd_stream_t stream);
 
+/* qconv_run_group_ws without a caller workspace, for callers that cannot
+ * allocate device memory (code recorded under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc). The split K reduction
+ * uses a scratch array of AQD_STATIC_SCRATCH_BYTES (64 MiB) that the library
+ * holds on each GPU it runs on, until the process ends; the call allocates
+ * nothing. Outputs are identical to qconv_run_group_ws's with a workspace of
+ * the queried size. A group whose split would need more scratch than that
+ * returns AQD_ERR_UNSUPPORTED (the message names the size) with no launch;
+ * run it with qconv_run_group_ws instead. Every call on one GPU shares that
+ * GPU's scratch and leaves its contents behind: calls that overlap in time on
+ * one GPU (on two streams, or from two threads) race; serialise them on one
+ * stream. Other errors as qconv_run_group. */
+#define AQD_STATIC_SCRATCH_BYTES (64u << 20)
+aqd_status_t qconv_run_group_static(int count, const qconv_seg_t *segs, aqd_stream_t stream);
+
 /* Tail of a residual block with a projection shortcut, in one launch
  * (Sec. 3.2.3, Eq. 7-8: the skip operand is the shortcut convolution's int32
  * output v_p = acc_p + bias_p, one of the paper's 32-bit integer operands;

@@ -80,6 +80,7 @@ def lib():
             "qconv_run_group": ([i, POINTER(QconvSeg), vp], st),
             "qconv_group_workspace": ([i, POINTER(QconvSeg), POINTER(ctypes.c_size_t)], st),
             "qconv_run_group_ws": ([i, POINTER(QconvSeg), vp, ctypes.c_size_t, vp], st),
+            "qconv_run_group_static": ([i, POINTER(QconvSeg), vp], st),
             "qconv_run_proj": ([vp, vp, i, i, i, i, vp, i, i, vp, vp, vp], st),
             "qconv_destroy": ([vp], None),
             "qadd_run": ([POINTER(QaddDesc), vp, vp, vp, POINTER(QaddParams), vp], st),
@@ -109,7 +110,8 @@ def lib():
 
 def exported_symbols():
     return ["qconv_create", "qconv_out_shape", "qconv_scales", "qconv_run", "qconv_run_group",
-            "qconv_group_workspace", "qconv_run_group_ws", "qconv_run_proj", "qconv_destroy",
+            "qconv_group_workspace", "qconv_run_group_ws", "qconv_run_group_static",
+            "qconv_run_proj", "qconv_destroy",
             "qadd_run", "aqd_maxpool_run", "aqd_channel_sums", "aqd_graph_begin", "aqd_graph_end",
             "aqd_graph_launch", "aqd_graph_destroy", "aqd_last_error", "aqd_pack_codes",
             "aqd_unpack_codes", "aqd_approx_ratio", "aqd_normalize_multiplier",
@@ -213,6 +215,11 @@ def qconv_group_workspace(segs) -> int:
 def qconv_run_group_ws(segs, workspace, ws_bytes, stream=None):
     _check(lib().qconv_run_group_ws(len(segs), _seg_array(segs), _addr(workspace), ws_bytes,
                                     _stream(stream)))
+
+
+def qconv_run_group_static(segs, stream=None):
+    """qconv_run_group_ws on the library's static scratch (allocates nothing)."""
+    _check(lib().qconv_run_group_static(len(segs), _seg_array(segs), _stream(stream)))
 
 
 def qconv_run_proj(conv, proj, level, n, h, w, x, hp, wp, xp, y, stream=None):

@@ -681,10 +681,44 @@ aqd_status_t qconv_group_workspace(int count, const qconv_seg_t *segs, size_t *b
     return AQD_OK;
 }
 
-aqd_status_t qconv_run_group_ws(int count, const qconv_seg_t *segs, void *workspace, size_t ws_bytes,
-                                aqd_stream_t stream_)
+}  // extern "C"
+
+// Scratch of qconv_run_group_static: the split-K partial sums of callers that
+// cannot allocate. Every GPU the library runs on holds its own copy until the
+// process ends; host code reaches it only through the per-device address from
+// hipGetSymbolAddress (the array's name is a host-side stand-in).
+static __device__ __align__(256) uint8_t scratch[AQD_STATIC_SCRATCH_BYTES];
+
+namespace {
+
+std::mutex g_scratch_mu;
+void *g_scratch[64] = {};
+
+// Device address of the current device's scratch, looked up once per device
+// (with that device current); nullptr if the lookup fails.
+void *static_scratch()
 {
-    hipStream_t stream = (hipStream_t)stream_;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        g_scratch[dev] = p;
+    }
+    return g_scratch[dev];
+}
+
+// A group launch; the split-K partial sums go to `workspace` (the caller's,
+// ws_bytes long, or null: no split), or with use_static to this device's
+// scratch array (no allocation).
+aqd_status_t run_group(int count, const qconv_seg_t *segs, void *workspace, size_t ws_bytes,
+                       bool use_static, hipStream_t stream)
+{
     SegCheck chk[AQD_MAX_SEGS];
     MfmaArgs a;
     bool direct = false;
@@ -704,7 +738,21 @@ aqd_status_t qconv_run_group_ws(int count, const qconv_seg_t *segs, void *worksp
         return AQD_OK;
     const qconv_s &h0 = *segs[0].conv;
     int nparts = 1, kchunk = a.ksteps;
-    if (workspace) {
+    if (use_static) {
+        plan_split(a, &nparts, &kchunk);
+        if (nparts > 1) {
+            const size_t need = split_bytes(a, nparts);
+            if (need > AQD_STATIC_SCRATCH_BYTES)
+                return fail(AQD_ERR_UNSUPPORTED,
+                            "this group's split K reduction needs " + std::to_string(need) +
+                                " bytes of scratch, more than the " +
+                                std::to_string((size_t)AQD_STATIC_SCRATCH_BYTES) +
+                                " of the static scratch; use qconv_run_group_ws with a workspace");
+            workspace = static_scratch();
+            if (!workspace)
+                return fail(AQD_ERR_DEVICE, "the address of the static scratch could not be found");
+        }
+    } else if (workspace) {
         REQUIRE(((uintptr_t)workspace & 255) == 0, "workspace must be 256-byte aligned");
         plan_split(a, &nparts, &kchunk);
         if (nparts > 1 && ws_bytes < split_bytes(a, nparts))
@@ -762,9 +810,24 @@ aqd_status_t qconv_run_group_ws(int count, const qconv_seg_t *segs, void *worksp
     return AQD_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+aqd_status_t qconv_run_group_ws(int count, const qconv_seg_t *segs, void *workspace, size_t ws_bytes,
+                                aqd_stream_t stream)
+{
+    return run_group(count, segs, workspace, ws_bytes, false, (hipStream_t)stream);
+}
+
+aqd_status_t qconv_run_group_static(int count, const qconv_seg_t *segs, aqd_stream_t stream)
+{
+    return run_group(count, segs, nullptr, 0, true, (hipStream_t)stream);
+}
+
 aqd_status_t qconv_run_group(int count, const qconv_seg_t *segs, aqd_stream_t stream)
 {
-    return qconv_run_group_ws(count, segs, nullptr, 0, stream);
+    return run_group(count, segs, nullptr, 0, false, (hipStream_t)stream);
 }
 
 aqd_status_t qconv_run_proj(qconv_t conv, qconv_t proj, int level, int n, int h, int w,
