@@ -317,7 +317,10 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
     qconv_s *hp = new (std::nothrow) qconv_s(h);
     if (!hp)
         return fail(AQD_ERR_NOMEM, "host allocation failed");
-    if (hipMalloc(&hp->w_dev, wbuf.size()) != hipSuccess) {
+    // MFMA weights: four K steps of 256-row tiles (64 KiB) of padding past the
+    // end, which the register-fed kernel's look-ahead may read (never use)
+    const size_t w_pad = mfma ? 4 * 256 * KC : 0;
+    if (hipMalloc(&hp->w_dev, wbuf.size() + w_pad) != hipSuccess) {
         delete hp;
         return fail(AQD_ERR_NOMEM, "hipMalloc of the weights failed");
     }
@@ -538,6 +541,12 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         } else if (t128 >= 64 && t128 < 200 && h0.ksteps <= 80) {
             tile_cfg = TILE_256x64;
             blk_px = 64;
+        } else if (h0.d.bits_in == 4 && h0.d.cin % 256 == 0 && h0.d.out_mode == AQD_OUT_CODES &&
+                   (h0.d.skip_bits == 0 || h0.d.skip_bits == 4) && t128 >= 200) {
+            // 256-channel input chunks: weights read into registers (no LDS
+            // traffic for them), activation codes staged in LDS four K steps
+            // at a time
+            tile_cfg = TILE_WV;
         }
     } else if ((h0.tile_cfg == TILE_128x256 || h0.tile_cfg == TILE_64x512) && h0.ksteps <= 4 &&
                h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_in == 4 && h0.d.bits_out == 4 &&
@@ -616,7 +625,7 @@ void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
 {
     if (a.tile_cfg == TILE_256x64S || a.tile_cfg == TILE_256x64 || a.tile_cfg == TILE_STREAM ||
         a.tile_cfg == TILE_STREAM_C128 || a.tile_cfg == TILE_STREAM_C64 || a.tile_cfg == TILE_128x128_O3 ||
-        a.tile_cfg == TILE_64x256_O3 || a.tile_cfg == TILE_STREAM_H128) {  // never split
+        a.tile_cfg == TILE_64x256_O3 || a.tile_cfg == TILE_STREAM_H128 || a.tile_cfg == TILE_WV) {  // never split
         *nparts = 1;
         *kchunk = a.ksteps;
         return;

@@ -24,7 +24,10 @@ enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
        // 1x1, 3-4 K steps, code outputs, no skip or a code skip, on handles laid
        // out for 256-channel tiles: persistent 128 x 64 tiles reading each
        // 256-row weight tile as two halves
-       TILE_STREAM_H128 = 10 };
+       TILE_STREAM_H128 = 10,
+       // cin a multiple of 256, code outputs: 256 x 128 tiles with the weights
+       // read into registers (qconv_wv.hip), same weight layout as 256x128
+       TILE_WV = 11 };
 constexpr int KC = 64;
 
 // tile shape of a configuration, and the channels one lane holds per pixel
@@ -82,6 +85,8 @@ hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
 // fused projection shortcut (4-bit, 256 x 64 tiles): tile counts use blk_px = 64
 constexpr int PROJ_BLK_PX = 64;
 hipError_t launch_qconv_proj(const MfmaArgs &a, hipStream_t stream);
+// TILE_WV launches (qconv_wv.hip)
+hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream);
 
 // ---- split-K combine + epilogue (qconv_splitk.hip) ---------------------------
 struct SplitSeg {

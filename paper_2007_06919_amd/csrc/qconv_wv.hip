@@ -1,0 +1,407 @@
+// Implicit-GEMM integer convolution on the gfx950 int8 MFMA
+// (v_mfma_i32_16x16x64_i8) for layers with 256-channel input chunks (cin a
+// multiple of 256), 4-bit activation codes and code outputs: the detection
+// heads' 3x3 256 -> 256 towers, the FPN's 3x3 outputs, ResNet-50's res4/res5
+// 3x3 and 1x1 layers with cin >= 512. The GEMM view is that of Eq. 4
+// (Sec. 3.2.1): rows = output channels (weights), columns = output pixels,
+// K = taps x input channels, one K step = 64 input channels of one tap.
+//
+// Workgroup tile 256 channels x 128 pixels, 4 waves; wave w owns channel rows
+// 64w .. 64w+63 (4 accumulator tiles of 16) for all 128 pixels (8 column
+// tiles of 16), so no two waves share a weight row:
+//  * weights (int8, decoded and tiled at create exactly as for the 256 x 128
+//    kernel) go from global memory (L2) straight into registers, three K
+//    steps ahead of their MFMAs: no LDS traffic for the larger operand;
+//  * activation codes (4-bit, packed as stored) go through LDS in stages of
+//    four K steps (one tap's 256 channels, 128 B per pixel: whole cache
+//    lines), a ring of four stages; each lane copies 16 B per K step
+//    through registers, and the copy is written two K steps after its load.
+//    In LDS a pixel row's eight-byte columns are XOR-swizzled with the pixel
+//    index, so that the fragment reads (8 B per lane, 16 pixels per lane
+//    group) and the copies' writes are free of bank conflicts;
+//  * one barrier per stage (four K steps);
+//  * the channel tile's epilogue table is fetched before the last stage.
+// The packed codes are widened to int8 in registers (mask/shift), in the
+// byte order the weights were stored in at create.
+//
+// Epilogue (Sec. 3.2.2-3.2.3, Eq. 6-8, and Eq. 2 on integers): the
+// accumulators start at the folded bias; a lane holds 16 consecutive channels
+// of 8 pixels and packs their requantised codes into 8-byte stores. The LDS
+// ring holds the channel tile's epilogue table and the side-0 skip table
+// after the last K step.
+
+#include "epilogue.h"
+#include "internal.h"
+#include "mfma_common.h"
+
+namespace aqd {
+namespace {
+
+constexpr int WV_BCO = 256;              // channels per workgroup tile
+constexpr int WV_BPX = 128;              // pixels per workgroup tile
+constexpr int WV_ROW = 128;              // bytes of one stage per pixel (256 codes of 4 bits)
+constexpr int WV_STAGE = WV_BPX * WV_ROW;  // 16 KiB
+constexpr int WV_NBUF = 4;
+constexpr int WV_LDS = WV_NBUF * WV_STAGE;
+
+// SKK: 0 = no skip, 1 = code skip (4-bit); FAST: every shift >= 2 (32-bit requantisation)
+template <int SKK, int FAST>
+__global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
+{
+    constexpr int BI = 4, MI = 4, NJ = 8, QMAX = 15, OW = 2;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[WV_LDS];
+
+    const int bid = blockIdx.x;
+    const int tile = (bid & 7) * A.tiles_per_xcd + (bid >> 3);
+    if (tile >= A.total_tiles)
+        return;
+    int s = 0;
+#pragma unroll
+    for (int i = 1; i < AQD_MAX_SEGS; ++i)
+        if (i < A.nseg && tile >= A.seg[i].tile_begin)
+            s = i;
+    const MfmaSeg &S = A.seg[s];
+    const int t_in_seg = tile - S.tile_begin;
+    const int co_tile = t_in_seg % A.co_tiles;
+    const int px_tile = t_in_seg / A.co_tiles;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r = lane & 15, g = lane >> 4;
+
+    const int row_bytes = A.cin * BI / 8;
+    const int spt = A.cin / 256;                 // stages per tap
+    const int KS = A.ksteps;
+    const int NST = KS / 4;                      // stages (KS is a multiple of 4)
+    const int hw = S.ho * S.wo;
+
+    // ---- activation copies: piece m of a stage = pixels 32m .. 32m+31 of the
+    // tile, lane tid copying 16-byte chunk tid % 8 of pixel 32m + tid / 8
+    const int c16 = tid & 7;
+    // per piece: first input row/column of the output pixel's window (a row
+    // far outside the image for pixels past the end) and the image's first
+    // pixel (n * h * w < 2^31, checked on the host)
+    // (pixel indices fit in 32 bits: n * ho * wo < 2^31, checked on the host)
+    int ih0[4], iw0[4], xpix[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        const unsigned p = (unsigned)(px_tile * WV_BPX + 32 * m + (tid >> 3));
+        const bool ok = p < (unsigned)S.P;
+        const unsigned pn = ok ? p / (unsigned)hw : 0u;
+        const unsigned prem = ok ? p - pn * (unsigned)hw : 0u;
+        const unsigned oh = prem / (unsigned)S.wo, ow = prem - oh * (unsigned)S.wo;
+        ih0[m] = ok ? (int)oh * A.stride - A.pad : -(1 << 30);
+        iw0[m] = (int)ow * A.stride - A.pad;
+        xpix[m] = (int)pn * S.h * S.w;
+    }
+    const uint8_t *xsrc = S.x + 16 * c16;
+    // LDS byte offsets: eight-byte column c of pixel p at 128 p + 8 (c ^ (p & 15))
+    const int wp = tid >> 3;                      // pixel within a piece (p & 15 == wp & 15)
+    const uint32_t wo0 = WV_ROW * wp + 8 * ((2 * c16) ^ (wp & 15));
+    const uint32_t wo1 = WV_ROW * wp + 8 * ((2 * c16 + 1) ^ (wp & 15));
+    // fragment of K step q: pixel 16j + r, eight-byte column 4q + g
+    auto ro = [&](int q) -> uint32_t { return WV_ROW * r + 8 * ((4 * q + g) ^ r); };
+
+    // copy state of the stage being loaded: tap (tr, tq), 128-byte chunk th
+    int tr = 0, tq = 0, th = 0;
+    auto advance = [&]() {
+        if (++th == spt) {
+            th = 0;
+            if (++tq == A.kw) {
+                tq = 0;
+                ++tr;
+            }
+        }
+    };
+    // a piece of the stage being loaded, without a branch: taps in the
+    // padding (and pixels past the end, and stages past the last) read a
+    // clamped position inside the image and are masked to code 0
+    auto load_piece = [&](int m) -> uint4 {
+        const int ih = ih0[m] + tr, iw = iw0[m] + tq;
+        const bool in = ((unsigned)ih < (unsigned)S.h) & ((unsigned)iw < (unsigned)S.w);
+        const int ihc = min(max(ih, 0), S.h - 1), iwc = min(max(iw, 0), S.w - 1);
+        const uint4 v = *(const uint4 *)(xsrc + (long long)(xpix[m] + ihc * S.w + iwc) * row_bytes +
+                                         WV_ROW * th);
+        const uint32_t keep = in ? 0xFFFFFFFFu : 0u;
+        return make_uint4(v.x & keep, v.y & keep, v.z & keep, v.w & keep);
+    };
+    auto write_piece = [&](int buf, int m, const uint4 v) {
+        uint8_t *base = lds + buf * WV_STAGE + m * (32 * WV_ROW);
+        *(uint2 *)(base + wo0) = make_uint2(v.x, v.y);
+        *(uint2 *)(base + wo1) = make_uint2(v.z, v.w);
+    };
+
+    // ---- weights: this wave's rows of K step k, accumulator tile i at
+    // wa + k * 16 KiB + i * 1 KiB (lane: row r, 16-byte column g; in global
+    // memory the columns are in order, only LDS copies swizzle them); the
+    // look-ahead reads up to three steps past the last (the allocation has
+    // four steps of padding) and those values are never used
+    const int8_t *wa = S.wt + ((long long)co_tile * KS * WV_BCO + 64 * wave + r) * KC + 16 * g;
+    auto load_a = [&](int k, v4i *dst) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+            dst[i] = *(const v4i *)(wa + (long long)k * (WV_BCO * KC) + i * 1024);
+    };
+
+    // ---- accumulators start at the bias (Eq. 6): lane group g of wave w holds
+    // channels 128 (w >> 1) + 32 g + 16 (w & 1) + 4 i + e of the tile
+    const int co_loc = 128 * (wave >> 1) + 32 * g + 16 * (wave & 1);
+    const int co_glob = co_tile * WV_BCO + co_loc;
+    v4i acc[MI][NJ];
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+        const v4i b = *(const v4i *)(S.epi + EPI_BIAS * A.cout_pad + co_glob + 4 * i);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+            acc[i][j] = b;
+    }
+
+    // ---- prologue: stage 0 and pieces 0-1 of stage 1 in LDS (pieces 2 and 3
+    // are written in the first two K steps, as every stage's last two are),
+    // weights of steps 0-2 in registers
+    uint4 rb[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+        write_piece(0, m, load_piece(m));
+    advance();
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+        write_piece(1, m, load_piece(m));
+    rb[2] = load_piece(2);
+    rb[3] = load_piece(3);
+    rb[0] = rb[1] = rb[2];
+    advance();  // copy state: stage 2
+    v4i fa[4][MI];
+    load_a(0, fa[0]);
+    load_a(1, fa[1]);
+    load_a(2, fa[2]);
+    uint2 fb[NJ];   // fragment j of the current step, or of the next one once read ahead
+
+    auto widen = [](const uint2 w) -> v4i {
+        return v4i{(int)(w.x & 0x0F0F0F0Fu), (int)((w.x >> 4) & 0x0F0F0F0Fu),
+                   (int)(w.y & 0x0F0F0F0Fu), (int)((w.y >> 4) & 0x0F0F0F0Fu)};
+    };
+    constexpr int RA = 3;  // fragments are read RA column tiles ahead of their MFMAs
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+#pragma unroll
+    for (int j = 0; j < RA; ++j)
+        fb[j] = *(const uint2 *)(lds + 2048 * j + ro(0));
+
+    // ---- main loop, one stage (four K steps) per call: stage g lives in
+    // buffer g % 4; during stage g the pieces of stage g + 2 are loaded (one
+    // per K step) and written two K steps later, into the buffer of stage
+    // g - 2. Fragment (k, j) is read during the MFMAs of column tile j - RA of
+    // step k (or of step k - 1). A barrier in the last step, before the first
+    // read of the next stage, makes that stage visible; the barrier of stage
+    // g - 1 orders every wave's reads of stage g - 2 before the writes of
+    // stage g + 2 into its buffer. Loads and writes for stages past the last
+    // go to buffers nobody reads again; the weight look-ahead past the last
+    // step reads the allocation's padding.
+    auto stage = [&](const int gs) {
+        const int buf = gs & 3;
+        static_for<4>([&](auto qc) {
+            constexpr int q = decltype(qc)::value;
+            const int k = 4 * gs + q;
+            // (a) a piece of stage gs + 2
+            rb[q] = load_piece(q);
+            // (b) weights of step k + 3 (set (q + 3) % 4; step k uses set q)
+            load_a(k + 3, fa[(q + 3) & 3]);
+            // (c) write the piece loaded two steps earlier (at q < 2: pieces 2
+            // and 3 of stage gs + 1, loaded in stage gs - 1 or by the prologue)
+            if constexpr (q >= 2)
+                write_piece((buf + 2) & 3, q - 2, rb[q - 2]);
+            else
+                write_piece((buf + 1) & 3, q + 2, rb[q + 2]);
+            const uint32_t r_this = ro(q) + buf * WV_STAGE;
+            const uint32_t r_next = q < 3 ? ro(q + 1) + buf * WV_STAGE : ro(0) + ((buf + 1) & 3) * WV_STAGE;
+            // (d, e) the MFMAs of step k, reading ahead
+            static_for<NJ>([&](auto jc) {
+                constexpr int j = decltype(jc)::value;
+                if constexpr (q == 3 && j == NJ - RA)
+                    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+                const v4i bj = widen(fb[j]);
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[q][i], bj, acc[i][j], 0, 0, 0);
+                if constexpr (j + RA < NJ)
+                    fb[j + RA] = *(const uint2 *)(lds + 2048 * (j + RA) + r_this);
+                else
+                    fb[j + RA - NJ] = *(const uint2 *)(lds + 2048 * (j + RA - NJ) + r_next);
+            });
+            if constexpr (q == 3)
+                advance();
+        });
+    };
+    for (int gs = 0; gs < NST - 1; ++gs)
+        stage(gs);
+    // the channel tile's epilogue table does not depend on the accumulators:
+    // its loads are issued before the last stage, whose MFMAs hide their latency
+    constexpr int PRM_PER = EPI_FIELDS * WV_BCO / 256;
+    int prm_r[PRM_PER];
+#pragma unroll
+    for (int t = 0; t < PRM_PER; ++t) {
+        const int i = tid + 256 * t;
+        const int which = i / WV_BCO, c = i - which * WV_BCO;
+        prm_r[t] = S.epi[which * A.cout_pad + co_tile * WV_BCO + c];
+    }
+    stage(NST - 1);
+
+    // ---------------------------------------------------------------- epilogue
+    const long long px0 = (long long)px_tile * WV_BPX + r;
+    const bool co_ok = co_glob < A.cout;          // a lane's 16 channels are all valid or all padding
+    bool okj[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+        okj[j] = co_ok && px0 + 16 * j < S.P;
+    // skip codes: issued before the tables go to LDS, so that the two overlap
+    uint32_t skw[NJ][OW];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        skw[j][0] = skw[j][1] = 0;
+        if constexpr (SKK == 1) {
+            if (okj[j]) {
+                const long long px = px0 + 16 * j;
+                long long spix = px;
+                if (A.up2) {
+                    const int n_ = (int)(px / hw);
+                    const int rem = (int)(px - (long long)n_ * hw);
+                    const int oh = rem / S.wo, ow = rem - oh * S.wo;
+                    spix = ((long long)n_ * S.hs + (oh >> 1)) * S.ws + (ow >> 1);
+                }
+                const uint2 t = *(const uint2 *)((const uint8_t *)S.skip + spix * (A.cout * BI / 8) + co_glob * BI / 8);
+                skw[j][0] = t.x;
+                skw[j][1] = t.y;
+            }
+        }
+    }
+    int32_t *prm = (int32_t *)lds;                 // [EPI_FIELDS][256]
+    int32_t *lut = prm + EPI_FIELDS * WV_BCO;      // [256][16]: RSM(k, c, d) of the side-0 skip codes
+    const bool use_lut = SKK == 1 && S.side0;
+    constexpr int LUT_PER = SKK == 1 ? WV_BCO * (QMAX + 1) / 256 : 1;
+    int lut_r[LUT_PER];
+    if (use_lut) {
+#pragma unroll
+        for (int t = 0; t < LUT_PER; ++t)
+            lut_r[t] = S.lut[co_tile * WV_BCO * (QMAX + 1) + tid + 256 * t];
+    }
+    __syncthreads();  // every wave is done with the ring
+#pragma unroll
+    for (int t = 0; t < PRM_PER; ++t)
+        prm[tid + 256 * t] = prm_r[t];
+    if (use_lut) {
+#pragma unroll
+        for (int t = 0; t < LUT_PER; ++t)
+            lut[tid + 256 * t] = lut_r[t];
+    }
+    __syncthreads();
+    static_assert((EPI_FIELDS + 16) * WV_BCO * 4 <= WV_LDS, "tables fit in the ring");
+
+    const int32_t *lut_l = lut + (co_loc << BI);  // this lane's 16 channels
+    uint32_t outw[NJ][OW];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+        outw[j][0] = outw[j][1] = 0;
+    // per channel group i: the requantisation parameters, read once for all
+    // columns
+    auto group = [&](auto lut_c, auto ic, int j0, int j1) {
+        constexpr bool LUT = decltype(lut_c)::value;
+        constexpr int i = decltype(ic)::value;
+        const int cl = co_loc + 4 * i;
+        const int4 m4 = *(const int4 *)(prm + EPI_MULT * WV_BCO + cl);
+        const int4 s4 = *(const int4 *)(prm + (FAST ? EPI_SHR : EPI_SHIFT) * WV_BCO + cl);
+        const int mult[4] = {m4.x, m4.y, m4.z, m4.w};
+        const int shf[4] = {s4.x, s4.y, s4.z, s4.w};
+        long long rnd[4] = {0, 0, 0, 0};  // 2^(shift-2) in the high word
+        if constexpr (FAST) {
+            const int4 r4 = *(const int4 *)(prm + EPI_RND * WV_BCO + cl);
+            rnd[0] = (long long)r4.x << 32; rnd[1] = (long long)r4.y << 32;
+            rnd[2] = (long long)r4.z << 32; rnd[3] = (long long)r4.w << 32;
+        }
+        int sc[4] = {0, 0, 0, 0}, sd[4] = {0, 0, 0, 0}, sside[4] = {0, 0, 0, 0};
+        if constexpr (SKK != 0 && !LUT) {
+            const int4 c4 = *(const int4 *)(prm + EPI_SKIP_C * WV_BCO + cl);
+            const int4 d4 = *(const int4 *)(prm + EPI_SKIP_D * WV_BCO + cl);
+            const int4 e4 = *(const int4 *)(prm + EPI_SKIP_SIDE * WV_BCO + cl);
+            sc[0] = c4.x; sc[1] = c4.y; sc[2] = c4.z; sc[3] = c4.w;
+            sd[0] = d4.x; sd[1] = d4.y; sd[2] = d4.z; sd[3] = d4.w;
+            sside[0] = e4.x; sside[1] = e4.y; sside[2] = e4.z; sside[3] = e4.w;
+        }
+#pragma unroll
+        for (int j = j0; j < j1; ++j) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int v = acc[i][j][e];  // acc + bias
+                const int bit = (4 * i + e) * BI;
+                int kv = 0;
+                if constexpr (SKK == 1)
+                    kv = (int)__builtin_amdgcn_ubfe(skw[j][bit >> 5], bit & 31, BI);
+                int y;
+                if constexpr (FAST) {
+                    int u = v;
+                    // u fits in int32, so sums modulo 2^32 are exact
+                    if constexpr (LUT) {
+                        u = (int)((unsigned)v + (unsigned)lut_l[((4 * i + e) << BI) + kv]);
+                    } else if constexpr (SKK != 0) {
+                        const int scaled = rsm32(sside[e] ? v : kv, sc[e], sd[e]);
+                        u = (int)((unsigned)scaled + (unsigned)(sside[e] ? kv : v));
+                    }
+                    y = requant32(u, mult[e], rnd[e], shf[e]);
+                    y = y < 0 ? 0 : (y > QMAX ? QMAX : y);
+                } else {
+                    long long u = v;
+                    if constexpr (LUT)
+                        u = (int)((unsigned)v + (unsigned)lut_l[((4 * i + e) << BI) + kv]);
+                    else if constexpr (SKK != 0)
+                        u = align_add(v, kv, sc[e], sd[e], sside[e]);
+                    y = (int)requant_clamp(u, mult[e], shf[e], QMAX);
+                }
+                outw[j][bit >> 5] |= (uint32_t)y << (bit & 31);
+            }
+        }
+    };
+    auto body = [&](auto lut_c) { static_for<MI>([&](auto ic) { group(lut_c, ic, 0, NJ); }); };
+    if (use_lut)
+        body(std::true_type{});
+    else
+        body(std::false_type{});
+    if (A.qmax == 7) {  // 3-bit codes (the epilogue clamped to 15)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            outw[j][0] = sat7_nibbles(outw[j][0]);
+            outw[j][1] = sat7_nibbles(outw[j][1]);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+        if (okj[j])
+            *(uint2 *)((uint8_t *)S.y + (px0 + 16 * j) * (A.cout * BI / 8) + co_glob * BI / 8) =
+                make_uint2(outw[j][0], outw[j][1]);
+}
+
+}  // namespace
+
+hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream)
+{
+    if (a.bits_out != 4 || (a.skip_bits != 0 && a.skip_bits != 4) || a.cin % 256 != 0 ||
+        a.ksteps % 4 != 0 || a.ksplit != 1 || a.part != 0)
+        return hipErrorInvalidValue;
+    dim3 grid(8 * a.tiles_per_xcd), block(256);
+    bool fast = true;
+    for (int i = 0; i < a.nseg; ++i)
+        fast = fast && a.seg[i].fast;
+    if (a.skip_bits == 0) {
+        if (fast)
+            hipLaunchKernelGGL((qconv_wv_kernel<0, 1>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_wv_kernel<0, 0>), grid, block, 0, stream, a);
+    } else {
+        if (fast)
+            hipLaunchKernelGGL((qconv_wv_kernel<1, 1>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_wv_kernel<1, 0>), grid, block, 0, stream, a);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace aqd

@@ -160,6 +160,88 @@ def test_conv_stream_parity(torch, case, variant):
         assert_same(got, oracle_conv(c, level), f"stream {variant} {case} level {level}")
 
 
+# cin a multiple of 256, code outputs and at least 200 tiles of 256 x 128:
+# the register-fed kernel (weights read into registers, codes staged in LDS
+# four K steps at a time). The head-tower shape, two and four stages per
+# tap, stride 2, a partial channel tile, code skips with and without the
+# upsample, 3-bit codes, ragged pixel tails.
+WV_CASES = [
+    # (n, h, w, cin, cout, k, stride, bits_in, bits_w, wenc, bits_out, skip_bits, up2)
+    (2, 100, 167, 256, 256, 3, 1, 4, 4, 1, 4, 0, False),    # head-tower shape: 261 tiles
+    (1, 120, 230, 512, 256, 3, 1, 4, 4, 0, 4, 0, False),    # two stages per tap: 216 tiles
+    (1, 150, 181, 1024, 256, 1, 1, 4, 4, 1, 4, 4, True),    # 1x1, four stages per tap, upsampled skip
+    (2, 203, 131, 256, 288, 3, 2, 4, 4, 0, 4, 4, False),    # stride 2, a partial channel tile, skip
+    (8, 50, 84, 256, 256, 3, 1, 3, 3, 1, 3, 3, False),      # 3-bit codes and skip, batch 8
+]
+
+
+def _wv_tiles(case):
+    n, h, w, cin, cout, k, s = case[:7]
+    ho, wo = (h + 2 * (k // 2) - k) // s + 1, (w + 2 * (k // 2) - k) // s + 1
+    return -(-n * ho * wo // 128) * -(-cout // 256)
+
+
+@pytest.mark.parametrize("case", WV_CASES, ids=lambda c: "x".join(map(str, c)))
+@pytest.mark.parametrize("variant", ["random_sides", "side0", "small_shifts"])
+def test_conv_register_fed_parity(torch, case, variant):
+    """Per-channel skip sides, all sides 0 (the skip table), and shifts < 2
+    (64-bit requantisation)."""
+    assert _wv_tiles(case) >= 200 and case[3] % 256 == 0
+    n, h, w, cin, cout, k, s, bi, bw, wenc, bo, sb, up2 = case
+    c = workloads.random_conv_case(seed=hash(case) % 1000 + 81, n=n, h=h, w=w, cin=cin, cout=cout,
+                                   k=k, stride=s, bits_in=bi, bits_w=bw, wenc=wenc, bits_out=bo,
+                                   skip_bits=sb, skip_up2=up2)
+    rng = np.random.Generator(np.random.PCG64(31))
+    for lv in c.levels:
+        if variant == "side0" and sb:
+            lv["skip_side"][:] = 0
+        if variant == "small_shifts":
+            lv["shift"] = rng.integers(-2, 2, size=cout).astype(np.int32)
+            lv["mult"] = rng.integers(1 << 24, 1 << 27, size=cout).astype(np.int32)
+    for level, got in enumerate(gpu_conv(c, torch)):
+        assert_same(got, oracle_conv(c, level), f"register-fed {variant} {case} level {level}")
+
+
+def test_register_fed_grouped_levels_and_guard_bytes(torch):
+    """The head towers' launch shape on the register-fed kernel: two handles
+    (class and box towers), five pyramid levels each with its own table, one
+    launch; every output sits between guard bytes that must stay untouched."""
+    dev = torch.device("cuda:0")
+    n, sizes = 3, [(50, 75), (25, 38), (13, 19), (7, 10), (4, 5)]
+    cases = [workloads.random_conv_case(seed=90 + t, n=1, h=8, w=8, cin=256, cout=256, k=3,
+                                        bits_in=4, bits_w=4, wenc=1, bits_out=4, num_levels=5)
+             for t in range(2)]
+    handles = [aqd.qconv_create(256, 256, 3, 1, 1, 4, 4, aqd.pack_codes(c.w_fields, 4), c.levels,
+                                wenc=1, bits_out=4) for c in cases]
+    rng = np.random.Generator(np.random.PCG64(19))
+    try:
+        segs, expect, outs = [], [], []
+        for t, c in enumerate(cases):
+            for lv, (h, w) in enumerate(sizes):
+                x = rng.integers(0, 16, size=(n, h, w, 256))
+                xd = torch.from_numpy(aqd.pack_codes(x, 4)).to(dev)
+                nbytes = n * h * w * 128
+                buf = torch.full((nbytes + 4096,), 0x5A, dtype=torch.uint8, device=dev)
+                yd = buf[2048:2048 + nbytes]
+                segs.append((handles[t], lv, n, h, w, xd, None, 0, 0, yd))
+                outs.append((buf, nbytes))
+                L = c.levels[lv]
+                want = ref.qconv(x, c.w_fields, 4, 1, 1, L["bias"], wenc=1, mult=L["mult"],
+                                 shift=L["shift"], bits_out=4)
+                expect.append(ref.pack_codes(want, 4).reshape(-1))
+        tiles = sum(-(-s[2] * s[3] * s[4] // 128) for s in segs)
+        assert tiles >= 200
+        aqd.qconv_run_group(segs)
+        torch.cuda.synchronize()
+        for i, ((buf, nbytes), want) in enumerate(zip(outs, expect)):
+            host = buf.cpu().numpy()
+            assert np.all(host[:2048] == 0x5A) and np.all(host[2048 + nbytes:] == 0x5A), i
+            assert_same(host[2048:2048 + nbytes], want, f"segment {i}")
+    finally:
+        for h in handles:
+            aqd.qconv_destroy(h)
+
+
 # Launches of more than one round of 128 x 256 or 64 x 512 tiles without a
 # skip run on tiles half as wide, three workgroups to a CU: 1x1 and 3x3,
 # stride 2, int32 and code outputs, ragged pixel tails.
