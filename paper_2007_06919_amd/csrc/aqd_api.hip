@@ -541,8 +541,10 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         } else if (t128 >= 64 && t128 < 200 && h0.ksteps <= 80) {
             tile_cfg = TILE_256x64;
             blk_px = 64;
-        } else if (h0.d.bits_in == 4 && h0.d.cin % 256 == 0 && h0.d.out_mode == AQD_OUT_CODES &&
-                   (h0.d.skip_bits == 0 || h0.d.skip_bits == 4) && t128 >= 200) {
+        } else if (h0.d.bits_in == 4 && h0.d.cin % 256 == 0 &&
+                   (h0.d.out_mode == AQD_OUT_CODES ? (h0.d.skip_bits == 0 || h0.d.skip_bits == 4)
+                                                   : h0.d.skip_bits == 0) &&
+                   t128 >= 200) {
             // 256-channel input chunks: weights read into registers (no LDS
             // traffic for them), activation codes staged in LDS four K steps
             // at a time

@@ -1,8 +1,9 @@
 // Implicit-GEMM integer convolution on the gfx950 int8 MFMA
 // (v_mfma_i32_16x16x64_i8) for layers with 256-channel input chunks (cin a
-// multiple of 256), 4-bit activation codes and code outputs: the detection
-// heads' 3x3 256 -> 256 towers, the FPN's 3x3 outputs, ResNet-50's res4/res5
-// 3x3 and 1x1 layers with cin >= 512. The GEMM view is that of Eq. 4
+// multiple of 256) and 4-bit activation codes, with code outputs (the
+// detection heads' 3x3 256 -> 256 towers, the FPN's 3x3 outputs, ResNet-50's
+// res4/res5 3x3 and 1x1 layers with cin >= 512) or int32 outputs (the class
+// predictor). The GEMM view is that of Eq. 4
 // (Sec. 3.2.1): rows = output channels (weights), columns = output pixels,
 // K = taps x input channels, one K step = 64 input channels of one tap.
 //
@@ -44,10 +45,12 @@ constexpr int WV_STAGE = WV_BPX * WV_ROW;  // 16 KiB
 constexpr int WV_NBUF = 4;
 constexpr int WV_LDS = WV_NBUF * WV_STAGE;
 
+// OUTK: 0 = 4-bit codes, 1 = int32 v = acc + bias (then SKK = 0);
 // SKK: 0 = no skip, 1 = code skip (4-bit); FAST: every shift >= 2 (32-bit requantisation)
-template <int SKK, int FAST>
+template <int OUTK, int SKK, int FAST>
 __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
 {
+    static_assert(OUTK == 0 || SKK == 0, "int32 outputs have no skip");
     constexpr int BI = 4, MI = 4, NJ = 8, QMAX = 15, OW = 2;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[WV_LDS];
 
@@ -239,13 +242,50 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
     // its loads are issued before the last stage, whose MFMAs hide their latency
     constexpr int PRM_PER = EPI_FIELDS * WV_BCO / 256;
     int prm_r[PRM_PER];
+    if constexpr (OUTK == 0) {
 #pragma unroll
-    for (int t = 0; t < PRM_PER; ++t) {
-        const int i = tid + 256 * t;
-        const int which = i / WV_BCO, c = i - which * WV_BCO;
-        prm_r[t] = S.epi[which * A.cout_pad + co_tile * WV_BCO + c];
+        for (int t = 0; t < PRM_PER; ++t) {
+            const int i = tid + 256 * t;
+            const int which = i / WV_BCO, c = i - which * WV_BCO;
+            prm_r[t] = S.epi[which * A.cout_pad + co_tile * WV_BCO + c];
+        }
     }
     stage(NST - 1);
+
+    if constexpr (OUTK == 1) {
+        // int32 outputs v = acc + bias (the bias is in the accumulators), in
+        // two passes of 64 pixels (column tiles 4p .. 4p+3): each lane's 16
+        // channels x 4 pixels go to LDS as rows of 256 int32 (1 KiB per pixel;
+        // 16-byte chunk c of pixel p at position c ^ (p & 7), so that neither
+        // the writes nor the reads conflict), then every thread stores 16-byte
+        // chunks of whole rows: 1 KiB of contiguous output per wave and
+        // instruction
+        const int valid_chunks = (A.cout - co_tile * WV_BCO < WV_BCO ? A.cout - co_tile * WV_BCO : WV_BCO) / 4;
+        static_for<2>([&](auto pc) {
+            constexpr int pass = decltype(pc)::value;
+            __syncthreads();  // the ring, or the last pass's rows, are no longer read
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int p = 16 * jj + r;
+#pragma unroll
+                for (int i = 0; i < MI; ++i) {
+                    const int c = co_loc / 4 + i;
+                    *(v4i *)(lds + p * 1024 + 16 * (c ^ (p & 7))) = acc[i][4 * pass + jj];
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int it = 0; it < 16; ++it) {
+                const int idx = it * 256 + tid;
+                const int p = idx >> 6, c = idx & 63;
+                const long long px = (long long)px_tile * WV_BPX + 64 * pass + p;
+                if (px < S.P && c < valid_chunks)
+                    *(v4i *)((int32_t *)S.y + px * A.cout + co_tile * WV_BCO + 4 * c) =
+                        *(const v4i *)(lds + p * 1024 + 16 * (c ^ (p & 7)));
+            }
+        });
+        return;
+    }
 
     // ---------------------------------------------------------------- epilogue
     const long long px0 = (long long)px_tile * WV_BPX + r;
@@ -383,23 +423,25 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
 
 hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream)
 {
-    if (a.bits_out != 4 || (a.skip_bits != 0 && a.skip_bits != 4) || a.cin % 256 != 0 ||
-        a.ksteps % 4 != 0 || a.ksplit != 1 || a.part != 0)
+    if ((a.bits_out != 4 && a.bits_out != 32) || (a.skip_bits != 0 && (a.skip_bits != 4 || a.bits_out == 32)) ||
+        a.cin % 256 != 0 || a.ksteps % 4 != 0 || a.ksplit != 1 || a.part != 0)
         return hipErrorInvalidValue;
     dim3 grid(8 * a.tiles_per_xcd), block(256);
     bool fast = true;
     for (int i = 0; i < a.nseg; ++i)
         fast = fast && a.seg[i].fast;
-    if (a.skip_bits == 0) {
+    if (a.bits_out == 32)
+        hipLaunchKernelGGL((qconv_wv_kernel<1, 0, 1>), grid, block, 0, stream, a);
+    else if (a.skip_bits == 0) {
         if (fast)
-            hipLaunchKernelGGL((qconv_wv_kernel<0, 1>), grid, block, 0, stream, a);
+            hipLaunchKernelGGL((qconv_wv_kernel<0, 0, 1>), grid, block, 0, stream, a);
         else
-            hipLaunchKernelGGL((qconv_wv_kernel<0, 0>), grid, block, 0, stream, a);
+            hipLaunchKernelGGL((qconv_wv_kernel<0, 0, 0>), grid, block, 0, stream, a);
     } else {
         if (fast)
-            hipLaunchKernelGGL((qconv_wv_kernel<1, 1>), grid, block, 0, stream, a);
+            hipLaunchKernelGGL((qconv_wv_kernel<0, 1, 1>), grid, block, 0, stream, a);
         else
-            hipLaunchKernelGGL((qconv_wv_kernel<1, 0>), grid, block, 0, stream, a);
+            hipLaunchKernelGGL((qconv_wv_kernel<0, 1, 0>), grid, block, 0, stream, a);
     }
     return hipGetLastError();
 }

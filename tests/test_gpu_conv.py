@@ -202,6 +202,24 @@ def test_conv_register_fed_parity(torch, case, variant):
         assert_same(got, oracle_conv(c, level), f"register-fed {variant} {case} level {level}")
 
 
+WV_INT32_CASES = [
+    # int32 outputs v = acc + bias through the register-fed kernel
+    (1, 100, 167, 256, 720, 3, 1, 4, 4, 1, 32, 0, False),   # class predictor: 720 = 2 x 256 + 208
+    (5, 60, 100, 512, 256, 1, 1, 4, 4, 0, 32, 0, False),    # 1x1, two stages per tap
+    (8, 201, 163, 256, 256, 3, 2, 4, 4, 1, 32, 0, False),   # stride 2, ragged pixel tail
+]
+
+
+@pytest.mark.parametrize("case", WV_INT32_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_conv_register_fed_int32_parity(torch, case):
+    assert _wv_tiles(case) >= 200 and case[3] % 256 == 0
+    n, h, w, cin, cout, k, s, bi, bw, wenc, bo, sb, up2 = case
+    c = workloads.random_conv_case(seed=hash(case) % 1000 + 85, n=n, h=h, w=w, cin=cin, cout=cout,
+                                   k=k, stride=s, bits_in=bi, bits_w=bw, wenc=wenc, bits_out=bo)
+    for level, got in enumerate(gpu_conv(c, torch)):
+        assert_same(got, oracle_conv(c, level), f"register-fed int32 {case} level {level}")
+
+
 def test_register_fed_grouped_levels_and_guard_bytes(torch):
     """The head towers' launch shape on the register-fed kernel: two handles
     (class and box towers), five pyramid levels each with its own table, one
