@@ -4,10 +4,13 @@
 
 One step = one forward pass of all 110 convolution segments over the batch
 (grouped launches on one HIP stream, recorded once into a HIP graph and
-replayed), inputs resident in HBM. The dominant kernel is the grouped
+replayed), inputs resident in HBM; each replay is bracketed by HIP events
+(mean, median, p10 and p90 per step). The dominant kernel is the grouped
 head-tower launch (3x3, 256 -> 256, class and box towers, five pyramid
 levels, eight images); a second timed pass enqueues the same steps launch by
-launch, with HIP events on the launch stream around each head-tower launch.
+launch on one stream, with HIP events on that stream around every grouped
+launch: the per-launch table (integer TOPS, GB/s against algorithmic bytes,
+fraction of the binding MFMA or HBM roof) and the head-tower launch time.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -24,62 +27,113 @@ sys.path.insert(0, ROOT)
 
 METRIC = "int TOPS per qconv layer + ms/image quantized RetinaNet-R50 800x1333, 1 GPU"
 MFMA_I8_PEAK_TOPS = 5000.0  # MI355X dense int8 MFMA
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 COPY_PROBE_BYTES = 256 << 20
 
 # HBM traffic of one head-tower launch, from two rocprofv3 counter runs
 # (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain copy of
 # COPY_PROBE_BYTES; valid only for the kernel source it was measured on.
-HEAD_TRAFFIC = {"kernel_sha256": "73fe7bae65181170d6e8b36f82f623e5bf55fbb9a8e17f1ec27d51190f8c6efb",
-                "fetch_bytes": 50980075, "write_bytes": 45670400}
+HEAD_KERNEL = "qconv_wv_kernel<0, 0, 1>"
+HEAD_KERNEL_SOURCES = ("qconv_wv.hip", "mfma_common.h")
+HEAD_TRAFFIC = {"kernel_sha256": "38688460b537cb2ba638d17ad9fe57cf21dacf978c3eecc076cae61e88d993ed",
+                "fetch_bytes": 51141251, "write_bytes": 45670400}
 
 
 def kernel_sha256():
+    """Hash of the dominant kernel's sources (the kernel and its helpers)."""
     import hashlib
-    with open(os.path.join(ROOT, "paper_2007_06919_amd", "csrc", "qconv_mfma.hip"), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for name in HEAD_KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2007_06919_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(budget_s=12.0, bits=4):
-    """The oracle on a bounded sample of the workload: the 3x3 256 -> 256
-    head-tower convolution of one image over the five pyramid levels
-    (seeded codes and epilogue tables of the same shapes), repeated until the
-    time budget is spent. Returns the oracle's integer-op rate."""
-    import numpy as np
-    from oracle import ref
+def cpu_baseline(bits=4):
+    """The oracle on a bounded sample of every workload: one image of each
+    (the calibration image; both images of the literal basic block), the
+    whole network per image, seeded inputs and parameters as on the GPU.
+    value: the oracle's integer-op rate on the sample of the timed workload
+    (one of its eight images); per_config: the oracle's wall time per sample
+    and the time the whole workload would take at that rate."""
+    from oracle import network, ref
     from paper_2007_06919_amd import workloads
 
-    sizes = workloads.pyramid_sizes(800, 1333)
-    done_ops, t_total, layers = 0, 0.0, 0
-    seed = 1000
-    while t_total < budget_s:
-        for lv, (h, w) in enumerate(sizes):
-            case = workloads.random_conv_case(seed, 1, h, w, 256, 256, k=3, bits_in=bits, bits_w=bits,
-                                              wenc=workloads.WENC_PAPER_ODD, bits_out=bits)
-            seed += 1
-            L = case.levels[0]
-            t0 = time.perf_counter()
-            ref.qconv(case.x, case.w_fields, bits, 1, 1, L["bias"], wenc=case.wenc, mult=L["mult"],
-                      shift=L["shift"], bits_out=bits)
-            t_total += time.perf_counter() - t0
-            done_ops += 2 * h * w * 256 * 9 * 256
-        layers += 1
-    return {"value": done_ops / t_total / 1e12, "unit": "int TOPS", "cores": ref.num_threads(),
+    per, main = {}, None
+    for idx, name in enumerate(workloads.CONFIG_NAMES):
+        if bits != 4 and idx == 4:
+            net, params = workloads.retinanet_config(8, 800, 1333, bits)
+            name = f"retinanet_r50_fpn_n8_800x1333_{bits}bit"
+        else:
+            net, params = workloads.config(idx)
+        n = net.tensors[net.inputs[0]].n
+        images = list(range(n)) if params.mode == "literal" else sorted(set(params.calib_images))
+        t0 = time.perf_counter()
+        network.run(net, params, images=images, keep=set())
+        wall = time.perf_counter() - t0
+        macs = net.total_macs() * len(images) // n
+        per[name] = {"images": f"{len(images)} of {n}", "wall_s": round(wall, 3),
+                     "full_wall_s": round(wall * n / len(images), 3),
+                     "int_tops": round(2 * macs / wall / 1e12, 5)}
+        log(f"[bench] oracle {name}: {len(images)} of {n} images in {wall:.2f} s")
+        if idx == 4:
+            main = (2 * macs / wall / 1e12, name, len(images), n, wall)
+    tops, name, k, n, wall = main
+    return {"value": round(tops, 5), "unit": "int TOPS", "cores": ref.num_threads(),
             "kind": "oracle",
-            "sample": f"{layers} x (3x3 256->256 {bits}-bit head-tower conv of one 800x1333 image over "
-                      f"P3-P7, {done_ops / 2 / 1e9:.1f} GMAC total, {t_total:.1f} s)"}
+            "sample": f"{name}: {k} of {n} images through the whole network ({wall:.1f} s); "
+                      f"the other workloads one image each (per_config)",
+            "per_config": per}
+
+
+def launch_cost(gpu, group):
+    """(integer ops, algorithmic HBM bytes) of one grouped launch: every input
+    code, weight, skip operand and output read or written once. A fused
+    projection shortcut adds its own input and weights; its int32 output is
+    never materialised."""
+    from paper_2007_06919_amd import aqd
+    net = gpu.net
+    sb = aqd.stored_bits
+
+    def tbytes(name):
+        t = net.tensors[name]
+        return t.n * t.h * t.w * t.c * (32 if t.bits == 32 else sb(t.bits)) // 8
+
+    macs, nbytes, seen = 0, 0, set()
+    for conv, si in group:
+        x, skip, y = conv.segs[si]
+        ty = net.tensors[y]
+        macs += ty.n * ty.h * ty.w * conv.cout * conv.k * conv.k * conv.cin
+        nbytes += tbytes(x) + tbytes(y)
+        if conv.name not in seen:
+            nbytes += conv.k * conv.k * conv.cin * conv.cout * sb(conv.bits_w) // 8
+            seen.add(conv.name)
+        proj = gpu.fused.get(conv.name)
+        if proj is not None:
+            px, _, py = proj.segs[0]
+            tp = net.tensors[py]
+            macs += tp.n * tp.h * tp.w * proj.cout * proj.cin
+            nbytes += tbytes(px) + proj.cin * proj.cout * sb(proj.bits_w) // 8
+        elif skip is not None:
+            nbytes += tbytes(skip)
+    return 2 * macs, nbytes
+
+
+def pct(v, q):
+    import numpy as np
+    return float(np.percentile(np.asarray(v), q))
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--bits", type=int, default=4, choices=(3, 4),
                     help="code width of the network (3: the paper's 3-bit RetinaNet, codes in "
                          "4-bit containers; the default 4 is the benchmarked workload)")
@@ -116,17 +170,17 @@ def main():
 
     n_img = net.tensors[net.inputs[0]].n
     total_ops = 2 * net.total_macs()
-    dominant = [gi for gi, g in enumerate(gpu.schedule)
-                if g[0][0].k == 3 and g[0][0].cin == 256 and g[0][0].cout == 256
-                and g[0][0].name.startswith(("cls.t", "box.t"))]
-    dom_ops = [2 * gpu.group_macs(gpu.schedule[gi]) for gi in dominant]
+    live = [gi for gi in range(len(gpu.schedule)) if gpu.lane[gi] is not None]
+    cost = {gi: launch_cost(gpu, gpu.schedule[gi]) for gi in live}
+    dominant = [gi for gi in live if gpu.schedule[gi][0][0].k == 3
+                and gpu.schedule[gi][0][0].cin == 256 and gpu.schedule[gi][0][0].cout == 256
+                and gpu.schedule[gi][0][0].name.startswith(("cls.t", "box.t"))]
     events = {}
 
-    def hook(gi, when):
-        if gi in dominant:
-            ev = torch.cuda.Event(enable_timing=True)
-            ev.record(stream)
-            events.setdefault(gi, []).append(ev)
+    def hook(gi, when, s):
+        ev = torch.cuda.Event(enable_timing=True)
+        ev.record(s)
+        events.setdefault(gi, []).append(ev)
 
     with torch.cuda.stream(stream):
         for _ in range(args.warmup):
@@ -138,42 +192,57 @@ def main():
             gpu.replay()
         stream.synchronize()
         torch.cuda.synchronize()
-        start = torch.cuda.Event(enable_timing=True)
-        end = torch.cuda.Event(enable_timing=True)
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
         wall0 = time.perf_counter()
-        start.record(stream)
-        for _ in range(args.steps):
+        marks[0].record(stream)
+        for i in range(args.steps):
             gpu.replay()
-        end.record(stream)
+            marks[i + 1].record(stream)
         stream.synchronize()
         torch.cuda.synchronize()
         wall = time.perf_counter() - wall0
-        # the same steps launch by launch, with events around the dominant launch
+        # the same steps launch by launch on one stream (no overlap), with
+        # events on the launch stream around every grouped launch
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for _ in range(args.steps):
-            gpu.forward(stream, launch_hook=hook)
+            gpu.forward(stream, launch_hook=hook, serial=True)
         e1.record(stream)
         stream.synchronize()
         torch.cuda.synchronize()
-    ms_total = start.elapsed_time(end)
-    ms_step = ms_total / args.steps
-    eager_ms_step = e0.elapsed_time(e1) / args.steps
+    step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]
+    ms_step = marks[0].elapsed_time(marks[-1]) / args.steps
+    serial_ms_step = e0.elapsed_time(e1) / args.steps
     value = total_ops / (ms_step / 1e3) / 1e12
 
-    durs, ops = [], []
-    for gi, o in zip(dominant, dom_ops):
-        evs = events[gi]
-        for k in range(0, len(evs), 2):
-            durs.append(evs[k].elapsed_time(evs[k + 1]))
-            ops.append(o)
-    avg_ms = float(np.mean(durs))
-    avg_ops = float(np.mean(ops))
-    achieved = avg_ops / (avg_ms / 1e3) / 1e12
-    log(f"[bench] {ms_step:.3f} ms/step as a graph replay (wall {wall / args.steps * 1e3:.3f} ms; "
-        f"{eager_ms_step:.3f} ms launch by launch), "
-        f"{value:.1f} int TOPS; head-tower launch {avg_ms * 1e3:.1f} us, {achieved:.1f} TOPS")
+    launch_us = {gi: [1e3 * evs[k].elapsed_time(evs[k + 1]) for k in range(0, len(evs), 2)]
+                 for gi, evs in events.items()}
+    per_launch = []
+    for gi in live:
+        ops, nbytes = cost[gi]
+        us = float(np.median(launch_us[gi]))
+        t_mfma = ops / (MFMA_I8_PEAK_TOPS * 1e12) * 1e6
+        t_hbm = nbytes / (HBM_PEAK_GBS * 1e9) * 1e6
+        bound = "mfma" if t_mfma >= t_hbm else "hbm"
+        conv0 = gpu.schedule[gi][0][0]
+        per_launch.append({
+            "launch": "+".join(sorted({c.name for c, _ in gpu.schedule[gi]})),
+            "segments": len(gpu.schedule[gi]), "shape": f"{conv0.k}x{conv0.k} {conv0.cin}->{conv0.cout}",
+            "us": round(us, 2), "int_tops": round(ops / us / 1e6, 1),
+            "gbs": round(nbytes / us / 1e3, 1), "bound": bound,
+            "frac": round(max(t_mfma, t_hbm) / us, 4),
+            "mfma_frac": round(t_mfma / us, 4), "hbm_frac": round(t_hbm / us, 4)})
+
+    durs = [u for gi in dominant for u in launch_us[gi]]
+    dom_ops = [cost[gi][0] for gi in dominant for _ in launch_us[gi]]
+    avg_us = float(np.mean(durs))
+    avg_ops = float(np.mean(dom_ops))
+    achieved = avg_ops / (avg_us / 1e6) / 1e12
+    log(f"[bench] {ms_step:.3f} ms/step as a graph replay (median {np.median(step_ms):.3f}, "
+        f"p10 {pct(step_ms, 10):.3f}, p90 {pct(step_ms, 90):.3f}; wall "
+        f"{wall / args.steps * 1e3:.3f} ms; {serial_ms_step:.3f} ms launch by launch on one "
+        f"stream), {value:.1f} int TOPS; head-tower launch {avg_us:.1f} us, {achieved:.1f} TOPS")
 
     out = {
         "metric": METRIC, "value": round(value, 3), "unit": "int TOPS", "n_gpus": 1,
@@ -185,13 +254,18 @@ def main():
                    "launches_per_step": gpu.launches_per_forward(), "int_ops_per_step": total_ops,
                    "hip_graph": True},
         "ms_per_image": round(ms_step / n_img, 4),
-        "eager_ms_per_step": round(eager_ms_step, 4),
+        "step_ms": {"mean": round(ms_step, 4), "median": round(float(np.median(step_ms)), 4),
+                    "p10": round(pct(step_ms, 10), 4), "p90": round(pct(step_ms, 90), 4),
+                    "replays": args.steps},
+        "serial_ms_per_step": round(serial_ms_step, 4),
         "roofline": {"bound": "mfma",
-                     "kernel": "qconv_mfma_kernel<4,8,4,2,2,0,0,1,0> (head towers 3x3 256->256, "
-                               "10 segments, 256x128 tiles)",
+                     "kernel": f"{HEAD_KERNEL} (head towers 3x3 256->256, 10 segments, "
+                               f"256x128 tiles)",
                      "achieved": round(achieved, 2), "peak": MFMA_I8_PEAK_TOPS, "unit": "TOPS",
                      "frac": round(achieved / MFMA_I8_PEAK_TOPS, 4), "traffic": None,
-                     "avg_launch_us": round(avg_ms * 1e3, 2), "ops_per_launch": int(avg_ops)},
+                     "avg_launch_us": round(avg_us, 2), "ops_per_launch": int(avg_ops),
+                     "launch_us_p10_p50_p90": [round(pct(durs, q), 2) for q in (10, 50, 90)]},
+        "per_launch": per_launch,
     }
     traffic = None
     if args.bits == 4 and HEAD_TRAFFIC and HEAD_TRAFFIC["kernel_sha256"] == kernel_sha256():
@@ -207,7 +281,7 @@ def main():
         log(f"[bench] copy probe: {COPY_PROBE_BYTES} bytes device to device")
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
-        out["cpu_baseline"] = cpu_baseline(args.cpu_budget, args.bits)
+        out["cpu_baseline"] = cpu_baseline(args.bits)
     print(json.dumps(out), flush=True)
 
 

@@ -333,9 +333,11 @@ class Net:
         self.stream.synchronize()
 
     # -------------------------------------------------------------- running
-    def forward(self, stream=None, launch_hook=None):
+    def forward(self, stream=None, launch_hook=None, serial=False):
         """Enqueue the whole network on the stream. launch_hook(group_index,
-        'before'|'after') is called around each grouped launch (for timing)."""
+        'before'|'after', stream) is called around each grouped launch (for
+        timing). serial: every launch on the one stream, in schedule order
+        (a topological order), so that no two launches overlap."""
         torch = self.torch
         main = self.stream if stream is None else stream
         streams = [main] + self.side
@@ -343,7 +345,7 @@ class Net:
         tail = {}          # side stream -> event after its last launch
         # side streams start after the work already enqueued on the main stream
         start = None
-        if len(self.side):
+        if len(self.side) and not serial:
             start = torch.cuda.Event()
             start.record(main)
         started = set()
@@ -351,23 +353,25 @@ class Net:
             k = self.lane[gi]
             if k is None:
                 continue
+            if serial:
+                k = 0
             s = streams[k]
             if k and k not in started:
                 s.wait_event(start)
                 started.add(k)
-            for d in self.deps[gi]:
+            for d in self.deps[gi] if not serial else ():
                 if self.lane[d] is not None and self.lane[d] != k:
                     s.wait_event(done[d])
             if launch_hook:
-                launch_hook(gi, "before")
+                launch_hook(gi, "before", s)
             sh = s.cuda_stream
             for fn, args in self._calls[gi]:
                 st = fn(*args, sh)
                 if st != aqd.AQD_OK:
                     raise aqd.AqdError(st, aqd.last_error())
             if launch_hook:
-                launch_hook(gi, "after")
-            if gi in self.signal:
+                launch_hook(gi, "after", s)
+            if gi in self.signal and not serial:
                 ev = torch.cuda.Event()
                 ev.record(s)
                 done[gi] = ev

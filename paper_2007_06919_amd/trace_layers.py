@@ -45,7 +45,7 @@ def layer_table(trace_csv, workload=4, top=30, passes=5):
     net, _ = workloads.config(workload)
     launches = launch_list(net)
     rows = sorted((r for r in csv.DictReader(open(trace_csv))
-                   if any(k in r["Kernel_Name"] for k in ("qconv_mfma", "qconv_stream", "qconv_direct", "splitk"))),
+                   if any(k in r["Kernel_Name"] for k in ("qconv_", "splitk_"))),
                   key=lambda r: int(r["Dispatch_Id"]))  # enqueue order (launches on several streams overlap)
     # one entry per launch; a combining kernel belongs to the launch before it
     seq = []
