@@ -27,6 +27,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "int TOPS per qconv layer + ms/image quantized RetinaNet-R50 800x1333, 1 GPU"
 MFMA_I8_PEAK_TOPS = 5000.0  # MI355X dense int8 MFMA
+MFMA_FP4_PEAK_TOPS = 10100.0  # MI355X dense FP4 MFMA
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 COPY_PROBE_BYTES = 256 << 20
 
@@ -128,6 +129,80 @@ def pct(v, q):
     return float(np.percentile(np.asarray(v), q))
 
 
+def fp4_layer(args):
+    """The 2-bit head-tower launch (class and box towers' 3x3 256 -> 256 layer
+    over P3-P7 of a batch of eight 800x1333 images: 10 segments, one grouped
+    launch) on the FP4 MFMA path and on the int8 MFMA path (handles created
+    with AQD_NO_FP4=1); both outputs must agree byte for byte."""
+    import numpy as np
+    import torch
+    from paper_2007_06919_amd import aqd, workloads
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.Stream(device=dev)
+    sizes = workloads.pyramid_sizes(800, 1333)
+    n = 8
+    rng = np.random.Generator(np.random.PCG64(2))
+    cases = [workloads.random_conv_case(seed=70 + t, n=1, h=8, w=8, cin=256, cout=256, k=3, bits_in=2,
+                                        bits_w=2, wenc=workloads.WENC_PAPER_ODD, bits_out=2,
+                                        num_levels=len(sizes)) for t in range(2)]
+    xs = [torch.from_numpy(aqd.pack_codes(rng.integers(0, 4, size=(n, h, w, 256)), 2)).to(dev)
+          for h, w in sizes]
+
+    def handles(no_fp4):
+        old = os.environ.get("AQD_NO_FP4")
+        os.environ["AQD_NO_FP4"] = "1" if no_fp4 else "0"
+        try:
+            return [aqd.qconv_create(256, 256, 3, 1, 1, 2, 2, aqd.pack_codes(c.w_fields, 2), c.levels,
+                                     wenc=workloads.WENC_PAPER_ODD, bits_out=2) for c in cases]
+        finally:
+            if old is None:
+                del os.environ["AQD_NO_FP4"]
+            else:
+                os.environ["AQD_NO_FP4"] = old
+
+    out, res = {}, {}
+    for name, no_fp4 in (("fp4", False), ("int8", True)):
+        hs = handles(no_fp4)
+        try:
+            paths = {aqd.qconv_path(h) for h in hs}
+            ys = [[torch.empty((n, h, w, 64), dtype=torch.uint8, device=dev) for h, w in sizes]
+                  for _ in hs]
+            segs = [(hs[t], lv, n, h, w, xs[lv], None, 0, 0, ys[t][lv])
+                    for t in range(2) for lv, (h, w) in enumerate(sizes)]
+            with torch.cuda.stream(stream):
+                for _ in range(args.warmup):
+                    aqd.qconv_run_group(segs, stream)
+                stream.synchronize()
+                ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                      for _ in range(args.steps)]
+                for e0, e1 in ev:
+                    e0.record(stream)
+                    aqd.qconv_run_group(segs, stream)
+                    e1.record(stream)
+                stream.synchronize()
+            us = [1e3 * e0.elapsed_time(e1) for e0, e1 in ev]
+            res[name] = {"path": sorted(paths), "us_median": round(float(np.median(us)), 2),
+                         "us_p10": round(pct(us, 10), 2), "us_p90": round(pct(us, 90), 2)}
+            out[name] = [y.cpu().numpy() for row in ys for y in row]
+            log(f"[bench] {name}: {res[name]}")
+        finally:
+            for h in hs:
+                aqd.qconv_destroy(h)
+    assert all(np.array_equal(a, b) for a, b in zip(out["fp4"], out["int8"])), "FP4 and int8 paths differ"
+    ops = 2 * 2 * sum(n * h * w for h, w in sizes) * 256 * 9 * 256
+    for name, peak in (("fp4", MFMA_FP4_PEAK_TOPS), ("int8", MFMA_I8_PEAK_TOPS)):
+        tops = ops / (res[name]["us_median"] * 1e-6) / 1e12
+        res[name].update(int_tops=round(tops, 1), peak_tops=peak, frac=round(tops / peak, 4))
+    print(json.dumps({"metric": "2-bit head-tower launch: FP4 MFMA path vs int8 MFMA path",
+                      "unit": "us", "steps": args.steps, "warmup": args.warmup, "int_ops_per_launch": ops,
+                      "config": {"workload": "retina_head_towers_p3p7_n8_800x1333_2bit", "batch": n,
+                                 "segments": 10},
+                      "outputs_equal": True, "speedup": round(res["int8"]["us_median"] / res["fp4"]["us_median"], 3),
+                      **res}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -137,6 +212,10 @@ def main():
     ap.add_argument("--bits", type=int, default=4, choices=(3, 4),
                     help="code width of the network (3: the paper's 3-bit RetinaNet, codes in "
                          "4-bit containers; the default 4 is the benchmarked workload)")
+    ap.add_argument("--fp4-layer", action="store_true",
+                    help="instead of the network: the 2-bit head-tower launch (3x3 256->256, class "
+                         "and box towers, P3-P7, batch 8, 800x1333) on the FP4 MFMA path and on the "
+                         "int8 MFMA path, timed launch by launch")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the run, one device copy of 256 MiB (a kernel of known traffic "
                          "for calibrating memory counters)")
@@ -145,6 +224,11 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); several GPUs "
               f"would each take whole images of the batch, which is not run here.", file=sys.stderr)
         sys.exit(2)
+    import faulthandler
+    faulthandler.enable()      # a crash prints the Python stack of every thread
+    if args.fp4_layer:
+        fp4_layer(args)
+        return
 
     import numpy as np
     import torch
@@ -175,6 +259,9 @@ def main():
     dominant = [gi for gi in live if gpu.schedule[gi][0][0].k == 3
                 and gpu.schedule[gi][0][0].cin == 256 and gpu.schedule[gi][0][0].cout == 256
                 and gpu.schedule[gi][0][0].name.startswith(("cls.t", "box.t"))]
+    from paper_2007_06919_amd import aqd
+    path = {gi: aqd.qconv_path(gpu.handles[gpu.schedule[gi][0][0].name]) for gi in live}
+    peak = {gi: MFMA_FP4_PEAK_TOPS if path[gi] == "fp4-mfma" else MFMA_I8_PEAK_TOPS for gi in live}
     events = {}
 
     def hook(gi, when, s):
@@ -186,12 +273,14 @@ def main():
         for _ in range(args.warmup):
             gpu.forward(stream)
         stream.synchronize()
+        log(f"[bench] {args.warmup} eager warm-up passes done")
         # the whole network recorded once into a HIP graph; a step = one replay
         gpu.capture(stream)
         for _ in range(args.warmup):
             gpu.replay()
         stream.synchronize()
         torch.cuda.synchronize()
+        log(f"[bench] graph captured, {args.warmup} warm-up replays done")
         marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
         wall0 = time.perf_counter()
         marks[0].record(stream)
@@ -201,6 +290,7 @@ def main():
         stream.synchronize()
         torch.cuda.synchronize()
         wall = time.perf_counter() - wall0
+        log(f"[bench] {args.steps} timed replays done")
         # the same steps launch by launch on one stream (no overlap), with
         # events on the launch stream around every grouped launch
         e0 = torch.cuda.Event(enable_timing=True)
@@ -222,13 +312,14 @@ def main():
     for gi in live:
         ops, nbytes = cost[gi]
         us = float(np.median(launch_us[gi]))
-        t_mfma = ops / (MFMA_I8_PEAK_TOPS * 1e12) * 1e6
+        t_mfma = ops / (peak[gi] * 1e12) * 1e6
         t_hbm = nbytes / (HBM_PEAK_GBS * 1e9) * 1e6
         bound = "mfma" if t_mfma >= t_hbm else "hbm"
         conv0 = gpu.schedule[gi][0][0]
         per_launch.append({
             "launch": "+".join(sorted({c.name for c, _ in gpu.schedule[gi]})),
             "segments": len(gpu.schedule[gi]), "shape": f"{conv0.k}x{conv0.k} {conv0.cin}->{conv0.cout}",
+            "path": path[gi],
             "us": round(us, 2), "int_tops": round(ops / us / 1e6, 1),
             "gbs": round(nbytes / us / 1e3, 1), "bound": bound,
             "frac": round(max(t_mfma, t_hbm) / us, 4),
@@ -239,6 +330,7 @@ def main():
     avg_us = float(np.mean(durs))
     avg_ops = float(np.mean(dom_ops))
     achieved = avg_ops / (avg_us / 1e6) / 1e12
+    dom_peak = peak[dominant[0]]
     log(f"[bench] {ms_step:.3f} ms/step as a graph replay (median {np.median(step_ms):.3f}, "
         f"p10 {pct(step_ms, 10):.3f}, p90 {pct(step_ms, 90):.3f}; wall "
         f"{wall / args.steps * 1e3:.3f} ms; {serial_ms_step:.3f} ms launch by launch on one "
@@ -261,8 +353,8 @@ def main():
         "roofline": {"bound": "mfma",
                      "kernel": f"{HEAD_KERNEL} (head towers 3x3 256->256, 10 segments, "
                                f"256x128 tiles)",
-                     "achieved": round(achieved, 2), "peak": MFMA_I8_PEAK_TOPS, "unit": "TOPS",
-                     "frac": round(achieved / MFMA_I8_PEAK_TOPS, 4), "traffic": None,
+                     "achieved": round(achieved, 2), "peak": dom_peak, "unit": "TOPS",
+                     "frac": round(achieved / dom_peak, 4), "traffic": None,
                      "avg_launch_us": round(avg_us, 2), "ops_per_launch": int(avg_ops),
                      "launch_us_p10_p50_p90": [round(pct(durs, q), 2) for q in (10, 50, 90)]},
         "per_launch": per_launch,

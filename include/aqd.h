@@ -243,6 +243,16 @@ aqd_status_t qconv_run_proj(qconv_t conv, qconv_t proj, int level, int n, int h,
 
 void qconv_destroy(qconv_t conv);
 
+/* The arithmetic a handle's launches run on, fixed at create: "fp4-mfma"
+ * (2-bit codes and 2-bit weights with cin and cout multiples of 256, exact
+ * while K * 3 * max|w| < 2^24: the scaled FP4 MFMA with e2m1 operands and
+ * fp32 sums of integers), "i8-mfma" (codes widened to int8 on the int8
+ * MFMA), "direct" (every other shape: one thread per output). A static
+ * string; "invalid" for a null handle. With the environment variable
+ * AQD_NO_FP4=1 at create, 2-bit layers take the int8 MFMA path instead (the
+ * same results; for comparing the two). */
+const char *qconv_path(qconv_t conv);
+
 /* Standalone integer skip connection (Sec. 3.2.3, Eq. 7) with
  * requantisation, for a top-down add that is not fused into a conv:
  *   y[n][i][j][c] = clamp(RSM(u_, mult[c], 31 + shift[c]), 0, 2^bits_out - 1)

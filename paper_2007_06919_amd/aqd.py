@@ -83,6 +83,7 @@ def lib():
             "qconv_run_group_static": ([i, POINTER(QconvSeg), vp], st),
             "qconv_run_proj": ([vp, vp, i, i, i, i, vp, i, i, vp, vp, vp], st),
             "qconv_destroy": ([vp], None),
+            "qconv_path": ([vp], ctypes.c_char_p),
             "qadd_run": ([POINTER(QaddDesc), vp, vp, vp, POINTER(QaddParams), vp], st),
             "aqd_channel_sums": ([vp, c_int64, i, vp, vp], st),
             "aqd_maxpool_run": ([POINTER(MaxpoolDesc), vp, vp, vp], st),
@@ -111,7 +112,7 @@ def lib():
 def exported_symbols():
     return ["qconv_create", "qconv_out_shape", "qconv_scales", "qconv_run", "qconv_run_group",
             "qconv_group_workspace", "qconv_run_group_ws", "qconv_run_group_static",
-            "qconv_run_proj", "qconv_destroy",
+            "qconv_run_proj", "qconv_destroy", "qconv_path",
             "qadd_run", "aqd_maxpool_run", "aqd_channel_sums", "aqd_graph_begin", "aqd_graph_end",
             "aqd_graph_launch", "aqd_graph_destroy", "aqd_last_error", "aqd_pack_codes",
             "aqd_unpack_codes", "aqd_approx_ratio", "aqd_normalize_multiplier",
@@ -231,6 +232,11 @@ def qconv_run_proj(conv, proj, level, n, h, w, x, hp, wp, xp, y, stream=None):
 def qconv_destroy(conv):
     if conv:
         lib().qconv_destroy(conv)
+
+
+def qconv_path(conv) -> str:
+    """'fp4-mfma', 'i8-mfma' or 'direct': the arithmetic of the handle's launches."""
+    return lib().qconv_path(conv).decode()
 
 
 # ------------------------------------------------------------------- qadd

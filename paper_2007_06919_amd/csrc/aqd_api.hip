@@ -68,6 +68,25 @@ int tile_row_channel(int rho, int cpl)
     return w * slice + cpl * g + 4 * i + e;
 }
 
+// FP4 path (qconv_fp4.hip): position kappa of a 256-channel stage in LDS
+// holds channel fp4_channel(kappa). A copy lane spreads 32 packed 2-bit codes
+// (channels 32c .. 32c+31) into 16-byte column c: word 0 = the even channels
+// of the first 16, word 1 = their odd ones, words 2 and 3 the same for the
+// second 16; nibble n of a word is its n-th channel.
+int fp4_channel(int kappa)
+{
+    const int c = kappa / 32, wd = (kappa % 32) / 8, n = kappa % 8;
+    return 32 * c + 16 * (wd >> 1) + 2 * n + (wd & 1);
+}
+
+// e2m1 nibble of a small integer (|v| <= 3: 0, 1, 2, 3 -> 0x0, 0x2, 0x4, 0x5;
+// bit 3 = sign)
+uint8_t e2m1_nibble(int v)
+{
+    static const uint8_t mag[4] = {0x0, 0x2, 0x4, 0x5};
+    return (uint8_t)((v < 0 ? 0x8 : 0x0) | mag[v < 0 ? -v : v]);
+}
+
 int pick_tile(int cout, bool codes, int bits_in)
 {
     if (bits_in == 4 && cout >= 256 && (!codes || cout % 32 == 0))
@@ -218,12 +237,19 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
                       (codes ? (d.cout % 16 == 0 && d.bits_out == d.bits_in &&
                                 (d.skip_bits == 0 || d.skip_bits == d.bits_in || d.skip_bits == 32))
                              : d.cout % 4 == 0);
+    // 2-bit codes and weights in 256-channel chunks: the scaled FP4 MFMA, exact
+    // while every partial sum stays below 2^24 (K * 3 * max|w| < 2^24)
+    const char *no_fp4 = std::getenv("AQD_NO_FP4");
+    const bool fp4 = mfma && !(no_fp4 && std::strcmp(no_fp4, "1") == 0) && dc.bits_in == 2 && dc.bits_w == 2 &&
+                     d.cin % 256 == 0 && d.cout % 256 == 0 &&
+                     (codes ? (dc.bits_out == 2 && (d.skip_bits == 0 || d.skip_bits == 2)) : d.skip_bits == 0) &&
+                     K * 3 * wmax < (1LL << 24);
     qconv_s h{};
     h.d = d;
     h.qmax = codes ? (1 << dc.bits_out) - 1 : 0;
     h.mfma = mfma;
     int cpl = 0;
-    h.tile_cfg = pick_tile(d.cout, codes, d.bits_in);
+    h.tile_cfg = fp4 ? TILE_FP4 : pick_tile(d.cout, codes, d.bits_in);
     mfma_tile_shape(h.tile_cfg, &h.blk_co, &h.blk_px, &cpl);
     const int BLK_CO = h.blk_co;
     h.co_tiles = mfma ? (d.cout + BLK_CO - 1) / BLK_CO : 1;
@@ -245,7 +271,26 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
     }
 
     std::vector<uint8_t> wbuf;
-    if (mfma) {
+    if (fp4) {
+        // tiles [co_tile][128-channel K step][row rho][64 bytes]: channel
+        // tile_row_channel(rho) of the tile; nibble kappa (byte kappa / 2, low
+        // nibble first) = e2m1 of the weight of input channel
+        // fp4_channel(128 q + kappa) of the stage, q = K step % 2
+        const int k4pt = d.cin / 128, ks4 = taps * k4pt;
+        wbuf.assign((size_t)h.co_tiles * ks4 * 256 * 64, 0);
+        for (int ct = 0; ct < h.co_tiles; ++ct)
+            for (int ks = 0; ks < ks4; ++ks) {
+                const int tap = ks / k4pt, c128 = ks % k4pt;
+                const int stage0 = 256 * (c128 / 2), q = c128 % 2;
+                for (int rho = 0; rho < 256; ++rho) {
+                    const int co = ct * 256 + tile_row_channel(rho, cpl);
+                    uint8_t *dst = wbuf.data() + (((size_t)ct * ks4 + ks) * 256 + rho) * 64;
+                    const int16_t *src = wv.data() + ((size_t)co * taps + tap) * d.cin + stage0;
+                    for (int kap = 0; kap < 128; ++kap)
+                        dst[kap / 2] |= (uint8_t)(e2m1_nibble(src[fp4_channel(128 * q + kap)]) << (4 * (kap % 2)));
+                }
+            }
+    } else if (mfma) {
         // tiles [co_tile][k step][row rho][byte p]: channel tile_row_channel(rho) of the tile,
         // input channel widened_channel(p) of the K step's 64-channel chunk
         const int kpt = d.cin / KC;
@@ -350,6 +395,15 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
     }
     *out = hp;
     return AQD_OK;
+}
+
+const char *qconv_path(qconv_t conv)
+{
+    if (!conv)
+        return "invalid";
+    if (!conv->mfma)
+        return "direct";
+    return conv->tile_cfg == TILE_FP4 ? "fp4-mfma" : "i8-mfma";
 }
 
 void qconv_destroy(qconv_t conv)
@@ -635,10 +689,15 @@ void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
     long long P = 0;
     for (int i = 0; i < a.nseg; ++i)
         P += a.seg[i].P;
+    // the FP4 path: half the MFMA time per 64-channel step, parts of whole
+    // 256-channel stages (4 steps)
+    const bool fp4 = a.tile_cfg == TILE_FP4;
+    const double step_scale = fp4 ? 0.5 : 1.0;
+    const int align = fp4 ? 4 : 1;
     auto cost = [&](int parts, int chunk) {
         const double units = (double)a.total_tiles * parts;
         const double per_cu = std::ceil(units / 256.0);
-        double t = chunk * (per_cu <= 1 ? 0.65 : 0.42 * per_cu) + 3.0 * std::ceil(per_cu / 2.0);
+        double t = step_scale * chunk * (per_cu <= 1 ? 0.65 : 0.42 * per_cu) + 3.0 * std::ceil(per_cu / 2.0);
         if (parts > 1)
             t += (double)parts * P * a.cout * 8.0 / 5e6 + 5.0;
         return t;
@@ -648,8 +707,8 @@ void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
     double best = cost(1, a.ksteps);
     static const int cand[] = {2, 3, 4, 6, 8, 12, 16};
     for (int c : cand) {
-        const int chunk = (a.ksteps + c - 1) / c;
-        if (chunk < 2)
+        const int chunk = ((a.ksteps + c - 1) / c + align - 1) / align * align;
+        if (chunk < 2 || (fp4 && chunk >= a.ksteps))
             break;
         const int parts = (a.ksteps + chunk - 1) / chunk;  // every part non-empty
         const double t = cost(parts, chunk);

@@ -27,7 +27,11 @@ enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
        TILE_STREAM_H128 = 10,
        // cin a multiple of 256, code outputs: 256 x 128 tiles with the weights
        // read into registers (qconv_wv.hip), same weight layout as 256x128
-       TILE_WV = 11 };
+       TILE_WV = 11,
+       // 2-bit codes and 2-bit weights, cin and cout multiples of 256: 256 x 128
+       // tiles on the scaled FP4 MFMA (qconv_fp4.hip), weights stored as e2m1
+       // nibbles at create (FP4_KROW bytes per row and 128-channel K step)
+       TILE_FP4 = 12 };
 constexpr int KC = 64;
 
 // tile shape of a configuration, and the channels one lane holds per pixel
@@ -87,6 +91,9 @@ constexpr int PROJ_BLK_PX = 64;
 hipError_t launch_qconv_proj(const MfmaArgs &a, hipStream_t stream);
 // TILE_WV launches (qconv_wv.hip)
 hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream);
+// TILE_FP4 launches (qconv_fp4.hip); a.ksteps and a.kchunk in 64-channel steps,
+// multiples of 4
+hipError_t launch_qconv_fp4(const MfmaArgs &a, hipStream_t stream);
 
 // ---- split-K combine + epilogue (qconv_splitk.hip) ---------------------------
 struct SplitSeg {

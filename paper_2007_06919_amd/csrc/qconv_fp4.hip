@@ -1,0 +1,471 @@
+// Implicit-GEMM integer convolution of 2-bit codes with 2-bit weights on the
+// gfx950 scaled FP4 MFMA (v_mfma_scale_f32_16x16x128_f8f6f4, e2m1 operands),
+// for layers with 256-channel input chunks (cin and cout multiples of 256):
+// the ResNet-50 res4/res5 layers, the FPN and the heads of the paper's 2-bit
+// detectors. GEMM view of Eq. 4 (Sec. 3.2.1): rows = output channels,
+// columns = output pixels, K = taps x input channels.
+//
+// Exactness. Every operand is a small integer that e2m1 holds exactly: a
+// 2-bit weight value (odd grid -3, -1, 1, 3 or two's complement -2 .. 1) is
+// stored as its e2m1 nibble with block scale 1, an activation code k in
+// {0, 1, 2, 3} as the nibble k itself, which e2m1 reads as k / 2, with block
+// scale 2. Each product is then an integer, the MFMA sums them in fp32, and
+// every partial sum is bounded by K * 3 * 3 < 2^24 (checked at create), so
+// the fp32 accumulator holds the exact integer sum; its conversion to int32
+// is exact too. The epilogue is the integer one of Eq. 6-8 and Eq. 2.
+//
+// Workgroup tile 256 channels x 128 pixels, 4 waves; wave w owns channel rows
+// 64w .. 64w+63 (4 accumulator tiles of 16) for all 128 pixels (8 column
+// tiles), as in the register-fed int8 kernel:
+//  * weights (e2m1 nibbles, tiled at create; one K step = 128 input channels
+//    of one tap, 64 bytes per row) go from global memory straight into
+//    registers, three K steps ahead of their MFMAs;
+//  * activation codes go through LDS in stages of one tap's 256 channels
+//    (two K steps): each lane copies 8 bytes of packed 2-bit codes per piece
+//    and spreads them into 16 bytes of nibbles with two masks and a shift
+//    (even channels of a word in one word of nibbles, odd ones in the next;
+//    the weights were stored in that channel order at create). A pixel's 128
+//    bytes of nibbles are 16-byte columns XOR-swizzled with the pixel index,
+//    so that the copies' writes and the fragment reads (16 bytes per lane)
+//    are free of bank conflicts. A stage is loaded one stage ahead of its
+//    use and written during the stage before it (two-buffer ring, one
+//    barrier per stage).
+//  * A part of a split K range (whole stages) writes int32 partial sums, the
+//    first part with the bias, for the split-K combining epilogue.
+
+#include "epilogue.h"
+#include "internal.h"
+#include "mfma_common.h"
+
+namespace aqd {
+namespace {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+
+constexpr int F4_BCO = 256;                   // channels per workgroup tile
+constexpr int F4_BPX = 128;                   // pixels per workgroup tile
+constexpr int F4_ROW = 128;                   // LDS bytes of one stage per pixel (256 nibbles)
+constexpr int F4_STAGE = F4_BPX * F4_ROW;     // 16 KiB
+constexpr int F4_TAB = 2 * F4_STAGE;          // epilogue tables after the ring of two stages
+constexpr int F4_LDS = 4 * F4_STAGE;          // int32 staging uses all 64 KiB
+constexpr int F4_KROW = 64;                   // weight bytes per row and K step (128 nibbles)
+constexpr int F4_SCALE_W = 127;               // E8M0 block scales: 2^0 for the weights,
+constexpr int F4_SCALE_X = 128;               // 2^1 for the codes (nibble k reads as k / 2)
+
+// c += a * b on the scaled FP4 MFMA (formats 4 = e2m1 for both operands, block
+// scales sa, sb as E8M0 exponents), accumulating in place. Inline assembly
+// because the compiler's form of this instruction never writes its
+// accumulator in place, and 128 accumulator registers rotating through fresh
+// ones do not fit. The compiler therefore does not see an MFMA here: the
+// wait states it would insert around one are the caller's (a VALU write of an
+// operand needs 2 before the MFMA reads it, a read of the result 18 after),
+// and a hazard scan of the built code is part of the tests.
+__device__ __forceinline__ void mfma_fp4(const v4i a, const v4i b, v4f &c, int sa, int sb)
+{
+    asm volatile("v_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:4 blgp:4"
+                 : "+v"(c) : "v"(a), "v"(b), "v"(sa), "v"(sb));
+}
+
+// Wait states around the inline MFMAs, and a fence the compiler cannot move
+// the accumulators' other uses across: every accumulator is an operand
+template <int MI, int NJ>
+__device__ __forceinline__ void mfma_fence(v4f (&acc)[MI][NJ])
+{
+    static_assert(MI * NJ == 32, "two groups of 16 operands");
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"
+                 : "+v"(acc[0][0]), "+v"(acc[0][1]), "+v"(acc[0][2]), "+v"(acc[0][3]),
+                   "+v"(acc[0][4]), "+v"(acc[0][5]), "+v"(acc[0][6]), "+v"(acc[0][7]),
+                   "+v"(acc[1][0]), "+v"(acc[1][1]), "+v"(acc[1][2]), "+v"(acc[1][3]),
+                   "+v"(acc[1][4]), "+v"(acc[1][5]), "+v"(acc[1][6]), "+v"(acc[1][7]));
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"
+                 : "+v"(acc[2][0]), "+v"(acc[2][1]), "+v"(acc[2][2]), "+v"(acc[2][3]),
+                   "+v"(acc[2][4]), "+v"(acc[2][5]), "+v"(acc[2][6]), "+v"(acc[2][7]),
+                   "+v"(acc[3][0]), "+v"(acc[3][1]), "+v"(acc[3][2]), "+v"(acc[3][3]),
+                   "+v"(acc[3][4]), "+v"(acc[3][5]), "+v"(acc[3][6]), "+v"(acc[3][7]));
+}
+
+// OUTK: 0 = 2-bit codes, 1 = int32 (v = acc + bias, or a split part's sums);
+// SKK: 0 = no skip, 1 = 2-bit code skip; FAST: every shift >= 2 (32-bit requantisation)
+template <int OUTK, int SKK, int FAST>
+__global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
+{
+    static_assert(OUTK == 0 || SKK == 0, "int32 outputs have no skip");
+    constexpr int MI = 4, NJ = 8, QMAX = 3, BO = 2;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[F4_LDS];
+
+    const int bid = blockIdx.x;
+    const int logical = (bid & 7) * A.tiles_per_xcd + (bid >> 3);
+    if (logical >= A.total_tiles)
+        return;
+    // work unit -> output tile and part of its K range (consecutive units)
+    const int tile = logical / A.ksplit;
+    const int kpart = logical - tile * A.ksplit;
+    int s = 0;
+#pragma unroll
+    for (int i = 1; i < AQD_MAX_SEGS; ++i)
+        if (i < A.nseg && tile >= A.seg[i].tile_begin)
+            s = i;
+    const MfmaSeg &S = A.seg[s];
+    const int t_in_seg = tile - S.tile_begin;
+    const int co_tile = t_in_seg % A.co_tiles;
+    const int px_tile = t_in_seg / A.co_tiles;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r = lane & 15, g = lane >> 4;
+
+    // K range of this part in stages (one tap's 256 channels; A.ksteps and
+    // A.kchunk count 64-channel steps, multiples of 4 on this path)
+    const int row_bytes = A.cin / 4;
+    const int spt = A.cin / 256;                           // stages per tap
+    const int st0 = kpart * (A.kchunk / 4);
+    const int NST = min(A.kchunk, A.ksteps - kpart * A.kchunk) / 4;  // >= 1 (host)
+    const int KS4 = A.ksteps / 2;                          // 128-channel K steps of the whole range
+    const int hw = S.ho * S.wo;
+
+    // ---- activation copies: piece m of a stage = pixels 32m .. 32m+31, lane
+    // tid copying packed bytes 8c .. 8c+7 (channels 32c .. 32c+31) of pixel
+    // 32m + tid / 8, c = tid % 8
+    const int c8 = tid & 7;
+    int ih0[4], iw0[4], xpix[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        const unsigned p = (unsigned)(px_tile * F4_BPX + 32 * m + (tid >> 3));
+        const bool ok = p < (unsigned)S.P;
+        const unsigned pn = ok ? p / (unsigned)hw : 0u;
+        const unsigned prem = ok ? p - pn * (unsigned)hw : 0u;
+        const unsigned oh = prem / (unsigned)S.wo, ow = prem - oh * (unsigned)S.wo;
+        ih0[m] = ok ? (int)oh * A.stride - A.pad : -(1 << 30);
+        iw0[m] = (int)ow * A.stride - A.pad;
+        xpix[m] = (int)pn * S.h * S.w;   // n * h * w < 2^31, checked on the host
+    }
+    const uint8_t *xsrc = S.x + 8 * c8;
+    // LDS: 16-byte column c of pixel p at 128 p + 16 (c ^ (p & 7))
+    const int wp = tid >> 3;
+    const uint32_t wofs = F4_ROW * wp + 16 * (c8 ^ (wp & 7));
+    // fragment of K step q of a stage: pixel 16j + r, column 4q + g
+    auto ro = [&](int q) -> uint32_t { return F4_ROW * r + 16 * ((4 * q + g) ^ (r & 7)); };
+
+    // copy state of the stage being loaded: tap (tr, tq), 256-channel chunk th
+    int th = st0 % spt, tr, tq;
+    {
+        const int tap = st0 / spt;
+        tr = tap / A.kw;
+        tq = tap - tr * A.kw;
+    }
+    auto advance = [&]() {
+        if (++th == spt) {
+            th = 0;
+            if (++tq == A.kw) {
+                tq = 0;
+                ++tr;
+            }
+        }
+    };
+    // taps in the padding, pixels past the end and stages past the last read a
+    // clamped position inside the image and are masked to code 0
+    auto load_piece = [&](int m) -> uint2 {
+        const int ih = ih0[m] + tr, iw = iw0[m] + tq;
+        const bool in = ((unsigned)ih < (unsigned)S.h) & ((unsigned)iw < (unsigned)S.w);
+        const int ihc = min(max(ih, 0), S.h - 1), iwc = min(max(iw, 0), S.w - 1);
+        const uint2 v = *(const uint2 *)(xsrc + (long long)(xpix[m] + ihc * S.w + iwc) * row_bytes + 64 * th);
+        const uint32_t keep = in ? 0xFFFFFFFFu : 0u;
+        return make_uint2(v.x & keep, v.y & keep);
+    };
+    // 32 packed codes -> 32 nibbles: word 2h holds the even channels of packed
+    // word h, word 2h + 1 the odd ones
+    auto write_piece = [&](int buf, int m, const uint2 v) {
+        const uint4 n = make_uint4(v.x & 0x33333333u, (v.x >> 2) & 0x33333333u,
+                                   v.y & 0x33333333u, (v.y >> 2) & 0x33333333u);
+        *(uint4 *)(lds + buf * F4_STAGE + m * (32 * F4_ROW) + wofs) = n;
+    };
+
+    // ---- weights: this wave's rows of K step k (128 channels), accumulator
+    // tile i at wa + k * 16 KiB + i * 1 KiB (lane: row r, 16-byte column g);
+    // the look-ahead reads up to three steps past the part's last (inside the
+    // tile range or the allocation's four steps of padding), never used
+    const int8_t *wa = S.wt + ((long long)co_tile * KS4 * F4_BCO + 64 * wave + r) * F4_KROW + 16 * g;
+    const int k0 = 2 * st0;
+    auto load_a = [&](int k, v4i *dst) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+            dst[i] = *(const v4i *)(wa + (long long)(k0 + k) * (F4_BCO * F4_KROW) + i * 1024);
+    };
+
+    // lane group g of wave w holds channels 128 (w >> 1) + 32 g + 16 (w & 1) + 4 i + e
+    const int co_loc = 128 * (wave >> 1) + 32 * g + 16 * (wave & 1);
+    const int co_glob = co_tile * F4_BCO + co_loc;
+    v4f acc[MI][NJ];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+            acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+    mfma_fence(acc);  // the zeros are written before the first MFMA reads them
+    // block scales in registers the compiler cannot rematerialise next to an MFMA
+    int scale_w = F4_SCALE_W, scale_x = F4_SCALE_X;
+    asm volatile("" : "+v"(scale_w), "+v"(scale_x));
+
+    // ---- the channel tile's epilogue table (and the side-0 skip table) go to
+    // LDS past the ring before the prologue: nothing holds them in registers
+    // through the main loop
+    int32_t *prm = (int32_t *)(lds + F4_TAB);      // [EPI_FIELDS][256]
+    int32_t *lut = prm + EPI_FIELDS * F4_BCO;      // [256][4]: RSM(k, c, d) of the side-0 skip codes
+    const bool use_lut = SKK == 1 && S.side0;
+    if constexpr (OUTK == 0) {
+#pragma unroll
+        for (int u = 0; u < EPI_FIELDS; ++u)
+            prm[tid + 256 * u] = S.epi[u * A.cout_pad + co_tile * F4_BCO + tid];
+        if (use_lut) {
+#pragma unroll
+            for (int u = 0; u < QMAX + 1; ++u)
+                lut[tid + 256 * u] = S.lut[co_tile * F4_BCO * (QMAX + 1) + tid + 256 * u];
+        }
+    }
+    static_assert(F4_TAB + (EPI_FIELDS + QMAX + 1) * F4_BCO * 4 <= F4_LDS, "tables fit past the ring");
+
+    // ---- prologue: stage 0 in LDS, stage 1 in registers, weights of steps 0-2
+    uint2 rb[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+        write_piece(0, m, load_piece(m));
+    advance();
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+        rb[m] = load_piece(m);
+    advance();  // copy state: stage 2
+    v4i fa[4][MI];
+    load_a(0, fa[0]);
+    load_a(1, fa[1]);
+    load_a(2, fa[2]);
+    v4i fb[NJ];
+    int kstep = 0;         // K step (128 channels) of this part being multiplied
+    constexpr int RA = 3;  // fragments are read RA column tiles ahead of their MFMAs
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+#pragma unroll
+    for (int j = 0; j < RA; ++j)
+        fb[j] = *(const v4i *)(lds + 2048 * j + ro(0));
+
+    // ---- main loop, one stage (two K steps) per call: stage t lives in buffer
+    // t % 2 (the parity P, a compile-time constant, so that the weight sets
+    // (K step % 4) are registers). During stage t the pieces of stage t + 1
+    // (loaded during stage t - 1) are written into buffer (t + 1) % 2, two per
+    // K step, each right before the load of the same piece of stage t + 2
+    // reuses its registers. The barrier in the last K step, before the first
+    // read of stage t + 1, makes that stage visible; every read of stage t - 1
+    // (the buffer's previous contents) came before the barrier of stage t - 1.
+    auto stage = [&](auto pc) {
+        constexpr int P = decltype(pc)::value;
+        static_for<2>([&](auto qc) {
+            constexpr int q = decltype(qc)::value;
+            constexpr int kq = 2 * P + q;  // K step % 4
+            write_piece(P ^ 1, 2 * q, rb[2 * q]);
+            write_piece(P ^ 1, 2 * q + 1, rb[2 * q + 1]);
+            rb[2 * q] = load_piece(2 * q);
+            rb[2 * q + 1] = load_piece(2 * q + 1);
+            load_a(kstep + 3, fa[(kq + 3) & 3]);
+            const uint32_t r_this = ro(q) + P * F4_STAGE;
+            const uint32_t r_next = q == 0 ? ro(1) + P * F4_STAGE : ro(0) + (P ^ 1) * F4_STAGE;
+            static_for<NJ>([&](auto jc) {
+                constexpr int j = decltype(jc)::value;
+                if constexpr (q == 1 && j == NJ - RA)
+                    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+                    mfma_fp4(fa[kq][i], fb[j], acc[i][j], scale_w, scale_x);
+                if constexpr (j + RA < NJ)
+                    fb[j + RA] = *(const v4i *)(lds + 2048 * (j + RA) + r_this);
+                else
+                    fb[j + RA - NJ] = *(const v4i *)(lds + 2048 * (j + RA - NJ) + r_next);
+            });
+            ++kstep;
+            if constexpr (q == 1)
+                advance();
+        });
+    };
+    // pairs of stages (even, odd parity); the odd stage of the last pair may
+    // be past the end
+    for (int t = 0; t < NST; t += 2) {
+        stage(std::integral_constant<int, 0>{});
+        if (t + 1 < NST)
+            stage(std::integral_constant<int, 1>{});
+    }
+
+    mfma_fence(acc);  // the last MFMAs have written the accumulators
+    // exact integer sums (see the header), converted where they are used;
+    // the bias of Eq. 6 joins there
+    if constexpr (OUTK == 1) {
+        // int32 outputs (or part sums at y + kpart * P * cout), in two passes
+        // of 64 pixels through LDS rows of 256 int32 (16-byte chunk c of pixel
+        // p at c ^ (p & 7)); every thread then stores 16-byte chunks of whole rows
+        int32_t *ybase = (int32_t *)S.y + (long long)kpart * S.P * A.cout;
+        const bool with_bias = !(A.part && kpart > 0);
+        v4i bias[MI];
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+            bias[i] = with_bias ? *(const v4i *)(S.epi + EPI_BIAS * A.cout_pad + co_glob + 4 * i)
+                                : v4i{0, 0, 0, 0};
+        static_for<2>([&](auto pc) {
+            constexpr int pass = decltype(pc)::value;
+            __syncthreads();  // the ring, or the last pass's rows, are no longer read
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int p = 16 * jj + r;
+#pragma unroll
+                for (int i = 0; i < MI; ++i) {
+                    const int c = co_loc / 4 + i;
+                    const v4f a = acc[i][4 * pass + jj];
+                    *(v4i *)(lds + p * 1024 + 16 * (c ^ (p & 7))) =
+                        v4i{(int)a.x, (int)a.y, (int)a.z, (int)a.w} + bias[i];
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int it = 0; it < 16; ++it) {
+                const int idx = it * 256 + tid;
+                const int p = idx >> 6, c = idx & 63;
+                const long long px = (long long)px_tile * F4_BPX + 64 * pass + p;
+                if (px < S.P)
+                    *(v4i *)(ybase + px * A.cout + co_tile * F4_BCO + 4 * c) =
+                        *(const v4i *)(lds + p * 1024 + 16 * (c ^ (p & 7)));
+            }
+        });
+        return;
+    }
+
+    // ---------------------------------------------------------------- epilogue
+    const long long px0 = (long long)px_tile * F4_BPX + r;
+    bool okj[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+        okj[j] = px0 + 16 * j < S.P;
+    // a lane's 16 channels of a pixel: one word of 2-bit codes
+    uint32_t skw[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        skw[j] = 0;
+        if constexpr (SKK == 1) {
+            if (okj[j]) {
+                const long long px = px0 + 16 * j;
+                long long spix = px;
+                if (A.up2) {
+                    const int n_ = (int)(px / hw);
+                    const int rem = (int)(px - (long long)n_ * hw);
+                    const int oh = rem / S.wo, ow = rem - oh * S.wo;
+                    spix = ((long long)n_ * S.hs + (oh >> 1)) * S.ws + (ow >> 1);
+                }
+                skw[j] = *(const uint32_t *)((const uint8_t *)S.skip + spix * (A.cout / 4) + co_glob / 4);
+            }
+        }
+    }
+    const int32_t *lut_l = lut + co_loc * (QMAX + 1);  // this lane's 16 channels
+    uint32_t outw[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+        outw[j] = 0;
+    auto group = [&](auto lut_c, auto ic) {
+        constexpr bool LUT = decltype(lut_c)::value;
+        constexpr int i = decltype(ic)::value;
+        const int cl = co_loc + 4 * i;
+        const int4 m4 = *(const int4 *)(prm + EPI_MULT * F4_BCO + cl);
+        const int4 s4 = *(const int4 *)(prm + (FAST ? EPI_SHR : EPI_SHIFT) * F4_BCO + cl);
+        const int4 b4 = *(const int4 *)(prm + EPI_BIAS * F4_BCO + cl);
+        const int mult[4] = {m4.x, m4.y, m4.z, m4.w};
+        const int shf[4] = {s4.x, s4.y, s4.z, s4.w};
+        const int bias[4] = {b4.x, b4.y, b4.z, b4.w};
+        long long rnd[4] = {0, 0, 0, 0};
+        if constexpr (FAST) {
+            const int4 r4 = *(const int4 *)(prm + EPI_RND * F4_BCO + cl);
+            rnd[0] = (long long)r4.x << 32; rnd[1] = (long long)r4.y << 32;
+            rnd[2] = (long long)r4.z << 32; rnd[3] = (long long)r4.w << 32;
+        }
+        int sc[4] = {0, 0, 0, 0}, sd[4] = {0, 0, 0, 0}, sside[4] = {0, 0, 0, 0};
+        if constexpr (SKK != 0 && !LUT) {
+            const int4 c4 = *(const int4 *)(prm + EPI_SKIP_C * F4_BCO + cl);
+            const int4 d4 = *(const int4 *)(prm + EPI_SKIP_D * F4_BCO + cl);
+            const int4 e4 = *(const int4 *)(prm + EPI_SKIP_SIDE * F4_BCO + cl);
+            sc[0] = c4.x; sc[1] = c4.y; sc[2] = c4.z; sc[3] = c4.w;
+            sd[0] = d4.x; sd[1] = d4.y; sd[2] = d4.z; sd[3] = d4.w;
+            sside[0] = e4.x; sside[1] = e4.y; sside[2] = e4.z; sside[3] = e4.w;
+        }
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int v = (int)acc[i][j][e] + bias[e];
+                const int bit = (4 * i + e) * BO;
+                int kv = 0;
+                if constexpr (SKK == 1)
+                    kv = (int)__builtin_amdgcn_ubfe(skw[j], bit, BO);
+                int y;
+                if constexpr (FAST) {
+                    int u = v;
+                    if constexpr (LUT) {
+                        u = (int)((unsigned)v + (unsigned)lut_l[(4 * i + e) * (QMAX + 1) + kv]);
+                    } else if constexpr (SKK != 0) {
+                        const int scaled = rsm32(sside[e] ? v : kv, sc[e], sd[e]);
+                        u = (int)((unsigned)scaled + (unsigned)(sside[e] ? kv : v));
+                    }
+                    y = requant32(u, mult[e], rnd[e], shf[e]);
+                    y = y < 0 ? 0 : (y > QMAX ? QMAX : y);
+                } else {
+                    long long u = v;
+                    if constexpr (LUT)
+                        u = (int)((unsigned)v + (unsigned)lut_l[(4 * i + e) * (QMAX + 1) + kv]);
+                    else if constexpr (SKK != 0)
+                        u = align_add(v, kv, sc[e], sd[e], sside[e]);
+                    y = (int)requant_clamp(u, mult[e], shf[e], QMAX);
+                    asm volatile("" : "+v"(y));  // one 64-bit product alive at a time
+                }
+                outw[j] |= (uint32_t)y << bit;
+            }
+        }
+    };
+    auto body = [&](auto lut_c) { static_for<MI>([&](auto ic) { group(lut_c, ic); }); };
+    if (use_lut)
+        body(std::true_type{});
+    else
+        body(std::false_type{});
+    // the packed words are complete here: the compiler would otherwise sink
+    // their last steps into the conditional stores and keep every 64-bit
+    // product alive until then
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+        asm volatile("" : "+v"(outw[j]));
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+        if (okj[j])
+            *(uint32_t *)((uint8_t *)S.y + (px0 + 16 * j) * (A.cout / 4) + co_glob / 4) = outw[j];
+}
+
+}  // namespace
+
+hipError_t launch_qconv_fp4(const MfmaArgs &a, hipStream_t stream)
+{
+    if ((a.bits_out != 2 && a.bits_out != 32) || (a.skip_bits != 0 && (a.skip_bits != 2 || a.bits_out == 32)) ||
+        a.cin % 256 != 0 || a.cout % 256 != 0 || a.co_tiles * F4_BCO != a.cout || a.ksteps % 4 != 0 ||
+        a.kchunk % 4 != 0 || a.kchunk < 4 || (a.part == 0 && a.ksplit != 1) || (a.part && a.bits_out != 32))
+        return hipErrorInvalidValue;
+    dim3 grid(8 * a.tiles_per_xcd), block(256);
+    bool fast = true;
+    for (int i = 0; i < a.nseg; ++i)
+        fast = fast && a.seg[i].fast;
+    if (a.bits_out == 32)
+        hipLaunchKernelGGL((qconv_fp4_kernel<1, 0, 1>), grid, block, 0, stream, a);
+    else if (a.skip_bits == 0) {
+        if (fast)
+            hipLaunchKernelGGL((qconv_fp4_kernel<0, 0, 1>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_fp4_kernel<0, 0, 0>), grid, block, 0, stream, a);
+    } else {
+        if (fast)
+            hipLaunchKernelGGL((qconv_fp4_kernel<0, 1, 1>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_fp4_kernel<0, 1, 0>), grid, block, 0, stream, a);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace aqd

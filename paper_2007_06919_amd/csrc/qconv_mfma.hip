@@ -586,6 +586,7 @@ __global__ void __launch_bounds__(64 * WC * WP, (Cfg<BI, MI, NJ, WC, WP, OCC>::W
                         else if constexpr (SKK != 0)
                             u = align_add(v, kv[e], sc[e], sd[e], sside[e]);
                         y = (int)requant_clamp(u, mult[e], shf[e], QMAX);
+                        asm volatile("" : "+v"(y));  // one 64-bit product alive at a time
                     }
                     const int bit = (4 * i + e) * BI;
                     outw[j][bit >> 5] |= (uint32_t)y << (bit & 31);
@@ -1022,6 +1023,7 @@ __global__ void __launch_bounds__(256, 2) qconv_stream_kernel(MfmaArgs A)
                             else if constexpr (SKK != 0)
                                 u = align_add(v, kv, sc[e], sd[e], sside[e]);
                             y = (int)requant_clamp(u, mult[e], shf[e], QMAX);
+                            asm volatile("" : "+v"(y));  // one 64-bit product alive at a time
                         }
                         outw[j][bit >> 5] |= (uint32_t)y << (bit & 31);
                     }
@@ -1097,6 +1099,7 @@ void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane)
     switch (tile_cfg) {
     case TILE_256x128: *blk_co = 256; *blk_px = 128; *chan_per_lane = 32; return;
     case TILE_WV: *blk_co = 256; *blk_px = 128; *chan_per_lane = 16; return;
+    case TILE_FP4: *blk_co = 256; *blk_px = 128; *chan_per_lane = 32; return;
     case TILE_256x64S:
     case TILE_256x64:
     case TILE_STREAM: *blk_co = 256; *blk_px = 64; *chan_per_lane = 32; return;
@@ -1236,6 +1239,8 @@ hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
         case TILE_128x256: return launch_modes<4, 4, 8, 2, 2>(a, stream);
         case TILE_64x512: return launch_modes<4, 4, 8, 1, 4>(a, stream);
         }
+    } else if (bits_in == 2 && a.tile_cfg == TILE_FP4) {
+        return launch_qconv_fp4(a, stream);
     } else if (bits_in == 2) {
         switch (a.tile_cfg) {
         case TILE_128x256: return launch_modes<2, 4, 8, 2, 2>(a, stream);

@@ -395,6 +395,7 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
                     else if constexpr (SKK != 0)
                         u = align_add(v, kv, sc[e], sd[e], sside[e]);
                     y = (int)requant_clamp(u, mult[e], shf[e], QMAX);
+                    asm volatile("" : "+v"(y));  // one 64-bit product alive at a time
                 }
                 outw[j][bit >> 5] |= (uint32_t)y << (bit & 31);
             }
