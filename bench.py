@@ -107,6 +107,9 @@ def launch_cost(gpu, group):
     macs, nbytes, seen = 0, 0, set()
     for conv, si in group:
         x, skip, y = conv.segs[si]
+        if conv.op != "conv":
+            nbytes += tbytes(x) + tbytes(y)
+            continue
         ty = net.tensors[y]
         macs += ty.n * ty.h * ty.w * conv.cout * conv.k * conv.k * conv.cin
         nbytes += tbytes(x) + tbytes(y)
@@ -212,6 +215,10 @@ def main():
     ap.add_argument("--bits", type=int, default=4, choices=(3, 4),
                     help="code width of the network (3: the paper's 3-bit RetinaNet, codes in "
                          "4-bit containers; the default 4 is the benchmarked workload)")
+    ap.add_argument("--io-bits", type=int, default=0, choices=(0, 8),
+                    help="8: the fully quantized network of the paper's AQD rows (Sec. 4): 8-bit image, "
+                         "7x7 stem and prediction convolutions, max-pooling; 0: the network from the "
+                         "max-pooled stem output on, predictions at the network's width")
     ap.add_argument("--fp4-layer", action="store_true",
                     help="instead of the network: the 2-bit head-tower launch (3x3 256->256, class "
                          "and box towers, P3-P7, batch 8, 800x1333) on the FP4 MFMA path and on the "
@@ -237,7 +244,10 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     t0 = time.time()
-    if args.bits == 4:
+    if args.io_bits:
+        net, params = workloads.retinanet_config(8, 800, 1333, args.bits, io_bits=args.io_bits)
+        workload = f"retinanet_r50_fpn_n8_800x1333_{args.bits}bit_io{args.io_bits}"
+    elif args.bits == 4:
         net, params = workloads.config(4)
         workload = workloads.CONFIG_NAMES[4]
     else:
@@ -260,7 +270,8 @@ def main():
                 and gpu.schedule[gi][0][0].cin == 256 and gpu.schedule[gi][0][0].cout == 256
                 and gpu.schedule[gi][0][0].name.startswith(("cls.t", "box.t"))]
     from paper_2007_06919_amd import aqd
-    path = {gi: aqd.qconv_path(gpu.handles[gpu.schedule[gi][0][0].name]) for gi in live}
+    path = {gi: aqd.qconv_path(gpu.handles[gpu.schedule[gi][0][0].name])
+            if gpu.schedule[gi][0][0].op == "conv" else gpu.schedule[gi][0][0].op for gi in live}
     peak = {gi: MFMA_FP4_PEAK_TOPS if path[gi] == "fp4-mfma" else MFMA_I8_PEAK_TOPS for gi in live}
     events = {}
 

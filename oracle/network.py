@@ -2,7 +2,7 @@
 
 TEST INFRASTRUCTURE (see ``oracle/ref.py``). Takes a network description
 (tensors with shapes and bitwidths, convolutions with their (x, skip, y)
-segments) and its seeded parameters as plain objects, derives each layer's
+segments, max-pooling layers) and its seeded parameters as plain objects, derives each layer's
 integer epilogue with the oracle's own host derivation, and evaluates the
 layers in order with the oracle convolution. Images of a batch are
 independent, so ``images`` may select a subset of the batch; the calibration
@@ -75,6 +75,12 @@ def run(net, params, images=None, keep=None):
     tables = {}
     alpha_t = {}
     for i, conv in enumerate(net.convs):
+        if conv.op == "maxpool":
+            # codes pooled as they are, the scale unchanged (Sec. 3.2.4)
+            x, _, y = conv.segs[0]
+            vals[y] = ref.maxpool(vals[x], conv.k, conv.stride, conv.pad)
+            tables[conv.name] = []
+            continue
         segs = []
         for si, seg in enumerate(conv.segs):
             x, skip, y = seg

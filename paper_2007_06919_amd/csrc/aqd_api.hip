@@ -48,9 +48,12 @@ bool overlap(const void *a, size_t na, const void *b, size_t nb)
 }
 
 // Positions of the 64 channels of one K step after the kernel's widening of
-// packed codes (see qconv_mfma.hip): LDS byte p holds channel sigma(p).
+// packed codes (see qconv_mfma.hip): LDS byte p holds channel sigma(p);
+// 8-bit codes are staged in channel order.
 int widened_channel(int bits_in, int p)
 {
+    if (bits_in == 8)
+        return p;
     if (bits_in == 4)
         return 8 * (p / 8) + 2 * (p % 4) + ((p / 4) % 2);
     return 16 * (p / 16) + 4 * (p % 4) + ((p / 4) % 4);  // bits_in == 2
@@ -233,10 +236,22 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
     // steps, output and skip codes of the input's width; the direct kernel
     // takes everything else
     const bool w_fits_i8 = dc.bits_w <= 4 || d.wenc == AQD_WENC_TWOS;
-    const bool mfma = (d.bits_in == 2 || d.bits_in == 4) && d.cin % KC == 0 && w_fits_i8 &&
-                      (codes ? (d.cout % 16 == 0 && d.bits_out == d.bits_in &&
-                                (d.skip_bits == 0 || d.skip_bits == d.bits_in || d.skip_bits == 32))
-                             : d.cout % 4 == 0);
+    // 8-bit codes with int32 outputs (the prediction convolutions of the
+    // fully quantized networks): the int8 MFMA on codes re-centred by -128
+    const bool b8 = dc.bits_in == 8 && !codes && d.skip_bits == 0 && d.cin % 128 == 0 && w_fits_i8 &&
+                    d.cout % 4 == 0;
+    // 4-bit codes in, 8-bit codes out (the last tower layer before 8-bit
+    // prediction convolutions): the register-fed kernel's 8-bit epilogue
+    const bool wv8 = d.bits_in == 4 && codes && dc.bits_out == 8 && d.skip_bits == 0 && d.cin % 256 == 0 &&
+                     d.cout >= 256 && d.cout % 32 == 0 && w_fits_i8;
+    // the ResNet stem (7x7, stride 2, pad 3) on a 3-channel 8-bit image
+    const bool stem = dc.bits_in == 8 && d.cin == 3 && d.kh == 7 && d.kw == 7 && d.stride == 2 &&
+                      d.pad == 3 && d.skip_bits == 0 && (!codes || dc.bits_out == 4) && d.cout % 64 == 0 &&
+                      w_fits_i8;
+    const bool mfma = b8 || wv8 || stem || ((d.bits_in == 2 || d.bits_in == 4) && d.cin % KC == 0 && w_fits_i8 &&
+                             (codes ? (d.cout % 16 == 0 && d.bits_out == d.bits_in &&
+                                       (d.skip_bits == 0 || d.skip_bits == d.bits_in || d.skip_bits == 32))
+                                    : d.cout % 4 == 0));
     // 2-bit codes and weights in 256-channel chunks: the scaled FP4 MFMA, exact
     // while every partial sum stays below 2^24 (K * 3 * max|w| < 2^24)
     const char *no_fp4 = std::getenv("AQD_NO_FP4");
@@ -249,12 +264,12 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
     h.qmax = codes ? (1 << dc.bits_out) - 1 : 0;
     h.mfma = mfma;
     int cpl = 0;
-    h.tile_cfg = fp4 ? TILE_FP4 : pick_tile(d.cout, codes, d.bits_in);
+    h.tile_cfg = fp4 ? TILE_FP4 : b8 ? TILE_B8 : stem ? TILE_STEM : pick_tile(d.cout, codes, d.bits_in);
     mfma_tile_shape(h.tile_cfg, &h.blk_co, &h.blk_px, &cpl);
     const int BLK_CO = h.blk_co;
     h.co_tiles = mfma ? (d.cout + BLK_CO - 1) / BLK_CO : 1;
     h.cout_pad = mfma ? h.co_tiles * BLK_CO : d.cout;
-    h.ksteps = mfma ? taps * (d.cin / KC) : 0;
+    h.ksteps = stem ? 3 : mfma ? taps * (d.cin / KC) : 0;
     h.fast.assign(d.num_levels, 0);
     h.side0.assign(d.num_levels, 0);
     for (int l = 0; l < d.num_levels && d.skip_bits; ++l) {  // (stored widths from here on)
@@ -271,7 +286,24 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
     }
 
     std::vector<uint8_t> wbuf;
-    if (fp4) {
+    if (stem) {
+        // [co_tile][K step][row rho][64 B]: K byte k = window row k / 24, tap
+        // (k % 24) / 3, channel k % 3 for k % 24 < 21, else zero; channel
+        // tile_row_channel(rho) of the 64-channel tile
+        wbuf.assign((size_t)h.co_tiles * 3 * 64 * KC, 0);
+        for (int ct = 0; ct < h.co_tiles; ++ct)
+            for (int rho = 0; rho < 64; ++rho) {
+                const int co = ct * 64 + tile_row_channel(rho, cpl);
+                for (int k = 0; k < 168; ++k) {
+                    const int kh = k / 24, rem = k % 24;
+                    if (rem >= 21)
+                        continue;
+                    const int kw = rem / 3, c = rem % 3;
+                    wbuf[(((size_t)ct * 3 + k / KC) * 64 + rho) * KC + k % KC] =
+                        (uint8_t)(int8_t)wv[((size_t)co * taps + kh * 7 + kw) * d.cin + c];
+                }
+            }
+    } else if (fp4) {
         // tiles [co_tile][128-channel K step][row rho][64 bytes]: channel
         // tile_row_channel(rho) of the tile; nibble kappa (byte kappa / 2, low
         // nibble first) = e2m1 of the weight of input channel
@@ -312,12 +344,25 @@ aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
         wbuf.resize(wv.size() * sizeof(int16_t));
         std::memcpy(wbuf.data(), wv.data(), wbuf.size());
     }
+    // 8-bit codes on the MFMA enter as a - 128: the bias carries 128 * sum(w)
+    // of the channel (every tap, padding included, enters as 0 - 128)
+    std::vector<long long> recentre(d.cout, 0);
+    if (b8 || stem)
+        for (int co = 0; co < d.cout; ++co) {
+            long long sw = 0;
+            for (size_t k = 0; k < (size_t)taps * d.cin; ++k)
+                sw += wv[(size_t)co * taps * d.cin + k];
+            recentre[co] = 128 * sw;
+        }
     std::vector<int32_t> epi((size_t)d.num_levels * EPI_FIELDS * h.cout_pad, 0);
     for (int l = 0; l < d.num_levels; ++l) {
         const qconv_epilogue_t &e = levels[l];
         int32_t *t = epi.data() + (size_t)l * EPI_FIELDS * h.cout_pad;
         for (int c = 0; c < d.cout; ++c) {
-            t[EPI_BIAS * h.cout_pad + c] = e.bias[c];
+            const long long b = (long long)e.bias[c] + recentre[c];
+            if (b < INT32_MIN || b > INT32_MAX)
+                return fail(AQD_ERR_UNSUPPORTED, "bias + 128 * sum(w) exceeds int32 (8-bit codes)");
+            t[EPI_BIAS * h.cout_pad + c] = (int32_t)b;
             if (codes) {
                 const int sh = e.shift[c];
                 t[EPI_MULT * h.cout_pad + c] = e.mult[c];
@@ -403,7 +448,7 @@ const char *qconv_path(qconv_t conv)
         return "invalid";
     if (!conv->mfma)
         return "direct";
-    return conv->tile_cfg == TILE_FP4 ? "fp4-mfma" : "i8-mfma";
+    return conv->tile_cfg == TILE_FP4 ? "fp4-mfma" : "i8-mfma";  // TILE_B8 included
 }
 
 void qconv_destroy(qconv_t conv)
@@ -577,9 +622,12 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         for (int i = 0; i < count; ++i)
             t128 += ((long long)segs[i].n * chk[i].ho * chk[i].wo + 127) / 128 * h0.co_tiles;
         const bool short_codes = h0.ksteps <= 4 && h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_in == 4 &&
-                                 (h0.d.skip_bits == 0 || h0.d.skip_bits == 4);
-        if (short_codes && h0.ksteps <= 2 && h0.d.kh == 1 && h0.d.kw == 1 && h0.d.pad == 0 &&
-            h0.d.cout % 256 == 0) {
+                                 h0.d.bits_out == 4 && (h0.d.skip_bits == 0 || h0.d.skip_bits == 4);
+        if (h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_out == 8) {
+            // 8-bit code outputs: only the register-fed kernel writes them
+            tile_cfg = TILE_WV;
+        } else if (short_codes && h0.ksteps <= 2 && h0.d.kh == 1 && h0.d.kw == 1 && h0.d.pad == 0 &&
+                   h0.d.cout % 256 == 0) {
             tile_cfg = TILE_STREAM;
             blk_px = 64;
         } else if (short_codes && h0.d.kh == 1 && h0.d.kw == 1 && h0.d.pad == 0 && h0.d.cout % 256 == 0 &&
@@ -681,7 +729,8 @@ void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
 {
     if (a.tile_cfg == TILE_256x64S || a.tile_cfg == TILE_256x64 || a.tile_cfg == TILE_STREAM ||
         a.tile_cfg == TILE_STREAM_C128 || a.tile_cfg == TILE_STREAM_C64 || a.tile_cfg == TILE_128x128_O3 ||
-        a.tile_cfg == TILE_64x256_O3 || a.tile_cfg == TILE_STREAM_H128 || a.tile_cfg == TILE_WV) {  // never split
+        a.tile_cfg == TILE_64x256_O3 || a.tile_cfg == TILE_STREAM_H128 || a.tile_cfg == TILE_WV ||
+        a.tile_cfg == TILE_STEM) {  // never split
         *nparts = 1;
         *kchunk = a.ksteps;
         return;
@@ -691,9 +740,9 @@ void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
         P += a.seg[i].P;
     // the FP4 path: half the MFMA time per 64-channel step, parts of whole
     // 256-channel stages (4 steps)
-    const bool fp4 = a.tile_cfg == TILE_FP4;
+    const bool fp4 = a.tile_cfg == TILE_FP4, b8 = a.tile_cfg == TILE_B8;
     const double step_scale = fp4 ? 0.5 : 1.0;
-    const int align = fp4 ? 4 : 1;
+    const int align = fp4 ? 4 : b8 ? 2 : 1;
     auto cost = [&](int parts, int chunk) {
         const double units = (double)a.total_tiles * parts;
         const double per_cu = std::ceil(units / 256.0);
@@ -708,7 +757,7 @@ void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
     static const int cand[] = {2, 3, 4, 6, 8, 12, 16};
     for (int c : cand) {
         const int chunk = ((a.ksteps + c - 1) / c + align - 1) / align * align;
-        if (chunk < 2 || (fp4 && chunk >= a.ksteps))
+        if (chunk < 2 || ((fp4 || b8) && chunk >= a.ksteps))
             break;
         const int parts = (a.ksteps + chunk - 1) / chunk;  // every part non-empty
         const double t = cost(parts, chunk);

@@ -29,9 +29,15 @@ enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
        // read into registers (qconv_wv.hip), same weight layout as 256x128
        TILE_WV = 11,
        // 2-bit codes and 2-bit weights, cin and cout multiples of 256: 256 x 128
-       // tiles on the scaled FP4 MFMA (qconv_fp4.hip), weights stored as e2m1
-       // nibbles at create (FP4_KROW bytes per row and 128-channel K step)
-       TILE_FP4 = 12 };
+       // tiles on the scaled FP4 MFMA (qconv_b16.hip), weights stored as e2m1
+       // nibbles at create (64 bytes per row and 128-channel K step)
+       TILE_FP4 = 12,
+       // 8-bit codes, cin a multiple of 128, int32 outputs: 256 x 128 tiles on
+       // the int8 MFMA (qconv_b16.hip), weights in channel order at create
+       TILE_B8 = 13,
+       // the 7x7 stride-2 stem on a 3-channel 8-bit image: 64 x 256 tiles, K =
+       // the whole window (qconv_stem.hip)
+       TILE_STEM = 14 };
 constexpr int KC = 64;
 
 // tile shape of a configuration, and the channels one lane holds per pixel
@@ -84,16 +90,18 @@ struct MfmaArgs {
     int cin2, stride2, ksteps2;  // projection shortcut (fused launch only)
 };
 
-// bits_in in {2, 4}
+// bits_in in {2, 4}, or 8 with TILE_B8
 hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream);
 // fused projection shortcut (4-bit, 256 x 64 tiles): tile counts use blk_px = 64
 constexpr int PROJ_BLK_PX = 64;
 hipError_t launch_qconv_proj(const MfmaArgs &a, hipStream_t stream);
 // TILE_WV launches (qconv_wv.hip)
 hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream);
-// TILE_FP4 launches (qconv_fp4.hip); a.ksteps and a.kchunk in 64-channel steps,
-// multiples of 4
-hipError_t launch_qconv_fp4(const MfmaArgs &a, hipStream_t stream);
+// TILE_FP4 (code_bits 2) and TILE_B8 (code_bits 8) launches (qconv_b16.hip);
+// a.ksteps and a.kchunk in 64-channel steps, multiples of a stage (4 and 2)
+hipError_t launch_qconv_b16(int code_bits, const MfmaArgs &a, hipStream_t stream);
+// TILE_STEM launches (qconv_stem.hip); weights [co_tile][3][64 rows][64 B]
+hipError_t launch_qconv_stem(const MfmaArgs &a, hipStream_t stream);
 
 // ---- split-K combine + epilogue (qconv_splitk.hip) ---------------------------
 struct SplitSeg {

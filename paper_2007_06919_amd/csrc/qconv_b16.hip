@@ -1,34 +1,46 @@
-// Implicit-GEMM integer convolution of 2-bit codes with 2-bit weights on the
-// gfx950 scaled FP4 MFMA (v_mfma_scale_f32_16x16x128_f8f6f4, e2m1 operands),
-// for layers with 256-channel input chunks (cin and cout multiples of 256):
-// the ResNet-50 res4/res5 layers, the FPN and the heads of the paper's 2-bit
-// detectors. GEMM view of Eq. 4 (Sec. 3.2.1): rows = output channels,
-// columns = output pixels, K = taps x input channels.
+// Implicit-GEMM integer convolution whose MFMA operand row of a K step is
+// 16 bytes of staged codes, used as they are (no widening in the main loop):
+//  * 2-bit codes with 2-bit weights on the gfx950 scaled FP4 MFMA
+//    (v_mfma_scale_f32_16x16x128_f8f6f4, e2m1 operands, K step = 128 input
+//    channels), for layers with cin and cout multiples of 256: the ResNet-50
+//    res4/res5 layers, the FPN and the heads of the paper's 2-bit detectors;
+//  * 8-bit codes (the input and output layers of the paper's fully quantized
+//    networks, Sec. 4) on the int8 MFMA (v_mfma_i32_16x16x64_i8, K step = 64
+//    input channels), for cin a multiple of 128, int32 outputs (the
+//    prediction convolutions).
+// GEMM view of Eq. 4 (Sec. 3.2.1): rows = output channels, columns = output
+// pixels, K = taps x input channels.
 //
-// Exactness. Every operand is a small integer that e2m1 holds exactly: a
+// Exactness, FP4. Every operand is a small integer that e2m1 holds exactly: a
 // 2-bit weight value (odd grid -3, -1, 1, 3 or two's complement -2 .. 1) is
 // stored as its e2m1 nibble with block scale 1, an activation code k in
 // {0, 1, 2, 3} as the nibble k itself, which e2m1 reads as k / 2, with block
 // scale 2. Each product is then an integer, the MFMA sums them in fp32, and
 // every partial sum is bounded by K * 3 * 3 < 2^24 (checked at create), so
 // the fp32 accumulator holds the exact integer sum; its conversion to int32
-// is exact too. The epilogue is the integer one of Eq. 6-8 and Eq. 2.
+// is exact too.
+// Exactness, int8. An 8-bit code a in [0, 255] does not fit int8; the staging
+// copy stores a - 128 (the byte a XOR 0x80, read as signed), padding taps
+// included (code 0 -> -128), and the bias folded at create carries
+// 128 * sum(w) of the channel, so v = acc + bias is the exact sum of Eq. 6.
+// The epilogue is the integer one of Eq. 6-8 and Eq. 2.
 //
 // Workgroup tile 256 channels x 128 pixels, 4 waves; wave w owns channel rows
 // 64w .. 64w+63 (4 accumulator tiles of 16) for all 128 pixels (8 column
 // tiles), as in the register-fed int8 kernel:
-//  * weights (e2m1 nibbles, tiled at create; one K step = 128 input channels
-//    of one tap, 64 bytes per row) go from global memory straight into
-//    registers, three K steps ahead of their MFMAs;
-//  * activation codes go through LDS in stages of one tap's 256 channels
-//    (two K steps): each lane copies 8 bytes of packed 2-bit codes per piece
-//    and spreads them into 16 bytes of nibbles with two masks and a shift
-//    (even channels of a word in one word of nibbles, odd ones in the next;
-//    the weights were stored in that channel order at create). A pixel's 128
-//    bytes of nibbles are 16-byte columns XOR-swizzled with the pixel index,
-//    so that the copies' writes and the fragment reads (16 bytes per lane)
-//    are free of bank conflicts. A stage is loaded one stage ahead of its
-//    use and written during the stage before it (two-buffer ring, one
+//  * weights (tiled at create, 64 bytes per row and K step: 128 e2m1 nibbles
+//    or 64 int8) go from global memory straight into registers, three K steps
+//    ahead of their MFMAs;
+//  * activation codes go through LDS in stages of 128 bytes per pixel (one
+//    tap's 256 2-bit or 128 8-bit channels; two K steps). A copy lane takes 8
+//    bytes of packed 2-bit codes and spreads them into 16 bytes of nibbles
+//    with two masks and a shift (even channels of a word in one word of
+//    nibbles, odd ones in the next; the weights were stored in that channel
+//    order at create), or 16 bytes of 8-bit codes and flips their top bits.
+//    A pixel's 128 bytes are 16-byte columns XOR-swizzled with the pixel
+//    index, so that the copies' writes and the fragment reads (16 bytes per
+//    lane) are free of bank conflicts. A stage is loaded one stage ahead of
+//    its use and written during the stage before it (two-buffer ring, one
 //    barrier per stage).
 //  * A part of a split K range (whole stages) writes int32 partial sums, the
 //    first part with the bias, for the split-K combining epilogue.
@@ -49,7 +61,7 @@ constexpr int F4_ROW = 128;                   // LDS bytes of one stage per pixe
 constexpr int F4_STAGE = F4_BPX * F4_ROW;     // 16 KiB
 constexpr int F4_TAB = 2 * F4_STAGE;          // epilogue tables after the ring of two stages
 constexpr int F4_LDS = 4 * F4_STAGE;          // int32 staging uses all 64 KiB
-constexpr int F4_KROW = 64;                   // weight bytes per row and K step (128 nibbles)
+constexpr int F4_KROW = 64;                   // weight bytes per row and K step
 constexpr int F4_SCALE_W = 127;               // E8M0 block scales: 2^0 for the weights,
 constexpr int F4_SCALE_X = 128;               // 2^1 for the codes (nibble k reads as k / 2)
 
@@ -85,13 +97,20 @@ __device__ __forceinline__ void mfma_fence(v4f (&acc)[MI][NJ])
                    "+v"(acc[3][4]), "+v"(acc[3][5]), "+v"(acc[3][6]), "+v"(acc[3][7]));
 }
 
-// OUTK: 0 = 2-bit codes, 1 = int32 (v = acc + bias, or a split part's sums);
-// SKK: 0 = no skip, 1 = 2-bit code skip; FAST: every shift >= 2 (32-bit requantisation)
-template <int OUTK, int SKK, int FAST>
-__global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
+// CB: input code width, 2 (FP4 MFMA) or 8 (int8 MFMA); OUTK: 0 = 2-bit codes
+// (CB 2 only), 1 = int32 (v = acc + bias, or a split part's sums); SKK: 0 = no
+// skip, 1 = 2-bit code skip; FAST: every shift >= 2 (32-bit requantisation)
+template <int CB, int OUTK, int SKK, int FAST>
+__global__ void __launch_bounds__(256, 2) qconv_b16_kernel(MfmaArgs A)
 {
+    static_assert(CB == 2 || CB == 8, "2-bit or 8-bit input codes");
     static_assert(OUTK == 0 || SKK == 0, "int32 outputs have no skip");
+    static_assert(CB == 2 || OUTK == 1, "8-bit inputs: int32 outputs");
+    constexpr bool FP4 = CB == 2;
     constexpr int MI = 4, NJ = 8, QMAX = 3, BO = 2;
+    constexpr int SPS = FP4 ? 4 : 2;            // 64-channel steps per stage
+    constexpr int SCH = FP4 ? 256 : 128;        // input channels per stage
+    using acc_t = typename std::conditional<FP4, v4f, v4i>::type;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[F4_LDS];
 
     const int bid = blockIdx.x;
@@ -116,18 +135,20 @@ __global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, g = lane >> 4;
 
-    // K range of this part in stages (one tap's 256 channels; A.ksteps and
-    // A.kchunk count 64-channel steps, multiples of 4 on this path)
-    const int row_bytes = A.cin / 4;
-    const int spt = A.cin / 256;                           // stages per tap
-    const int st0 = kpart * (A.kchunk / 4);
-    const int NST = min(A.kchunk, A.ksteps - kpart * A.kchunk) / 4;  // >= 1 (host)
-    const int KS4 = A.ksteps / 2;                          // 128-channel K steps of the whole range
+    // K range of this part in stages (one tap's SCH channels; A.ksteps and
+    // A.kchunk count 64-channel steps, multiples of SPS on this path); the
+    // kernel's K steps are two per stage
+    const int row_bytes = A.cin * CB / 8;
+    const int spt = A.cin / SCH;                           // stages per tap
+    const int st0 = kpart * (A.kchunk / SPS);
+    const int NST = min(A.kchunk, A.ksteps - kpart * A.kchunk) / SPS;  // >= 1 (host)
+    const int KSK = 2 * (A.ksteps / SPS);                  // kernel K steps of the whole range
     const int hw = S.ho * S.wo;
 
     // ---- activation copies: piece m of a stage = pixels 32m .. 32m+31, lane
-    // tid copying packed bytes 8c .. 8c+7 (channels 32c .. 32c+31) of pixel
-    // 32m + tid / 8, c = tid % 8
+    // tid copying stage bytes 8c .. 8c+7 (2-bit: channels 32c .. 32c+31) or
+    // 16c .. 16c+15 (8-bit: channels 16c .. 16c+15) of pixel 32m + tid / 8,
+    // c = tid % 8
     const int c8 = tid & 7;
     int ih0[4], iw0[4], xpix[4];
 #pragma unroll
@@ -141,7 +162,7 @@ __global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
         iw0[m] = (int)ow * A.stride - A.pad;
         xpix[m] = (int)pn * S.h * S.w;   // n * h * w < 2^31, checked on the host
     }
-    const uint8_t *xsrc = S.x + 8 * c8;
+    const uint8_t *xsrc = S.x + (FP4 ? 8 : 16) * c8;
     // LDS: 16-byte column c of pixel p at 128 p + 16 (c ^ (p & 7))
     const int wp = tid >> 3;
     const uint32_t wofs = F4_ROW * wp + 16 * (c8 ^ (wp & 7));
@@ -166,27 +187,38 @@ __global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
     };
     // taps in the padding, pixels past the end and stages past the last read a
     // clamped position inside the image and are masked to code 0
-    auto load_piece = [&](int m) -> uint2 {
+    using piece_t = typename std::conditional<FP4, uint2, uint4>::type;
+    auto load_piece = [&](int m) -> piece_t {
         const int ih = ih0[m] + tr, iw = iw0[m] + tq;
         const bool in = ((unsigned)ih < (unsigned)S.h) & ((unsigned)iw < (unsigned)S.w);
         const int ihc = min(max(ih, 0), S.h - 1), iwc = min(max(iw, 0), S.w - 1);
-        const uint2 v = *(const uint2 *)(xsrc + (long long)(xpix[m] + ihc * S.w + iwc) * row_bytes + 64 * th);
+        const uint8_t *src = xsrc + (long long)(xpix[m] + ihc * S.w + iwc) * row_bytes + (SCH * CB / 8) * th;
         const uint32_t keep = in ? 0xFFFFFFFFu : 0u;
-        return make_uint2(v.x & keep, v.y & keep);
+        if constexpr (FP4) {
+            const uint2 v = *(const uint2 *)src;
+            return make_uint2(v.x & keep, v.y & keep);
+        } else {
+            const uint4 v = *(const uint4 *)src;
+            return make_uint4(v.x & keep, v.y & keep, v.z & keep, v.w & keep);
+        }
     };
-    // 32 packed codes -> 32 nibbles: word 2h holds the even channels of packed
-    // word h, word 2h + 1 the odd ones
-    auto write_piece = [&](int buf, int m, const uint2 v) {
-        const uint4 n = make_uint4(v.x & 0x33333333u, (v.x >> 2) & 0x33333333u,
-                                   v.y & 0x33333333u, (v.y >> 2) & 0x33333333u);
+    // 2-bit: 32 packed codes -> 32 nibbles, word 2h holding the even channels
+    // of packed word h, word 2h + 1 the odd ones; 8-bit: code a -> a - 128
+    auto write_piece = [&](int buf, int m, const piece_t v) {
+        uint4 n;
+        if constexpr (FP4)
+            n = make_uint4(v.x & 0x33333333u, (v.x >> 2) & 0x33333333u,
+                           v.y & 0x33333333u, (v.y >> 2) & 0x33333333u);
+        else
+            n = make_uint4(v.x ^ 0x80808080u, v.y ^ 0x80808080u, v.z ^ 0x80808080u, v.w ^ 0x80808080u);
         *(uint4 *)(lds + buf * F4_STAGE + m * (32 * F4_ROW) + wofs) = n;
     };
 
-    // ---- weights: this wave's rows of K step k (128 channels), accumulator
-    // tile i at wa + k * 16 KiB + i * 1 KiB (lane: row r, 16-byte column g);
-    // the look-ahead reads up to three steps past the part's last (inside the
-    // tile range or the allocation's four steps of padding), never used
-    const int8_t *wa = S.wt + ((long long)co_tile * KS4 * F4_BCO + 64 * wave + r) * F4_KROW + 16 * g;
+    // ---- weights: this wave's rows of K step k, accumulator tile i at
+    // wa + k * 16 KiB + i * 1 KiB (lane: row r, 16-byte column g); the
+    // look-ahead reads up to three steps past the part's last (inside the tile
+    // range or the allocation's four steps of padding), never used
+    const int8_t *wa = S.wt + ((long long)co_tile * KSK * F4_BCO + 64 * wave + r) * F4_KROW + 16 * g;
     const int k0 = 2 * st0;
     auto load_a = [&](int k, v4i *dst) {
 #pragma unroll
@@ -197,13 +229,14 @@ __global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
     // lane group g of wave w holds channels 128 (w >> 1) + 32 g + 16 (w & 1) + 4 i + e
     const int co_loc = 128 * (wave >> 1) + 32 * g + 16 * (wave & 1);
     const int co_glob = co_tile * F4_BCO + co_loc;
-    v4f acc[MI][NJ];
+    acc_t acc[MI][NJ];
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
-            acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
-    mfma_fence(acc);  // the zeros are written before the first MFMA reads them
+            acc[i][j] = acc_t{0, 0, 0, 0};
+    if constexpr (FP4)
+        mfma_fence(acc);  // the zeros are written before the first MFMA reads them
     // block scales in registers the compiler cannot rematerialise next to an MFMA
     int scale_w = F4_SCALE_W, scale_x = F4_SCALE_X;
     asm volatile("" : "+v"(scale_w), "+v"(scale_x));
@@ -227,7 +260,7 @@ __global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
     static_assert(F4_TAB + (EPI_FIELDS + QMAX + 1) * F4_BCO * 4 <= F4_LDS, "tables fit past the ring");
 
     // ---- prologue: stage 0 in LDS, stage 1 in registers, weights of steps 0-2
-    uint2 rb[4];
+    piece_t rb[4];
 #pragma unroll
     for (int m = 0; m < 4; ++m)
         write_piece(0, m, load_piece(m));
@@ -241,8 +274,8 @@ __global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
     load_a(1, fa[1]);
     load_a(2, fa[2]);
     v4i fb[NJ];
-    int kstep = 0;         // K step (128 channels) of this part being multiplied
-    constexpr int RA = 3;  // fragments are read RA column tiles ahead of their MFMAs
+    int kstep = 0;         // K step of this part being multiplied
+    constexpr int RA = FP4 ? 3 : 2;  // fragments are read RA column tiles ahead of their MFMAs
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 #pragma unroll
     for (int j = 0; j < RA; ++j)
@@ -273,8 +306,12 @@ __global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
                 if constexpr (q == 1 && j == NJ - RA)
                     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 #pragma unroll
-                for (int i = 0; i < MI; ++i)
-                    mfma_fp4(fa[kq][i], fb[j], acc[i][j], scale_w, scale_x);
+                for (int i = 0; i < MI; ++i) {
+                    if constexpr (FP4)
+                        mfma_fp4(fa[kq][i], fb[j], acc[i][j], scale_w, scale_x);
+                    else
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[kq][i], fb[j], acc[i][j], 0, 0, 0);
+                }
                 if constexpr (j + RA < NJ)
                     fb[j + RA] = *(const v4i *)(lds + 2048 * (j + RA) + r_this);
                 else
@@ -293,7 +330,8 @@ __global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
             stage(std::integral_constant<int, 1>{});
     }
 
-    mfma_fence(acc);  // the last MFMAs have written the accumulators
+    if constexpr (FP4)
+        mfma_fence(acc);  // the last MFMAs have written the accumulators
     // exact integer sums (see the header), converted where they are used;
     // the bias of Eq. 6 joins there
     if constexpr (OUTK == 1) {
@@ -301,6 +339,8 @@ __global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
         // of 64 pixels through LDS rows of 256 int32 (16-byte chunk c of pixel
         // p at c ^ (p & 7)); every thread then stores 16-byte chunks of whole rows
         int32_t *ybase = (int32_t *)S.y + (long long)kpart * S.P * A.cout;
+        // the tile's valid 16-byte chunks (a partial last channel tile)
+        const int valid_chunks = min(A.cout - co_tile * F4_BCO, F4_BCO) / 4;
         const bool with_bias = !(A.part && kpart > 0);
         v4i bias[MI];
 #pragma unroll
@@ -316,7 +356,7 @@ __global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
 #pragma unroll
                 for (int i = 0; i < MI; ++i) {
                     const int c = co_loc / 4 + i;
-                    const v4f a = acc[i][4 * pass + jj];
+                    const acc_t a = acc[i][4 * pass + jj];
                     *(v4i *)(lds + p * 1024 + 16 * (c ^ (p & 7))) =
                         v4i{(int)a.x, (int)a.y, (int)a.z, (int)a.w} + bias[i];
                 }
@@ -327,7 +367,7 @@ __global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
                 const int idx = it * 256 + tid;
                 const int p = idx >> 6, c = idx & 63;
                 const long long px = (long long)px_tile * F4_BPX + 64 * pass + p;
-                if (px < S.P)
+                if (px < S.P && c < valid_chunks)
                     *(v4i *)(ybase + px * A.cout + co_tile * F4_BCO + 4 * c) =
                         *(const v4i *)(lds + p * 1024 + 16 * (c ^ (p & 7)));
             }
@@ -442,28 +482,39 @@ __global__ void __launch_bounds__(256, 2) qconv_fp4_kernel(MfmaArgs A)
 
 }  // namespace
 
-hipError_t launch_qconv_fp4(const MfmaArgs &a, hipStream_t stream)
+hipError_t launch_qconv_b16(int code_bits, const MfmaArgs &a, hipStream_t stream)
 {
-    if ((a.bits_out != 2 && a.bits_out != 32) || (a.skip_bits != 0 && (a.skip_bits != 2 || a.bits_out == 32)) ||
-        a.cin % 256 != 0 || a.cout % 256 != 0 || a.co_tiles * F4_BCO != a.cout || a.ksteps % 4 != 0 ||
-        a.kchunk % 4 != 0 || a.kchunk < 4 || (a.part == 0 && a.ksplit != 1) || (a.part && a.bits_out != 32))
-        return hipErrorInvalidValue;
     dim3 grid(8 * a.tiles_per_xcd), block(256);
+    if (a.part == 0 && a.ksplit != 1)
+        return hipErrorInvalidValue;
+    if (code_bits == 8) {
+        // int32 outputs (or split parts); a partial last channel tile
+        if (a.bits_out != 32 || a.skip_bits != 0 || a.cin % 128 != 0 || a.co_tiles * F4_BCO < a.cout ||
+            a.cout % 4 != 0 || a.ksteps % 2 != 0 || a.kchunk % 2 != 0 || a.kchunk < 2)
+            return hipErrorInvalidValue;
+        hipLaunchKernelGGL((qconv_b16_kernel<8, 1, 0, 1>), grid, block, 0, stream, a);
+        return hipGetLastError();
+    }
+    if (code_bits != 2 || (a.bits_out != 2 && a.bits_out != 32) ||
+        (a.skip_bits != 0 && (a.skip_bits != 2 || a.bits_out == 32)) || a.cin % 256 != 0 ||
+        a.cout % 256 != 0 || a.co_tiles * F4_BCO != a.cout || a.ksteps % 4 != 0 || a.kchunk % 4 != 0 ||
+        a.kchunk < 4 || (a.part && a.bits_out != 32))
+        return hipErrorInvalidValue;
     bool fast = true;
     for (int i = 0; i < a.nseg; ++i)
         fast = fast && a.seg[i].fast;
     if (a.bits_out == 32)
-        hipLaunchKernelGGL((qconv_fp4_kernel<1, 0, 1>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((qconv_b16_kernel<2, 1, 0, 1>), grid, block, 0, stream, a);
     else if (a.skip_bits == 0) {
         if (fast)
-            hipLaunchKernelGGL((qconv_fp4_kernel<0, 0, 1>), grid, block, 0, stream, a);
+            hipLaunchKernelGGL((qconv_b16_kernel<2, 0, 0, 1>), grid, block, 0, stream, a);
         else
-            hipLaunchKernelGGL((qconv_fp4_kernel<0, 0, 0>), grid, block, 0, stream, a);
+            hipLaunchKernelGGL((qconv_b16_kernel<2, 0, 0, 0>), grid, block, 0, stream, a);
     } else {
         if (fast)
-            hipLaunchKernelGGL((qconv_fp4_kernel<0, 1, 1>), grid, block, 0, stream, a);
+            hipLaunchKernelGGL((qconv_b16_kernel<2, 0, 1, 1>), grid, block, 0, stream, a);
         else
-            hipLaunchKernelGGL((qconv_fp4_kernel<0, 1, 0>), grid, block, 0, stream, a);
+            hipLaunchKernelGGL((qconv_b16_kernel<2, 0, 1, 0>), grid, block, 0, stream, a);
     }
     return hipGetLastError();
 }

@@ -1099,7 +1099,9 @@ void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane)
     switch (tile_cfg) {
     case TILE_256x128: *blk_co = 256; *blk_px = 128; *chan_per_lane = 32; return;
     case TILE_WV: *blk_co = 256; *blk_px = 128; *chan_per_lane = 16; return;
-    case TILE_FP4: *blk_co = 256; *blk_px = 128; *chan_per_lane = 32; return;
+    case TILE_FP4:
+    case TILE_B8: *blk_co = 256; *blk_px = 128; *chan_per_lane = 32; return;
+    case TILE_STEM: *blk_co = 64; *blk_px = 256; *chan_per_lane = 16; return;
     case TILE_256x64S:
     case TILE_256x64:
     case TILE_STREAM: *blk_co = 256; *blk_px = 64; *chan_per_lane = 32; return;
@@ -1239,8 +1241,10 @@ hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
         case TILE_128x256: return launch_modes<4, 4, 8, 2, 2>(a, stream);
         case TILE_64x512: return launch_modes<4, 4, 8, 1, 4>(a, stream);
         }
-    } else if (bits_in == 2 && a.tile_cfg == TILE_FP4) {
-        return launch_qconv_fp4(a, stream);
+    } else if ((bits_in == 2 && a.tile_cfg == TILE_FP4) || (bits_in == 8 && a.tile_cfg == TILE_B8)) {
+        return launch_qconv_b16(bits_in, a, stream);
+    } else if (bits_in == 8 && a.tile_cfg == TILE_STEM) {
+        return launch_qconv_stem(a, stream);
     } else if (bits_in == 2) {
         switch (a.tile_cfg) {
         case TILE_128x256: return launch_modes<2, 4, 8, 2, 2>(a, stream);

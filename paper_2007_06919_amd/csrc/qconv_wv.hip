@@ -45,13 +45,16 @@ constexpr int WV_STAGE = WV_BPX * WV_ROW;  // 16 KiB
 constexpr int WV_NBUF = 4;
 constexpr int WV_LDS = WV_NBUF * WV_STAGE;
 
-// OUTK: 0 = 4-bit codes, 1 = int32 v = acc + bias (then SKK = 0);
+// OUTK: 0 = 4-bit codes, 1 = int32 v = acc + bias (then SKK = 0), 2 = 8-bit
+// codes (the last tower layer of the fully quantized heads; then SKK = 0);
 // SKK: 0 = no skip, 1 = code skip (4-bit); FAST: every shift >= 2 (32-bit requantisation)
 template <int OUTK, int SKK, int FAST>
 __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
 {
-    static_assert(OUTK == 0 || SKK == 0, "int32 outputs have no skip");
-    constexpr int BI = 4, MI = 4, NJ = 8, QMAX = 15, OW = 2;
+    static_assert(OUTK == 0 || SKK == 0, "int32 and 8-bit outputs have no skip");
+    constexpr int BI = 4, MI = 4, NJ = 8;
+    constexpr int BO = OUTK == 2 ? 8 : 4;          // output code width
+    constexpr int QMAX = (1 << BO) - 1, OW = BO / 2;  // words of a lane's 16 channels
     __shared__ __attribute__((aligned(1024))) uint8_t lds[WV_LDS];
 
     const int bid = blockIdx.x;
@@ -242,7 +245,7 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
     // its loads are issued before the last stage, whose MFMAs hide their latency
     constexpr int PRM_PER = EPI_FIELDS * WV_BCO / 256;
     int prm_r[PRM_PER];
-    if constexpr (OUTK == 0) {
+    if constexpr (OUTK != 1) {
 #pragma unroll
         for (int t = 0; t < PRM_PER; ++t) {
             const int i = tid + 256 * t;
@@ -295,7 +298,7 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
     for (int j = 0; j < NJ; ++j)
         okj[j] = co_ok && px0 + 16 * j < S.P;
     // skip codes: issued before the tables go to LDS, so that the two overlap
-    uint32_t skw[NJ][OW];
+    uint32_t skw[NJ][2];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
         skw[j][0] = skw[j][1] = 0;
@@ -341,7 +344,9 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
     uint32_t outw[NJ][OW];
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
-        outw[j][0] = outw[j][1] = 0;
+#pragma unroll
+        for (int o = 0; o < OW; ++o)
+            outw[j][o] = 0;
     // per channel group i: the requantisation parameters, read once for all
     // columns
     auto group = [&](auto lut_c, auto ic, int j0, int j1) {
@@ -372,10 +377,10 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int v = acc[i][j][e];  // acc + bias
-                const int bit = (4 * i + e) * BI;
+                const int bit = (4 * i + e) * BO, kbit = (4 * i + e) * BI;
                 int kv = 0;
                 if constexpr (SKK == 1)
-                    kv = (int)__builtin_amdgcn_ubfe(skw[j][bit >> 5], bit & 31, BI);
+                    kv = (int)__builtin_amdgcn_ubfe(skw[j][kbit >> 5], kbit & 31, BI);
                 int y;
                 if constexpr (FAST) {
                     int u = v;
@@ -406,26 +411,40 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
         body(std::true_type{});
     else
         body(std::false_type{});
-    if (A.qmax == 7) {  // 3-bit codes (the epilogue clamped to 15)
+    if (OUTK == 0 && A.qmax == 7) {  // 3-bit codes (the epilogue clamped to 15)
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
             outw[j][0] = sat7_nibbles(outw[j][0]);
             outw[j][1] = sat7_nibbles(outw[j][1]);
         }
     }
+    // the packed words are complete here: the compiler would otherwise sink
+    // their last steps into the conditional stores and keep every 64-bit
+    // product alive until then
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
-        if (okj[j])
-            *(uint2 *)((uint8_t *)S.y + (px0 + 16 * j) * (A.cout * BI / 8) + co_glob * BI / 8) =
-                make_uint2(outw[j][0], outw[j][1]);
+#pragma unroll
+        for (int o = 0; o < OW; ++o)
+            asm volatile("" : "+v"(outw[j][o]));
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+        if (okj[j]) {
+            uint8_t *dst = (uint8_t *)S.y + (px0 + 16 * j) * (A.cout * BO / 8) + co_glob * BO / 8;
+            if constexpr (BO == 8)
+                *(uint4 *)dst = make_uint4(outw[j][0], outw[j][1], outw[j][2], outw[j][3]);
+            else
+                *(uint2 *)dst = make_uint2(outw[j][0], outw[j][1]);
+        }
 }
 
 }  // namespace
 
 hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream)
 {
-    if ((a.bits_out != 4 && a.bits_out != 32) || (a.skip_bits != 0 && (a.skip_bits != 4 || a.bits_out == 32)) ||
-        a.cin % 256 != 0 || a.ksteps % 4 != 0 || a.ksplit != 1 || a.part != 0)
+    const bool codes8 = a.bits_out == 8;
+    if ((a.bits_out != 4 && a.bits_out != 8 && a.bits_out != 32) ||
+        (a.skip_bits != 0 && (a.skip_bits != 4 || a.bits_out != 4)) || a.cin % 256 != 0 ||
+        a.ksteps % 4 != 0 || a.ksplit != 1 || a.part != 0)
         return hipErrorInvalidValue;
     dim3 grid(8 * a.tiles_per_xcd), block(256);
     bool fast = true;
@@ -433,7 +452,12 @@ hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream)
         fast = fast && a.seg[i].fast;
     if (a.bits_out == 32)
         hipLaunchKernelGGL((qconv_wv_kernel<1, 0, 1>), grid, block, 0, stream, a);
-    else if (a.skip_bits == 0) {
+    else if (codes8) {
+        if (fast)
+            hipLaunchKernelGGL((qconv_wv_kernel<2, 0, 1>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_wv_kernel<2, 0, 0>), grid, block, 0, stream, a);
+    } else if (a.skip_bits == 0) {
         if (fast)
             hipLaunchKernelGGL((qconv_wv_kernel<0, 0, 1>), grid, block, 0, stream, a);
         else

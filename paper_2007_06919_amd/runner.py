@@ -42,6 +42,8 @@ from .workloads import NetParams, NetSpec
 def _conv_key(net: NetSpec, conv) -> tuple:
     x, skip, y = conv.segs[0]
     ty = net.tensors[y]
+    if conv.op != "conv":
+        return (conv.op, conv.name)   # launched alone
     return (conv.cin, conv.cout, conv.k, conv.stride, net.tensors[x].bits, conv.bits_w, conv.wenc,
             ty.bits, net.tensors[skip].bits if skip else 0, conv.skip_up2)
 
@@ -126,6 +128,7 @@ class Net:
             packed = aqd.pack_codes(params.inputs[name], t.bits)
             self.bufs[name].copy_(torch.from_numpy(packed))
         self.handles: Dict[str, int] = {}
+        self._pool_descs = []
         self.tables: Dict[str, List[dict]] = {}
         self._alpha_t: Dict[str, np.ndarray] = {}
         self.schedule = self._make_schedule()
@@ -134,8 +137,8 @@ class Net:
         self._build()
         self.ws_bytes = 0
         if split_k:
-            self.ws_bytes = max(aqd.qconv_group_workspace([self._seg_args(c, si) for c, si in g])
-                                for g in self.schedule)
+            self.ws_bytes = max([aqd.qconv_group_workspace([self._seg_args(c, si) for c, si in g])
+                                 for g in self.schedule if g[0][0].op == "conv"], default=0)
         self.ws = (torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
                    if self.ws_bytes else None)
         # independent launches (FPN side branches, the box prediction next to
@@ -188,7 +191,9 @@ class Net:
         for gi, group in enumerate(self.schedule):
             k = self.lane[gi]
             cs = []
-            if k is not None:
+            if k is not None and group[0][0].op == "maxpool":
+                cs.append(self._pool_call(group[0][0]))
+            elif k is not None:
                 plain = [(c, si) for c, si in group
                          if c.name not in self._fused_away and c.name not in self.fused]
                 if plain:
@@ -210,6 +215,16 @@ class Net:
                                     self.bufs[xp].data_ptr(), self.bufs[y].data_ptr())))
             calls.append(cs)
         return calls
+
+    def _pool_call(self, conv):
+        """(function, arguments) of a max-pooling layer's launch; the
+        descriptor is kept alive on the runner."""
+        x, _, y = conv.segs[0]
+        tx = self.net.tensors[x]
+        d = aqd.MaxpoolDesc(tx.n, tx.h, tx.w, tx.c, tx.bits, conv.k, conv.stride, conv.pad)
+        self._pool_descs.append(d)
+        return (aqd.lib().aqd_maxpool_run, (aqd.ctypes.byref(d), self.bufs[x].data_ptr(),
+                                            self.bufs[y].data_ptr()))
 
     def launches_per_forward(self) -> int:
         n = 0
@@ -312,6 +327,12 @@ class Net:
         (later layers calibrate on the outputs of earlier ones)."""
         for conv in self.net.convs:
             x, skip, y = conv.segs[0]
+            if conv.op == "maxpool":
+                tx = self.net.tensors[x]
+                self.tables[conv.name] = []
+                aqd.maxpool_run(tx.n, tx.h, tx.w, tx.c, tx.bits, conv.k, conv.stride, conv.pad,
+                                self.bufs[x], self.bufs[y], self.stream)
+                continue
             ty = self.net.tensors[y]
             out_mode = aqd.OUT_INT32 if ty.bits == 32 else aqd.OUT_CODES
             bits_out = 0 if ty.bits == 32 else ty.bits
@@ -408,6 +429,8 @@ class Net:
     def group_macs(self, group) -> int:
         tot = 0
         for conv, si in group:
+            if conv.op != "conv":
+                continue
             t = self.net.tensors[conv.segs[si][2]]
             tot += t.n * t.h * t.w * conv.cout * conv.k * conv.k * conv.cin
         return tot

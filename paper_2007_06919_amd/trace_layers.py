@@ -24,6 +24,8 @@ def launch_list(net):
     away = {d.name for d in fused.values()}
 
     def macs(c, si):
+        if c.op != "conv":
+            return 0
         t = net.tensors[c.segs[si][2]]
         return t.n * t.h * t.w * c.cout * c.k * c.k * c.cin
 
@@ -45,7 +47,7 @@ def layer_table(trace_csv, workload=4, top=30, passes=5):
     net, _ = workloads.config(workload)
     launches = launch_list(net)
     rows = sorted((r for r in csv.DictReader(open(trace_csv))
-                   if any(k in r["Kernel_Name"] for k in ("qconv_", "splitk_"))),
+                   if any(k in r["Kernel_Name"] for k in ("qconv_", "splitk_", "maxpool_kernel"))),
                   key=lambda r: int(r["Dispatch_Id"]))  # enqueue order (launches on several streams overlap)
     # one entry per launch; a combining kernel belongs to the launch before it
     seq = []

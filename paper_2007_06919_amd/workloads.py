@@ -88,6 +88,7 @@ class ConvSpec:
     segs: List[Tuple[str, Optional[str], str]]
     skip_up2: bool = False
     wenc: int = WENC_TWOS
+    op: str = "conv"     # "conv", or "maxpool" (k x k, stride, pad k // 2; no weights)
 
     @property
     def pad(self) -> int:
@@ -119,6 +120,16 @@ class NetSpec:
         self.convs.append(c)
         return c
 
+    def maxpool(self, name, x, y, k, stride) -> ConvSpec:
+        """k x k max-pooling of codes (pad k // 2); the output has the input's
+        width and step (Sec. 3.2.4)."""
+        tx = self.tensors[x]
+        ho, wo = out_size(tx.h, k, stride, k // 2), out_size(tx.w, k, stride, k // 2)
+        self.add_tensor(y, tx.n, ho, wo, tx.c, tx.bits)
+        c = ConvSpec(name, tx.c, tx.c, k, stride, 0, [(x, None, y)], False, self.wenc, op="maxpool")
+        self.convs.append(c)
+        return c
+
     def conv_levels(self, name, xs, ys, cout, k, bits_w, bits_out) -> ConvSpec:
         """Stride-1 conv with shared weights over several levels."""
         segs = []
@@ -131,6 +142,8 @@ class NetSpec:
         return c
 
     def macs(self, conv: ConvSpec) -> int:
+        if conv.op != "conv":
+            return 0
         total = 0
         for _, _, y in conv.segs:
             t = self.tensors[y]
@@ -190,18 +203,25 @@ def pyramid_sizes(h: int, w: int) -> List[Tuple[int, int]]:
     return sizes
 
 
-def add_retina_heads(net: NetSpec, levels, bits, towers=("cls", "box")):
+def add_retina_heads(net: NetSpec, levels, bits, towers=("cls", "box"), io_bits=None):
     """RetinaNet heads shared over the pyramid levels, with a private epilogue
-    table per level (multi-level BN)."""
+    table per level (multi-level BN). io_bits: the prediction convolutions as
+    output layers of that width (their input codes, from the last tower
+    layer, and their two's-complement weights; Sec. 4, the fully quantized
+    networks), else at ``bits``."""
     for tower in towers:
         xs = list(levels)
         for i in range(1, 5):
             ys = [f"{tower}{i}.{lv}" for lv in levels]
-            net.conv_levels(f"{tower}.t{i}", xs, ys, 256, 3, bits, bits)
+            net.conv_levels(f"{tower}.t{i}", xs, ys, 256, 3, bits, io_bits if (io_bits and i == 4) else bits)
             xs = ys
         cout = NUM_ANCHORS * NUM_CLASSES if tower == "cls" else NUM_ANCHORS * 4
         ys = [f"{tower}_out.{lv}" for lv in levels]
-        net.conv_levels(f"{tower}.pred", xs, ys, cout, 3, bits, 32)
+        wenc = net.wenc
+        if io_bits:
+            net.wenc = WENC_TWOS
+        net.conv_levels(f"{tower}.pred", xs, ys, cout, 3, io_bits or bits, 32)
+        net.wenc = wenc
         net.outputs.extend(ys)
 
 
@@ -251,14 +271,28 @@ def head_tower_net(n, h, w, bits, wenc=WENC_PAPER_ODD) -> NetSpec:
     return net
 
 
-def retinanet_r50_net(n, h, w, bits, heads=True, wenc=WENC_PAPER_ODD) -> NetSpec:
-    """ResNet-50 (bottleneck, stride on the 3x3) without the stem, FPN with
-    fused top-down adds, P6/P7, and optionally the RetinaNet heads."""
+def retinanet_r50_net(n, h, w, bits, heads=True, wenc=WENC_PAPER_ODD, io_bits=None) -> NetSpec:
+    """ResNet-50 (bottleneck, stride on the 3x3), FPN with fused top-down
+    adds, P6/P7, and optionally the RetinaNet heads. Without io_bits the
+    network starts after the stem (input: the max-pooled stem output); with
+    io_bits (8: the paper's fully quantized networks, Sec. 4) it starts at
+    the image (3 channels of io_bits codes) with the 7x7 stride-2 stem
+    (io_bits two's-complement weights, ``bits`` output codes) and the 3x3
+    stride-2 max-pooling, and the heads' prediction convolutions are io_bits
+    layers."""
     net = NetSpec(wenc=wenc)
-    h2 = out_size(out_size(h, 7, 2, 3), 3, 2, 1)
-    w2 = out_size(out_size(w, 7, 2, 3), 3, 2, 1)
-    net.add_tensor("c2in", n, h2, w2, 64, bits)
-    net.inputs.append("c2in")
+    if io_bits:
+        net.add_tensor("img", n, h, w, 3, io_bits)
+        net.inputs.append("img")
+        net.wenc = WENC_TWOS
+        net.conv("stem", "img", "c1", 64, 7, 2, io_bits, bits)
+        net.wenc = wenc
+        net.maxpool("pool", "c1", "c2in", 3, 2)
+    else:
+        h2 = out_size(out_size(h, 7, 2, 3), 3, 2, 1)
+        w2 = out_size(out_size(w, 7, 2, 3), 3, 2, 1)
+        net.add_tensor("c2in", n, h2, w2, 64, bits)
+        net.inputs.append("c2in")
     x = "c2in"
     cin = 64
     stage_out = {}
@@ -288,7 +322,7 @@ def retinanet_r50_net(n, h, w, bits, heads=True, wenc=WENC_PAPER_ODD) -> NetSpec
     net.conv("fpn.p6", c5, "p6", 256, 3, 2, bits, bits)
     net.conv("fpn.p7", "p6", "p7", 256, 3, 2, bits, bits)
     if heads:
-        add_retina_heads(net, LEVELS, bits)
+        add_retina_heads(net, LEVELS, bits, io_bits=io_bits)
     else:
         net.outputs.extend(LEVELS)
     return net
@@ -361,6 +395,8 @@ def make_params(net: NetSpec, seed: int, mode: str) -> NetParams:
     alpha = {name: NU / qmax(t.bits) for name, t in net.tensors.items() if t.bits != 32}
     weights, alpha_w, segs = {}, {}, {}
     for conv in net.convs:
+        if conv.op != "conv":
+            continue
         weights[conv.name], _ = draw_weights(rng, conv.cout, conv.k, conv.cin, conv.bits_w,
                                              conv.wenc)
         alpha_w[conv.name] = 1.0 / qmax(conv.bits_w)
@@ -422,10 +458,12 @@ def scaled_config(idx: int, n: int, h: int, w: int, seed: Optional[int] = None):
     return net, make_params(net, seed, "calibrated")
 
 
-def retinanet_config(n: int, h: int, w: int, bits: int, seed: int = 6):
+def retinanet_config(n: int, h: int, w: int, bits: int, seed: int = 6, io_bits=None):
     """ResNet-50 + FPN + RetinaNet heads at any code width (3: the paper's
-    3-bit networks, Tables 2 and 4), calibrated, same recipe as workload 4."""
-    net = retinanet_r50_net(n, h, w, bits, heads=True)
+    3-bit networks, Tables 2 and 4), calibrated, same recipe as workload 4;
+    io_bits=8: the fully quantized network (8-bit image, stem and
+    prediction convolutions, max-pooling)."""
+    net = retinanet_r50_net(n, h, w, bits, heads=True, io_bits=io_bits)
     return net, make_params(net, seed, "calibrated")
 
 

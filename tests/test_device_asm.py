@@ -46,7 +46,7 @@ def device_asm(tmp_path_factory):
 
 @pytest.fixture(scope="module")
 def fp4_asm(device_asm):
-    return device_asm["qconv_fp4.hip"][1]
+    return device_asm["qconv_b16.hip"][1]
 
 
 def test_no_kernel_uses_scratch(device_asm):

@@ -79,3 +79,29 @@ def test_fcos_wiring():
     towers = [c for c in net.convs if ".t" in c.name]
     assert len(towers) == 8 and all(c.cin == c.cout == 256 and len(c.segs) == 5 for c in towers)
     assert len(net.outputs) == 15 and len(net.convs) == 60 + 11
+
+
+def test_fully_quantized_retinanet_wiring():
+    """The network of the paper's AQD rows (Sec. 4): an 8-bit 3-channel image,
+    the 7x7 stride-2 stem with 8-bit two's-complement weights and 4-bit
+    outputs, 3x3 stride-2 max-pooling to the backbone's input, 4-bit layers
+    elsewhere, and 8-bit prediction convolutions fed by 8-bit tower outputs."""
+    net = W.retinanet_r50_net(2, 800, 1333, 4, io_bits=8)
+    stem, pool = net.convs[0], net.convs[1]
+    assert net.inputs == ["img"] and net.tensors["img"].shape == (2, 800, 1333, 3)
+    assert net.tensors["img"].bits == 8
+    assert (stem.op, stem.k, stem.stride, stem.bits_w, stem.wenc) == ("conv", 7, 2, 8, W.WENC_TWOS)
+    assert net.tensors["c1"].shape == (2, 400, 667, 64) and net.tensors["c1"].bits == 4
+    assert (pool.op, pool.k, pool.stride, pool.pad) == ("maxpool", 3, 2, 1)
+    assert net.tensors["c2in"].shape == (2, 200, 334, 64) and net.tensors["c2in"].bits == 4
+    assert net.macs(pool) == 0
+    for tower in ("cls", "box"):
+        t4 = next(c for c in net.convs if c.name == f"{tower}.t4")
+        pred = next(c for c in net.convs if c.name == f"{tower}.pred")
+        assert all(net.tensors[y].bits == 8 for _, _, y in t4.segs)
+        assert pred.bits_w == 8 and pred.wenc == W.WENC_TWOS
+        assert all(net.tensors[x].bits == 8 and net.tensors[y].bits == 32 for x, _, y in pred.segs)
+    rest = [c for c in net.convs[2:] if not c.name.endswith((".t4", ".pred"))]
+    assert all(c.bits_w == 4 and net.tensors[c.segs[0][2]].bits in (4, 32) for c in rest)
+    params = W.make_params(net, 1, "calibrated")
+    assert "pool" not in params.weights and params.weights["stem"].shape == (64, 7, 7, 3)
