@@ -35,7 +35,7 @@ enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
        // 8-bit codes, cin a multiple of 128, int32 outputs: 256 x 128 tiles on
        // the int8 MFMA (qconv_b16.hip), weights in channel order at create
        TILE_B8 = 13,
-       // the 7x7 stride-2 stem on a 3-channel 8-bit image: 64 x 256 tiles, K =
+       // the 7x7 stride-2 stem on a 3-channel 8-bit image: 64 x 128 tiles, K =
        // the whole window (qconv_stem.hip)
        TILE_STEM = 14 };
 constexpr int KC = 64;

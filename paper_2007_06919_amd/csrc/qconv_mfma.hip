@@ -1101,7 +1101,7 @@ void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane)
     case TILE_WV: *blk_co = 256; *blk_px = 128; *chan_per_lane = 16; return;
     case TILE_FP4:
     case TILE_B8: *blk_co = 256; *blk_px = 128; *chan_per_lane = 32; return;
-    case TILE_STEM: *blk_co = 64; *blk_px = 256; *chan_per_lane = 16; return;
+    case TILE_STEM: *blk_co = 64; *blk_px = 128; *chan_per_lane = 16; return;
     case TILE_256x64S:
     case TILE_256x64:
     case TILE_STREAM: *blk_co = 256; *blk_px = 64; *chan_per_lane = 32; return;
