@@ -134,10 +134,20 @@ typedef struct qconv_s *qconv_t;
  * w_packed: host, [cout][kh][kw][cin] b-bit weight fields packed along cin
  *           (the code tensor layout above with bits_w).
  * levels:   host array of desc->num_levels epilogue tables.
+ * The arithmetic is fixed here (qconv_path): the matrix cores take 2/3/4-bit
+ * codes with cin a multiple of 64 and weights that fit int8 (code outputs of
+ * the input's width, or 8-bit code outputs of 4-bit layers with cin a
+ * multiple of 256 and cout >= 256); 2-bit codes with 2-bit weights and cin,
+ * cout multiples of 256 take the FP4 matrix cores; 8-bit codes with cin a
+ * multiple of 128 and int32 outputs, and the 7x7 stride-2 pad-3 stem on 3
+ * channels of 8-bit codes (4-bit or int32 outputs), take the int8 matrix
+ * cores on codes re-centred by -128, the handle's bias carrying
+ * 128 * sum(w); every other description runs on the direct kernel.
  * On success *out receives the handle. Errors: INVALID (bad description,
  * NULL pointers, parameter out of range), UNSUPPORTED (accumulator bound
- * K * (2^bits_in - 1) * max|w| >= 2^31, or 8-bit odd-grid weights),
- * NOMEM / DEVICE (device allocation or copy failed; nothing is leaked). */
+ * K * (2^bits_in - 1) * max|w| >= 2^31, 8-bit odd-grid weights, or a
+ * re-centred bias outside int32), NOMEM / DEVICE (device allocation or copy
+ * failed; nothing is leaked). */
 aqd_status_t qconv_create(const qconv_desc_t *desc, const uint8_t *w_packed,
                           const qconv_epilogue_t *levels, qconv_t *out);
 
