@@ -623,8 +623,14 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
             t128 += ((long long)segs[i].n * chk[i].ho * chk[i].wo + 127) / 128 * h0.co_tiles;
         const bool short_codes = h0.ksteps <= 4 && h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_in == 4 &&
                                  h0.d.bits_out == 4 && (h0.d.skip_bits == 0 || h0.d.skip_bits == 4);
+        // the register-fed kernel addresses each segment's input with 32-bit
+        // buffer offsets
+        bool x_small = true;
+        for (int i = 0; i < count; ++i)
+            x_small = x_small && chk[i].xbytes < (1ull << 31);
         if (h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_out == 8) {
             // 8-bit code outputs: only the register-fed kernel writes them
+            REQUIRE(x_small, "8-bit code outputs take inputs of less than 2^31 bytes per segment");
             tile_cfg = TILE_WV;
         } else if (short_codes && h0.ksteps <= 2 && h0.d.kh == 1 && h0.d.kw == 1 && h0.d.pad == 0 &&
                    h0.d.cout % 256 == 0) {
@@ -646,7 +652,7 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         } else if (h0.d.bits_in == 4 && h0.d.cin % 256 == 0 &&
                    (h0.d.out_mode == AQD_OUT_CODES ? (h0.d.skip_bits == 0 || h0.d.skip_bits == 4)
                                                    : h0.d.skip_bits == 0) &&
-                   t128 >= 200) {
+                   t128 >= 200 && x_small) {
             // 256-channel input chunks: weights read into registers (no LDS
             // traffic for them), activation codes staged in LDS four K steps
             // at a time

@@ -1,6 +1,7 @@
 // Device helpers shared by the MFMA convolution kernels: compile-time loops,
 // the 32-bit forms of the integer epilogue's rounding steps, LDS swizzles and
-// addressing, the LDS-DMA copy, and packed-word loads and stores.
+// addressing, the LDS-DMA copy, raw buffer loads, and packed-word loads and
+// stores.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -26,6 +27,22 @@ __device__ __forceinline__ void static_for(F &&f)
 }
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+
+// Raw buffer loads (buffer_load_dwordx4 ... offen): 16 bytes at byte offset
+// voff + soff of the resource's base. The hardware checks the offset against
+// the resource's size and returns zeros for an access at or past it (no
+// memory is touched), which the kernels use for padding taps and look-ahead
+// past the last K step. Word 3 of the descriptor: 32-bit data format, as a
+// raw (untyped) buffer on gfx9-family GPUs needs.
+typedef __amdgpu_buffer_rsrc_t buf_rsrc;
+__device__ __forceinline__ buf_rsrc make_rsrc(const void *p, int bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, bytes, 0x00020000);
+}
+__device__ __forceinline__ v4i load_b128(buf_rsrc r, int voff, int soff)
+{
+    return (v4i)__builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
 
 
 // round(a * c / 2^d), ties up, d in [0, 31], result modulo 2^32: one 64-bit

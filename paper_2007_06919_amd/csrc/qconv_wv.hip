@@ -83,25 +83,34 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
     const int hw = S.ho * S.wo;
 
     // ---- activation copies: piece m of a stage = pixels 32m .. 32m+31 of the
-    // tile, lane tid copying 16-byte chunk tid % 8 of pixel 32m + tid / 8
+    // tile, lane tid copying 16-byte chunk tid % 8 of pixel 32m + tid / 8.
+    // Buffer loads: a tap in the padding, a pixel past the end and a stage
+    // past the last read at an offset past the buffer's size and get zeros
+    // (code 0), with no branch and no mask on the data.
     const int c16 = tid & 7;
-    // per piece: first input row/column of the output pixel's window (a row
-    // far outside the image for pixels past the end) and the image's first
-    // pixel (n * h * w < 2^31, checked on the host)
-    // (pixel indices fit in 32 bits: n * ho * wo < 2^31, checked on the host)
-    int ih0[4], iw0[4], xpix[4];
+    // per piece: the byte offset of its pixel's window origin (negative at the
+    // top and left borders) and which window rows (bit t) and columns (bit
+    // 16 + t) lie inside the image (none for pixels past the end); the input
+    // holds n * h * w * row_bytes < 2^31 bytes (checked on the host)
+    int xbase[4];
+    uint32_t xvalid[4];
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
         const unsigned p = (unsigned)(px_tile * WV_BPX + 32 * m + (tid >> 3));
         const bool ok = p < (unsigned)S.P;
         const unsigned pn = ok ? p / (unsigned)hw : 0u;
         const unsigned prem = ok ? p - pn * (unsigned)hw : 0u;
-        const unsigned oh = prem / (unsigned)S.wo, ow = prem - oh * (unsigned)S.wo;
-        ih0[m] = ok ? (int)oh * A.stride - A.pad : -(1 << 30);
-        iw0[m] = (int)ow * A.stride - A.pad;
-        xpix[m] = (int)pn * S.h * S.w;
+        const int oh = (int)(prem / (unsigned)S.wo), ow = (int)prem - oh * S.wo;
+        const int ih0 = oh * A.stride - A.pad, iw0 = ow * A.stride - A.pad;
+        uint32_t v = 0;
+        for (int t = 0; t < A.kh; ++t)
+            v |= ((unsigned)(ih0 + t) < (unsigned)S.h ? 1u : 0u) << t;
+        for (int t = 0; t < A.kw; ++t)
+            v |= ((unsigned)(iw0 + t) < (unsigned)S.w ? 1u : 0u) << (16 + t);
+        xvalid[m] = ok ? v : 0u;
+        xbase[m] = (((int)pn * S.h + ih0) * S.w + iw0) * row_bytes + 16 * c16;
     }
-    const uint8_t *xsrc = S.x + 16 * c16;
+    const buf_rsrc xr = make_rsrc(S.x, S.n * S.h * S.w * row_bytes);
     // LDS byte offsets: eight-byte column c of pixel p at 128 p + 8 (c ^ (p & 15))
     const int wp = tid >> 3;                      // pixel within a piece (p & 15 == wp & 15)
     const uint32_t wo0 = WV_ROW * wp + 8 * ((2 * c16) ^ (wp & 15));
@@ -109,8 +118,11 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
     // fragment of K step q: pixel 16j + r, eight-byte column 4q + g
     auto ro = [&](int q) -> uint32_t { return WV_ROW * r + 8 * ((4 * q + g) ^ r); };
 
-    // copy state of the stage being loaded: tap (tr, tq), 128-byte chunk th
+    // copy state of the stage being loaded (uniform): tap (tr, tq), 128-byte
+    // chunk th; its byte offset from a window origin and the window bits it needs
     int tr = 0, tq = 0, th = 0;
+    int x_off = 0;
+    uint32_t x_need = 0x10001u;
     auto advance = [&]() {
         if (++th == spt) {
             th = 0;
@@ -119,36 +131,27 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
                 ++tr;
             }
         }
+        x_off = (tr * S.w + tq) * row_bytes + WV_ROW * th;
+        x_need = (1u << tr) | (1u << (16 + tq));
     };
-    // a piece of the stage being loaded, without a branch: taps in the
-    // padding (and pixels past the end, and stages past the last) read a
-    // clamped position inside the image and are masked to code 0
-    auto load_piece = [&](int m) -> uint4 {
-        const int ih = ih0[m] + tr, iw = iw0[m] + tq;
-        const bool in = ((unsigned)ih < (unsigned)S.h) & ((unsigned)iw < (unsigned)S.w);
-        const int ihc = min(max(ih, 0), S.h - 1), iwc = min(max(iw, 0), S.w - 1);
-        const uint4 v = *(const uint4 *)(xsrc + (long long)(xpix[m] + ihc * S.w + iwc) * row_bytes +
-                                         WV_ROW * th);
-        const uint32_t keep = in ? 0xFFFFFFFFu : 0u;
-        return make_uint4(v.x & keep, v.y & keep, v.z & keep, v.w & keep);
+    auto load_piece = [&](int m) -> v4i {
+        const int off = (xvalid[m] & x_need) == x_need ? xbase[m] + x_off : (int)0x80000000;
+        return load_b128(xr, off, 0);
     };
-    auto write_piece = [&](int buf, int m, const uint4 v) {
+    auto write_piece = [&](int buf, int m, const v4i v) {
         uint8_t *base = lds + buf * WV_STAGE + m * (32 * WV_ROW);
-        *(uint2 *)(base + wo0) = make_uint2(v.x, v.y);
-        *(uint2 *)(base + wo1) = make_uint2(v.z, v.w);
+        *(uint2 *)(base + wo0) = make_uint2((uint32_t)v.x, (uint32_t)v.y);
+        *(uint2 *)(base + wo1) = make_uint2((uint32_t)v.z, (uint32_t)v.w);
     };
 
     // ---- weights: this wave's rows of K step k, accumulator tile i at
-    // wa + k * 16 KiB + i * 1 KiB (lane: row r, 16-byte column g; in global
-    // memory the columns are in order, only LDS copies swizzle them); the
-    // look-ahead reads up to three steps past the last (the allocation has
-    // four steps of padding) and those values are never used
-    const int8_t *wa = S.wt + ((long long)co_tile * KS * WV_BCO + 64 * wave + r) * KC + 16 * g;
-    auto load_a = [&](int k, v4i *dst) {
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-            dst[i] = *(const v4i *)(wa + (long long)k * (WV_BCO * KC) + i * 1024);
-    };
+    // k * 16 KiB + i * 1 KiB from the channel tile's first step (lane: row r,
+    // 16-byte column g; in global memory the columns are in order, only LDS
+    // copies swizzle them); the look-ahead past the last step reads past the
+    // buffer's size and gets zeros, which no MFMA uses
+    const buf_rsrc wr = make_rsrc(S.wt + (long long)co_tile * KS * WV_BCO * KC, KS * WV_BCO * KC);
+    const int w_lane = (64 * wave + r) * KC + 16 * g;
+    auto load_w = [&](int k, int i) -> v4i { return load_b128(wr, w_lane + i * 1024, k * (WV_BCO * KC)); };
 
     // ---- accumulators start at the bias (Eq. 6): lane group g of wave w holds
     // channels 128 (w >> 1) + 32 g + 16 (w & 1) + 4 i + e of the tile
@@ -163,26 +166,27 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
             acc[i][j] = b;
     }
 
-    // ---- prologue: stage 0 and pieces 0-1 of stage 1 in LDS (pieces 2 and 3
-    // are written in the first two K steps, as every stage's last two are),
-    // weights of steps 0-2 in registers
-    uint4 rb[4];
+    // ---- prologue: stage 0 and pieces 0-2 of stage 1 in LDS (piece 3 is
+    // written at the end of the first K step, as every stage's last piece
+    // is), weights of steps 0-1 in registers
+    v4i rb[4];
 #pragma unroll
     for (int m = 0; m < 4; ++m)
         write_piece(0, m, load_piece(m));
     advance();
 #pragma unroll
-    for (int m = 0; m < 2; ++m)
+    for (int m = 0; m < 3; ++m)
         write_piece(1, m, load_piece(m));
-    rb[2] = load_piece(2);
     rb[3] = load_piece(3);
-    rb[0] = rb[1] = rb[2];
+    rb[0] = rb[1] = rb[2] = rb[3];
     advance();  // copy state: stage 2
     v4i fa[4][MI];
-    load_a(0, fa[0]);
-    load_a(1, fa[1]);
-    load_a(2, fa[2]);
-    uint2 fb[NJ];   // fragment j of the current step, or of the next one once read ahead
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+        fa[0][i] = load_w(0, i);
+        fa[1][i] = load_w(1, i);
+    }
+    uint2 fb[NJ];   // packed fragment j of the current step, or of the next one once read ahead
 
     auto widen = [](const uint2 w) -> v4i {
         return v4i{(int)(w.x & 0x0F0F0F0Fu), (int)((w.x >> 4) & 0x0F0F0F0Fu),
@@ -193,48 +197,64 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
 #pragma unroll
     for (int j = 0; j < RA; ++j)
         fb[j] = *(const uint2 *)(lds + 2048 * j + ro(0));
+    v4i bw = widen(fb[0]);  // the widened fragment of the next column tile's MFMAs
 
     // ---- main loop, one stage (four K steps) per call: stage g lives in
     // buffer g % 4; during stage g the pieces of stage g + 2 are loaded (one
-    // per K step) and written two K steps later, into the buffer of stage
-    // g - 2. Fragment (k, j) is read during the MFMAs of column tile j - RA of
-    // step k (or of step k - 1). A barrier in the last step, before the first
-    // read of the next stage, makes that stage visible; the barrier of stage
-    // g - 1 orders every wave's reads of stage g - 2 before the writes of
-    // stage g + 2 into its buffer. Loads and writes for stages past the last
-    // go to buffers nobody reads again; the weight look-ahead past the last
-    // step reads the allocation's padding.
+    // per K step, at its start) and written at the end of the next K step
+    // (piece 3 at the end of the first step of stage g + 1), into the buffer
+    // of stage g - 2. The weights of step k + 2 are loaded during the first
+    // four column tiles of step k. Fragment (k, j) is read RA column tiles
+    // ahead (during step k, or k - 1) and widened during the MFMAs of column
+    // tile j - 1. A barrier in the last step, before the first read of the
+    // next stage, makes that stage visible; the barrier of stage g - 1 orders
+    // every wave's reads of stage g - 2 before the writes of stage g + 2 into
+    // its buffer. Loads and writes for stages past the last go to buffers
+    // nobody reads again.
+    // Each column tile is one scheduling region, in the order: MFMA, weight
+    // load, fragment read, then the widening of the next fragment (two
+    // instructions) between each of the other three MFMAs; the VALU work
+    // then issues while the matrix core runs.
     auto stage = [&](const int gs) {
         const int buf = gs & 3;
         static_for<4>([&](auto qc) {
             constexpr int q = decltype(qc)::value;
             const int k = 4 * gs + q;
-            // (a) a piece of stage gs + 2
-            rb[q] = load_piece(q);
-            // (b) weights of step k + 3 (set (q + 3) % 4; step k uses set q)
-            load_a(k + 3, fa[(q + 3) & 3]);
-            // (c) write the piece loaded two steps earlier (at q < 2: pieces 2
-            // and 3 of stage gs + 1, loaded in stage gs - 1 or by the prologue)
-            if constexpr (q >= 2)
-                write_piece((buf + 2) & 3, q - 2, rb[q - 2]);
-            else
-                write_piece((buf + 1) & 3, q + 2, rb[q + 2]);
+            rb[q] = load_piece(q);  // a piece of stage gs + 2
+            __builtin_amdgcn_sched_barrier(0);
             const uint32_t r_this = ro(q) + buf * WV_STAGE;
             const uint32_t r_next = q < 3 ? ro(q + 1) + buf * WV_STAGE : ro(0) + ((buf + 1) & 3) * WV_STAGE;
-            // (d, e) the MFMAs of step k, reading ahead
             static_for<NJ>([&](auto jc) {
                 constexpr int j = decltype(jc)::value;
                 if constexpr (q == 3 && j == NJ - RA)
                     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-                const v4i bj = widen(fb[j]);
+                if constexpr (j < MI)
+                    fa[(q + 2) & 3][j] = load_w(k + 2, j);  // set (q + 2) % 4 was step k - 2's
+                const v4i bn = widen(fb[(j + 1) % NJ]);
 #pragma unroll
                 for (int i = 0; i < MI; ++i)
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[q][i], bj, acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[q][i], bw, acc[i][j], 0, 0, 0);
                 if constexpr (j + RA < NJ)
                     fb[j + RA] = *(const uint2 *)(lds + 2048 * (j + RA) + r_this);
                 else
                     fb[j + RA - NJ] = *(const uint2 *)(lds + 2048 * (j + RA - NJ) + r_next);
+                bw = bn;
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+                __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_barrier(0);
             });
+            // the piece loaded one step earlier (at q = 0: piece 3 of stage gs + 1)
+            if constexpr (q >= 1)
+                write_piece((buf + 2) & 3, q - 1, rb[q - 1]);
+            else
+                write_piece((buf + 1) & 3, 3, rb[3]);
             if constexpr (q == 3)
                 advance();
         });
@@ -444,8 +464,13 @@ hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream)
     const bool codes8 = a.bits_out == 8;
     if ((a.bits_out != 4 && a.bits_out != 8 && a.bits_out != 32) ||
         (a.skip_bits != 0 && (a.skip_bits != 4 || a.bits_out != 4)) || a.cin % 256 != 0 ||
-        a.ksteps % 4 != 0 || a.ksplit != 1 || a.part != 0)
+        a.ksteps % 4 != 0 || a.ksplit != 1 || a.part != 0 || a.kh > 16 || a.kw > 16)
         return hipErrorInvalidValue;
+    // 32-bit buffer offsets and sizes: inputs and weights below 2^31 bytes
+    for (int i = 0; i < a.nseg; ++i)
+        if ((long long)a.seg[i].n * a.seg[i].h * a.seg[i].w * (a.cin / 2) >= (1LL << 31) ||
+            (long long)a.co_tiles * a.ksteps * WV_BCO * KC >= (1LL << 31))
+            return hipErrorInvalidValue;
     dim3 grid(8 * a.tiles_per_xcd), block(256);
     bool fast = true;
     for (int i = 0; i < a.nseg; ++i)
