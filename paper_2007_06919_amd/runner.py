@@ -402,6 +402,16 @@ class Net:
         for k in sorted(tail):
             main.wait_event(tail[k])
 
+    def launch_group(self, gi, stream=None):
+        """Enqueue grouped launch gi alone on the stream, on the tensors the
+        last pass left (it rewrites its outputs with the same values): for
+        timing one launch back to back."""
+        s = self.stream if stream is None else stream
+        for fn, args in self._calls[gi]:
+            st = fn(*args, s.cuda_stream)
+            if st != aqd.AQD_OK:
+                raise aqd.AqdError(st, aqd.last_error())
+
     def capture(self, stream=None):
         """Record one forward pass on the (non-null) stream into a HIP graph;
         replay() then enqueues the whole network as one launch. The recorded
