@@ -40,8 +40,8 @@ B2B_REPS = 10               # back-to-back repeats of each dominant launch (sust
 # COPY_PROBE_BYTES; valid only for the kernel source it was measured on.
 HEAD_KERNEL = "qconv_wv_kernel<0, 0, 1>"
 HEAD_KERNEL_SOURCES = ("qconv_wv.hip", "mfma_common.h")
-HEAD_TRAFFIC = {"kernel_sha256": "79685e33e30d6d92c6c74eda6410e3aa83c28ab4ce9379beb6cbdcd1dc2ab6da",
-                "fetch_bytes": 51022857, "write_bytes": 45670400}
+HEAD_TRAFFIC = {"kernel_sha256": "bdafddde26999011ea1c98e076a647f9e768992b3377d569be65e84243902dd7",
+                "fetch_bytes": 51019467, "write_bytes": 45670400}
 
 
 def kernel_sha256():

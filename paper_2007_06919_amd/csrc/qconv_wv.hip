@@ -11,25 +11,31 @@
 // 64w .. 64w+63 (4 accumulator tiles of 16) for all 128 pixels (8 column
 // tiles of 16), so no two waves share a weight row:
 //  * weights (int8, decoded and tiled at create exactly as for the 256 x 128
-//    kernel) go from global memory (L2) straight into registers, three K
-//    steps ahead of their MFMAs: no LDS traffic for the larger operand;
+//    kernel) go from global memory (L2) straight into registers, two K steps
+//    ahead of their MFMAs, one 16-byte buffer load per column tile during the
+//    first four column tiles of a step: no LDS traffic for the larger operand;
 //  * activation codes (4-bit, packed as stored) go through LDS in stages of
 //    four K steps (one tap's 256 channels, 128 B per pixel: whole cache
-//    lines), a ring of four stages; each lane copies 16 B per K step
-//    through registers, and the copy is written two K steps after its load.
-//    In LDS a pixel row's eight-byte columns are XOR-swizzled with the pixel
-//    index, so that the fragment reads (8 B per lane, 16 pixels per lane
-//    group) and the copies' writes are free of bank conflicts;
+//    lines), a ring of four stages; each lane copies 16 B per K step through
+//    registers: loaded at the start of a step, written at the end of the
+//    next. Buffer loads return zeros past the end of the input, so padding
+//    taps cost no branch and no mask. In LDS a pixel row's eight-byte columns
+//    are XOR-swizzled with the pixel index, so that the fragment reads (8 B
+//    per lane, 16 pixels per lane group) and the copies' writes are free of
+//    bank conflicts;
 //  * one barrier per stage (four K steps);
+//  * each column tile is one scheduling region: its 4 MFMAs with the widening
+//    of the next column's fragment (mask/shift of the packed codes to int8, in
+//    the byte order the weights were stored in at create) between them, so
+//    that the VALU work issues while the matrix core runs;
 //  * the channel tile's epilogue table is fetched before the last stage.
-// The packed codes are widened to int8 in registers (mask/shift), in the
-// byte order the weights were stored in at create.
 //
 // Epilogue (Sec. 3.2.2-3.2.3, Eq. 6-8, and Eq. 2 on integers): the
 // accumulators start at the folded bias; a lane holds 16 consecutive channels
-// of 8 pixels and packs their requantised codes into 8-byte stores. The LDS
-// ring holds the channel tile's epilogue table and the side-0 skip table
-// after the last K step.
+// of 8 pixels and packs their requantised codes. The LDS ring holds the
+// channel tile's epilogue table and the side-0 skip table after the last K
+// step, then the tile's packed codes, which leave as 16-byte chunks of
+// contiguous pixel rows (a partial channel tile stores from registers).
 
 #include "epilogue.h"
 #include "internal.h"
@@ -446,6 +452,35 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
 #pragma unroll
         for (int o = 0; o < OW; ++o)
             asm volatile("" : "+v"(outw[j][o]));
+    // a whole channel tile's codes go through LDS (free again once every wave
+    // has read its tables) and out as 16-byte chunks of contiguous pixel rows
+    constexpr int ROWB = WV_BCO * BO / 8;         // bytes of a pixel's 256 channels
+    constexpr int CPR = ROWB / 16;                // 16-byte chunks per row (8 or 16)
+    if (A.cout - co_tile * WV_BCO >= WV_BCO) {
+        __syncthreads();
+        const int c0 = co_loc * BO / 8;           // this lane's byte offset in a row
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int p = 16 * j + r;
+            uint8_t *d = lds + p * ROWB + 16 * ((c0 >> 4) ^ (p & (CPR - 1))) + (c0 & 8);
+            if constexpr (BO == 8)
+                *(uint4 *)d = make_uint4(outw[j][0], outw[j][1], outw[j][2], outw[j][3]);
+            else
+                *(uint2 *)d = make_uint2(outw[j][0], outw[j][1]);
+        }
+        __syncthreads();
+        const long long rowg = (long long)A.cout * BO / 8;
+#pragma unroll
+        for (int it = 0; it < WV_BPX * CPR / 256; ++it) {
+            const int idx = it * 256 + tid;
+            const int p = idx / CPR, c = idx % CPR;
+            const long long px = (long long)px_tile * WV_BPX + p;
+            if (px < S.P)
+                *(uint4 *)((uint8_t *)S.y + px * rowg + co_tile * ROWB + 16 * c) =
+                    *(const uint4 *)(lds + p * ROWB + 16 * (c ^ (p & (CPR - 1))));
+        }
+        return;
+    }
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
         if (okj[j]) {
