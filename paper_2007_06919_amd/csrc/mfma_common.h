@@ -28,8 +28,8 @@ __device__ __forceinline__ void static_for(F &&f)
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 
-// Raw buffer loads (buffer_load_dwordx4 ... offen): 16 bytes at byte offset
-// voff + soff of the resource's base. The hardware checks the offset against
+// Raw buffer loads (buffer_load_dwordx4 / _dwordx2 ... offen): 16 or 8 bytes
+// at byte offset voff + soff of the resource's base. The hardware checks the offset against
 // the resource's size and returns zeros for an access at or past it (no
 // memory is touched), which the kernels use for padding taps and look-ahead
 // past the last K step. Word 3 of the descriptor: 32-bit data format, as a
@@ -42,6 +42,12 @@ __device__ __forceinline__ buf_rsrc make_rsrc(const void *p, int bytes)
 __device__ __forceinline__ v4i load_b128(buf_rsrc r, int voff, int soff)
 {
     return (v4i)__builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
+__device__ __forceinline__ uint2 load_b64(buf_rsrc r, int voff, int soff)
+{
+    typedef unsigned v2u __attribute__((ext_vector_type(2)));
+    const v2u v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+    return make_uint2(v.x, v.y);
 }
 
 

@@ -150,32 +150,50 @@ __global__ void __launch_bounds__(256, 2) qconv_b16_kernel(MfmaArgs A)
     // 16c .. 16c+15 (8-bit: channels 16c .. 16c+15) of pixel 32m + tid / 8,
     // c = tid % 8
     const int c8 = tid & 7;
-    int ih0[4], iw0[4], xpix[4];
+    // per piece: the byte offset of its pixel's window origin (negative at the
+    // top and left borders) and which window rows (bit t) and columns (bit
+    // 16 + t) lie inside the image (none for pixels past the end); the input
+    // holds n * h * w * row_bytes < 2^31 bytes (checked on the host)
+    int xbase[4];
+    uint32_t xvalid[4];
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
         const unsigned p = (unsigned)(px_tile * F4_BPX + 32 * m + (tid >> 3));
         const bool ok = p < (unsigned)S.P;
         const unsigned pn = ok ? p / (unsigned)hw : 0u;
         const unsigned prem = ok ? p - pn * (unsigned)hw : 0u;
-        const unsigned oh = prem / (unsigned)S.wo, ow = prem - oh * (unsigned)S.wo;
-        ih0[m] = ok ? (int)oh * A.stride - A.pad : -(1 << 30);
-        iw0[m] = (int)ow * A.stride - A.pad;
-        xpix[m] = (int)pn * S.h * S.w;   // n * h * w < 2^31, checked on the host
+        const int oh = (int)(prem / (unsigned)S.wo), ow = (int)prem - oh * S.wo;
+        const int ih0 = oh * A.stride - A.pad, iw0 = ow * A.stride - A.pad;
+        uint32_t v = 0;
+        for (int t = 0; t < A.kh; ++t)
+            v |= ((unsigned)(ih0 + t) < (unsigned)S.h ? 1u : 0u) << t;
+        for (int t = 0; t < A.kw; ++t)
+            v |= ((unsigned)(iw0 + t) < (unsigned)S.w ? 1u : 0u) << (16 + t);
+        xvalid[m] = ok ? v : 0u;
+        xbase[m] = (((int)pn * S.h + ih0) * S.w + iw0) * row_bytes + (FP4 ? 8 : 16) * c8;
     }
-    const uint8_t *xsrc = S.x + (FP4 ? 8 : 16) * c8;
+    const buf_rsrc xr = make_rsrc(S.x, S.n * S.h * S.w * row_bytes);
     // LDS: 16-byte column c of pixel p at 128 p + 16 (c ^ (p & 7))
     const int wp = tid >> 3;
     const uint32_t wofs = F4_ROW * wp + 16 * (c8 ^ (wp & 7));
     // fragment of K step q of a stage: pixel 16j + r, column 4q + g
     auto ro = [&](int q) -> uint32_t { return F4_ROW * r + 16 * ((4 * q + g) ^ (r & 7)); };
 
-    // copy state of the stage being loaded: tap (tr, tq), 256-channel chunk th
+    // copy state of the stage being loaded (uniform): tap (tr, tq), SCH-channel
+    // chunk th; its byte offset from a window origin and the window bits it needs
     int th = st0 % spt, tr, tq;
     {
         const int tap = st0 / spt;
         tr = tap / A.kw;
         tq = tap - tr * A.kw;
     }
+    int x_off = 0;
+    uint32_t x_need = 0;
+    auto set_copy = [&]() {
+        x_off = (tr * S.w + tq) * row_bytes + (SCH * CB / 8) * th;
+        x_need = (1u << tr) | (1u << (16 + tq));
+    };
+    set_copy();
     auto advance = [&]() {
         if (++th == spt) {
             th = 0;
@@ -184,22 +202,18 @@ __global__ void __launch_bounds__(256, 2) qconv_b16_kernel(MfmaArgs A)
                 ++tr;
             }
         }
+        set_copy();
     };
-    // taps in the padding, pixels past the end and stages past the last read a
-    // clamped position inside the image and are masked to code 0
+    // buffer loads: taps in the padding, pixels past the end and stages past
+    // the last read past the end of the input and get zeros (code 0)
     using piece_t = typename std::conditional<FP4, uint2, uint4>::type;
     auto load_piece = [&](int m) -> piece_t {
-        const int ih = ih0[m] + tr, iw = iw0[m] + tq;
-        const bool in = ((unsigned)ih < (unsigned)S.h) & ((unsigned)iw < (unsigned)S.w);
-        const int ihc = min(max(ih, 0), S.h - 1), iwc = min(max(iw, 0), S.w - 1);
-        const uint8_t *src = xsrc + (long long)(xpix[m] + ihc * S.w + iwc) * row_bytes + (SCH * CB / 8) * th;
-        const uint32_t keep = in ? 0xFFFFFFFFu : 0u;
+        const int off = (xvalid[m] & x_need) == x_need ? xbase[m] + x_off : (int)0x80000000;
         if constexpr (FP4) {
-            const uint2 v = *(const uint2 *)src;
-            return make_uint2(v.x & keep, v.y & keep);
+            return load_b64(xr, off, 0);
         } else {
-            const uint4 v = *(const uint4 *)src;
-            return make_uint4(v.x & keep, v.y & keep, v.z & keep, v.w & keep);
+            const v4i v = load_b128(xr, off, 0);
+            return make_uint4((uint32_t)v.x, (uint32_t)v.y, (uint32_t)v.z, (uint32_t)v.w);
         }
     };
     // 2-bit: 32 packed codes -> 32 nibbles, word 2h holding the even channels
@@ -215,15 +229,17 @@ __global__ void __launch_bounds__(256, 2) qconv_b16_kernel(MfmaArgs A)
     };
 
     // ---- weights: this wave's rows of K step k, accumulator tile i at
-    // wa + k * 16 KiB + i * 1 KiB (lane: row r, 16-byte column g); the
-    // look-ahead reads up to three steps past the part's last (inside the tile
-    // range or the allocation's four steps of padding), never used
-    const int8_t *wa = S.wt + ((long long)co_tile * KSK * F4_BCO + 64 * wave + r) * F4_KROW + 16 * g;
+    // k * 16 KiB + i * 1 KiB from the channel tile's first step (lane: row r,
+    // 16-byte column g); the look-ahead reads up to three steps past the
+    // part's last (inside the tile range, or past the buffer's size: zeros),
+    // never used
+    const buf_rsrc wr = make_rsrc(S.wt + (long long)co_tile * KSK * F4_BCO * F4_KROW, KSK * F4_BCO * F4_KROW);
+    const int w_lane = (64 * wave + r) * F4_KROW + 16 * g;
     const int k0 = 2 * st0;
     auto load_a = [&](int k, v4i *dst) {
 #pragma unroll
         for (int i = 0; i < MI; ++i)
-            dst[i] = *(const v4i *)(wa + (long long)(k0 + k) * (F4_BCO * F4_KROW) + i * 1024);
+            dst[i] = load_b128(wr, w_lane + i * 1024, (k0 + k) * (F4_BCO * F4_KROW));
     };
 
     // lane group g of wave w holds channels 128 (w >> 1) + 32 g + 16 (w & 1) + 4 i + e
@@ -485,8 +501,13 @@ __global__ void __launch_bounds__(256, 2) qconv_b16_kernel(MfmaArgs A)
 hipError_t launch_qconv_b16(int code_bits, const MfmaArgs &a, hipStream_t stream)
 {
     dim3 grid(8 * a.tiles_per_xcd), block(256);
-    if (a.part == 0 && a.ksplit != 1)
+    if ((a.part == 0 && a.ksplit != 1) || a.kh > 16 || a.kw > 16)
         return hipErrorInvalidValue;
+    // 32-bit buffer offsets and sizes: inputs and weights below 2^31 bytes
+    for (int i = 0; i < a.nseg; ++i)
+        if ((long long)a.seg[i].n * a.seg[i].h * a.seg[i].w * a.cin * code_bits / 8 >= (1LL << 31) ||
+            (long long)a.co_tiles * (2 * (a.ksteps / (code_bits == 2 ? 4 : 2))) * F4_BCO * F4_KROW >= (1LL << 31))
+            return hipErrorInvalidValue;
     if (code_bits == 8) {
         // int32 outputs (or split parts); a partial last channel tile
         if (a.bits_out != 32 || a.skip_bits != 0 || a.cin % 128 != 0 || a.co_tiles * F4_BCO < a.cout ||
