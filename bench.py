@@ -306,6 +306,18 @@ def main():
         torch.cuda.synchronize()
         wall = time.perf_counter() - wall0
         log(f"[bench] {args.steps} timed replays done")
+        # the dominant launches again, each B2B_REPS times back to back between
+        # two events on the launch stream (sustained load); before the
+        # launch-by-launch pass, so that a kernel trace ends with that pass
+        b0 = torch.cuda.Event(enable_timing=True)
+        b1 = torch.cuda.Event(enable_timing=True)
+        b0.record(stream)
+        for gi in dominant:
+            for _ in range(B2B_REPS):
+                gpu.launch_group(gi, stream)
+        b1.record(stream)
+        stream.synchronize()
+        torch.cuda.synchronize()
         # the same steps launch by launch on one stream (no overlap), with
         # events on the launch stream around every grouped launch
         e0 = torch.cuda.Event(enable_timing=True)
@@ -314,17 +326,6 @@ def main():
         for _ in range(args.steps):
             gpu.forward(stream, launch_hook=hook, serial=True)
         e1.record(stream)
-        stream.synchronize()
-        torch.cuda.synchronize()
-        # the dominant launches again, each B2B_REPS times back to back between
-        # two events on the launch stream (sustained load)
-        b0 = torch.cuda.Event(enable_timing=True)
-        b1 = torch.cuda.Event(enable_timing=True)
-        b0.record(stream)
-        for gi in dominant:
-            for _ in range(B2B_REPS):
-                gpu.launch_group(gi, stream)
-        b1.record(stream)
         stream.synchronize()
         torch.cuda.synchronize()
     step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]

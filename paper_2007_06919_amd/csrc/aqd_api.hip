@@ -614,6 +614,13 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
     // splitting K is the better cure) on 256 x 64 tiles two to a CU (measured:
     // from ~260 tiles on, the larger tile is faster)
     int tile_cfg = h0.tile_cfg, blk_px = h0.blk_px;
+    // the register-fed, FP4 and 8-bit kernels address each segment's input
+    // with 32-bit buffer offsets
+    bool x_small = true;
+    for (int i = 0; i < count; ++i)
+        x_small = x_small && chk[i].xbytes < (1ull << 31);
+    REQUIRE(x_small || (tile_cfg != TILE_FP4 && tile_cfg != TILE_B8),
+            "2-bit (FP4) and 8-bit MFMA layers take inputs of less than 2^31 bytes per segment");
     long long t_handle = 0;  // tiles at the handle's own tile shape
     for (int i = 0; i < count; ++i)
         t_handle += ((long long)segs[i].n * chk[i].ho * chk[i].wo + h0.blk_px - 1) / h0.blk_px * h0.co_tiles;
@@ -623,11 +630,6 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
             t128 += ((long long)segs[i].n * chk[i].ho * chk[i].wo + 127) / 128 * h0.co_tiles;
         const bool short_codes = h0.ksteps <= 4 && h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_in == 4 &&
                                  h0.d.bits_out == 4 && (h0.d.skip_bits == 0 || h0.d.skip_bits == 4);
-        // the register-fed kernel addresses each segment's input with 32-bit
-        // buffer offsets
-        bool x_small = true;
-        for (int i = 0; i < count; ++i)
-            x_small = x_small && chk[i].xbytes < (1ull << 31);
         if (h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_out == 8) {
             // 8-bit code outputs: only the register-fed kernel writes them
             REQUIRE(x_small, "8-bit code outputs take inputs of less than 2^31 bytes per segment");
@@ -670,6 +672,21 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
                h0.d.skip_bits == 0 && (h0.d.out_mode == AQD_OUT_INT32 || h0.d.bits_out == 4)) {
         tile_cfg = h0.tile_cfg == TILE_128x256 ? TILE_128x128_O3 : TILE_64x256_O3;
         blk_px = h0.tile_cfg == TILE_128x256 ? 128 : 256;
+    }
+    if (tile_cfg == TILE_WV && h0.d.out_mode == AQD_OUT_CODES) {
+        // a little above one round of 256 x 128 tiles at one workgroup per CU
+        // (the CUs that get a second tile set the launch's time): 256 x 144
+        // tiles, one round
+        long long t128 = 0, t144 = 0;
+        for (int i = 0; i < count; ++i) {
+            const long long p = (long long)segs[i].n * chk[i].ho * chk[i].wo;
+            t128 += (p + 127) / 128 * h0.co_tiles;
+            t144 += (p + 143) / 144 * h0.co_tiles;
+        }
+        if (t128 > 256 && t144 <= 256) {
+            tile_cfg = TILE_WV144;
+            blk_px = 144;
+        }
     }
     // the half view splits each 256-channel tile in two
     const int co_tiles = tile_cfg == TILE_STREAM_H128 ? 2 * h0.co_tiles : h0.co_tiles;
@@ -735,7 +752,7 @@ void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
 {
     if (a.tile_cfg == TILE_256x64S || a.tile_cfg == TILE_256x64 || a.tile_cfg == TILE_STREAM ||
         a.tile_cfg == TILE_STREAM_C128 || a.tile_cfg == TILE_STREAM_C64 || a.tile_cfg == TILE_128x128_O3 ||
-        a.tile_cfg == TILE_64x256_O3 || a.tile_cfg == TILE_STREAM_H128 || a.tile_cfg == TILE_WV ||
+        a.tile_cfg == TILE_64x256_O3 || a.tile_cfg == TILE_STREAM_H128 || a.tile_cfg == TILE_WV || a.tile_cfg == TILE_WV144 ||
         a.tile_cfg == TILE_STEM) {  // never split
         *nparts = 1;
         *kchunk = a.ksteps;

@@ -37,7 +37,10 @@ enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
        TILE_B8 = 13,
        // the 7x7 stride-2 stem on a 3-channel 8-bit image: 64 x 128 tiles, K =
        // the whole window (qconv_stem.hip)
-       TILE_STEM = 14 };
+       TILE_STEM = 14,
+       // TILE_WV's kernel on 256 x 144 tiles, one workgroup per CU: code
+       // outputs of launches a little above one round of 256 x 128 tiles
+       TILE_WV144 = 15 };
 constexpr int KC = 64;
 
 // tile shape of a configuration, and the channels one lane holds per pixel

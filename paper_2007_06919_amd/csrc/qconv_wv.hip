@@ -45,20 +45,25 @@ namespace aqd {
 namespace {
 
 constexpr int WV_BCO = 256;              // channels per workgroup tile
-constexpr int WV_BPX = 128;              // pixels per workgroup tile
 constexpr int WV_ROW = 128;              // bytes of one stage per pixel (256 codes of 4 bits)
-constexpr int WV_STAGE = WV_BPX * WV_ROW;  // 16 KiB
 constexpr int WV_NBUF = 4;
-constexpr int WV_LDS = WV_NBUF * WV_STAGE;
 
 // OUTK: 0 = 4-bit codes, 1 = int32 v = acc + bias (then SKK = 0), 2 = 8-bit
 // codes (the last tower layer of the fully quantized heads; then SKK = 0);
-// SKK: 0 = no skip, 1 = code skip (4-bit); FAST: every shift >= 2 (32-bit requantisation)
-template <int OUTK, int SKK, int FAST>
-__global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
+// SKK: 0 = no skip, 1 = code skip (4-bit); FAST: every shift >= 2 (32-bit
+// requantisation); NJ: column tiles of 16 pixels, 8 (256 x 128 tiles, two
+// workgroups per CU) or 9 (256 x 144 tiles, one per CU: launches a little
+// above one round of the smaller tile fit in one round; code outputs only)
+template <int OUTK, int SKK, int FAST, int NJ>
+__global__ void __launch_bounds__(256, NJ == 8 ? 2 : 1) qconv_wv_kernel(MfmaArgs A)
 {
     static_assert(OUTK == 0 || SKK == 0, "int32 and 8-bit outputs have no skip");
-    constexpr int BI = 4, MI = 4, NJ = 8;
+    static_assert(NJ == 8 || (NJ == 9 && OUTK != 1), "256 x 144 tiles: code outputs");
+    constexpr int BI = 4, MI = 4;
+    constexpr int WV_BPX = 16 * NJ;                // pixels per workgroup tile
+    constexpr int NPC = (WV_BPX + 31) / 32;        // copy pieces of 32 pixels per stage (4 or 5)
+    constexpr int WV_STAGE = 32 * NPC * WV_ROW;    // 16 or 20 KiB (rows past the tile unused)
+    constexpr int WV_LDS = WV_NBUF * WV_STAGE;
     constexpr int BO = OUTK == 2 ? 8 : 4;          // output code width
     constexpr int QMAX = (1 << BO) - 1, OW = BO / 2;  // words of a lane's 16 channels
     __shared__ __attribute__((aligned(1024))) uint8_t lds[WV_LDS];
@@ -98,12 +103,13 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
     // top and left borders) and which window rows (bit t) and columns (bit
     // 16 + t) lie inside the image (none for pixels past the end); the input
     // holds n * h * w * row_bytes < 2^31 bytes (checked on the host)
-    int xbase[4];
-    uint32_t xvalid[4];
+    int xbase[NPC];
+    uint32_t xvalid[NPC];
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        const unsigned p = (unsigned)(px_tile * WV_BPX + 32 * m + (tid >> 3));
-        const bool ok = p < (unsigned)S.P;
+    for (int m = 0; m < NPC; ++m) {
+        const unsigned pl = (unsigned)(32 * m + (tid >> 3));    // pixel within the tile
+        const unsigned p = (unsigned)(px_tile * WV_BPX) + pl;
+        const bool ok = p < (unsigned)S.P && pl < (unsigned)WV_BPX;
         const unsigned pn = ok ? p / (unsigned)hw : 0u;
         const unsigned prem = ok ? p - pn * (unsigned)hw : 0u;
         const int oh = (int)(prem / (unsigned)S.wo), ow = (int)prem - oh * S.wo;
@@ -172,18 +178,20 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
             acc[i][j] = b;
     }
 
-    // ---- prologue: stage 0 and pieces 0-2 of stage 1 in LDS (piece 3 is
-    // written at the end of the first K step, as every stage's last piece
-    // is), weights of steps 0-1 in registers
-    v4i rb[4];
+    // ---- prologue: stage 0 and pieces 0-2 of stage 1 in LDS (pieces 3 and 4
+    // are written at the end of the first K step, as every stage's last ones
+    // are), weights of steps 0-1 in registers
+    v4i rb[NPC];
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int m = 0; m < NPC; ++m)
         write_piece(0, m, load_piece(m));
     advance();
 #pragma unroll
     for (int m = 0; m < 3; ++m)
         write_piece(1, m, load_piece(m));
-    rb[3] = load_piece(3);
+#pragma unroll
+    for (int m = 3; m < NPC; ++m)
+        rb[m] = load_piece(m);
     rb[0] = rb[1] = rb[2] = rb[3];
     advance();  // copy state: stage 2
     v4i fa[4][MI];
@@ -206,10 +214,10 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
     v4i bw = widen(fb[0]);  // the widened fragment of the next column tile's MFMAs
 
     // ---- main loop, one stage (four K steps) per call: stage g lives in
-    // buffer g % 4; during stage g the pieces of stage g + 2 are loaded (one
-    // per K step, at its start) and written at the end of the next K step
-    // (piece 3 at the end of the first step of stage g + 1), into the buffer
-    // of stage g - 2. The weights of step k + 2 are loaded during the first
+    // buffer g % 4; during stage g the pieces of stage g + 2 are loaded (piece
+    // q at the start of K step q, piece 4 too in the last step) and written at
+    // the end of the next K step (the last step's at the end of the first
+    // step of stage g + 1), into the buffer of stage g - 2. The weights of step k + 2 are loaded during the first
     // four column tiles of step k. Fragment (k, j) is read RA column tiles
     // ahead (during step k, or k - 1) and widened during the MFMAs of column
     // tile j - 1. A barrier in the last step, before the first read of the
@@ -226,7 +234,9 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
         static_for<4>([&](auto qc) {
             constexpr int q = decltype(qc)::value;
             const int k = 4 * gs + q;
-            rb[q] = load_piece(q);  // a piece of stage gs + 2
+            rb[q] = load_piece(q);  // pieces of stage gs + 2
+            if constexpr (q == 3 && NPC == 5)
+                rb[4] = load_piece(4);
             __builtin_amdgcn_sched_barrier(0);
             const uint32_t r_this = ro(q) + buf * WV_STAGE;
             const uint32_t r_next = q < 3 ? ro(q + 1) + buf * WV_STAGE : ro(0) + ((buf + 1) & 3) * WV_STAGE;
@@ -256,11 +266,15 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                 __builtin_amdgcn_sched_barrier(0);
             });
-            // the piece loaded one step earlier (at q = 0: piece 3 of stage gs + 1)
-            if constexpr (q >= 1)
+            // the pieces loaded one step earlier (at q = 0: the last ones of
+            // stage gs + 1)
+            if constexpr (q >= 1) {
                 write_piece((buf + 2) & 3, q - 1, rb[q - 1]);
-            else
-                write_piece((buf + 1) & 3, 3, rb[3]);
+            } else {
+#pragma unroll
+                for (int m = 3; m < NPC; ++m)
+                    write_piece((buf + 1) & 3, m, rb[m]);
+            }
             if constexpr (q == 3)
                 advance();
         });
@@ -268,17 +282,20 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
     for (int gs = 0; gs < NST - 1; ++gs)
         stage(gs);
     // the channel tile's epilogue table does not depend on the accumulators:
-    // its loads are issued before the last stage, whose MFMAs hide their latency
+    // its loads are issued before the last stage, whose MFMAs hide their
+    // latency
     constexpr int PRM_PER = EPI_FIELDS * WV_BCO / 256;
     int prm_r[PRM_PER];
-    if constexpr (OUTK != 1) {
+    auto load_prm = [&]() {
 #pragma unroll
         for (int t = 0; t < PRM_PER; ++t) {
             const int i = tid + 256 * t;
             const int which = i / WV_BCO, c = i - which * WV_BCO;
             prm_r[t] = S.epi[which * A.cout_pad + co_tile * WV_BCO + c];
         }
-    }
+    };
+    if constexpr (OUTK != 1)
+        load_prm();
     stage(NST - 1);
 
     if constexpr (OUTK == 1) {
@@ -471,11 +488,11 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
         __syncthreads();
         const long long rowg = (long long)A.cout * BO / 8;
 #pragma unroll
-        for (int it = 0; it < WV_BPX * CPR / 256; ++it) {
+        for (int it = 0; it < (WV_BPX * CPR + 255) / 256; ++it) {
             const int idx = it * 256 + tid;
             const int p = idx / CPR, c = idx % CPR;
             const long long px = (long long)px_tile * WV_BPX + p;
-            if (px < S.P)
+            if (px < S.P && p < WV_BPX)
                 *(uint4 *)((uint8_t *)S.y + px * rowg + co_tile * ROWB + 16 * c) =
                     *(const uint4 *)(lds + p * ROWB + 16 * (c ^ (p & (CPR - 1))));
         }
@@ -492,12 +509,40 @@ __global__ void __launch_bounds__(256, 2) qconv_wv_kernel(MfmaArgs A)
         }
 }
 
+template <int NJ>
+void launch_wv_modes(const MfmaArgs &a, bool fast, dim3 grid, hipStream_t stream)
+{
+    const dim3 block(256);
+    if constexpr (NJ == 8) {
+        if (a.bits_out == 32) {
+            hipLaunchKernelGGL((qconv_wv_kernel<1, 0, 1, NJ>), grid, block, 0, stream, a);
+            return;
+        }
+    }
+    if (a.bits_out == 8) {
+        if (fast)
+            hipLaunchKernelGGL((qconv_wv_kernel<2, 0, 1, NJ>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_wv_kernel<2, 0, 0, NJ>), grid, block, 0, stream, a);
+    } else if (a.skip_bits == 0) {
+        if (fast)
+            hipLaunchKernelGGL((qconv_wv_kernel<0, 0, 1, NJ>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_wv_kernel<0, 0, 0, NJ>), grid, block, 0, stream, a);
+    } else {
+        if (fast)
+            hipLaunchKernelGGL((qconv_wv_kernel<0, 1, 1, NJ>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv_wv_kernel<0, 1, 0, NJ>), grid, block, 0, stream, a);
+    }
+}
+
 }  // namespace
 
 hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream)
 {
-    const bool codes8 = a.bits_out == 8;
-    if ((a.bits_out != 4 && a.bits_out != 8 && a.bits_out != 32) ||
+    const bool wide = a.tile_cfg == TILE_WV144;
+    if ((a.bits_out != 4 && a.bits_out != 8 && a.bits_out != 32) || (wide && a.bits_out == 32) ||
         (a.skip_bits != 0 && (a.skip_bits != 4 || a.bits_out != 4)) || a.cin % 256 != 0 ||
         a.ksteps % 4 != 0 || a.ksplit != 1 || a.part != 0 || a.kh > 16 || a.kw > 16)
         return hipErrorInvalidValue;
@@ -506,28 +551,14 @@ hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream)
         if ((long long)a.seg[i].n * a.seg[i].h * a.seg[i].w * (a.cin / 2) >= (1LL << 31) ||
             (long long)a.co_tiles * a.ksteps * WV_BCO * KC >= (1LL << 31))
             return hipErrorInvalidValue;
-    dim3 grid(8 * a.tiles_per_xcd), block(256);
+    const dim3 grid(8 * a.tiles_per_xcd);
     bool fast = true;
     for (int i = 0; i < a.nseg; ++i)
         fast = fast && a.seg[i].fast;
-    if (a.bits_out == 32)
-        hipLaunchKernelGGL((qconv_wv_kernel<1, 0, 1>), grid, block, 0, stream, a);
-    else if (codes8) {
-        if (fast)
-            hipLaunchKernelGGL((qconv_wv_kernel<2, 0, 1>), grid, block, 0, stream, a);
-        else
-            hipLaunchKernelGGL((qconv_wv_kernel<2, 0, 0>), grid, block, 0, stream, a);
-    } else if (a.skip_bits == 0) {
-        if (fast)
-            hipLaunchKernelGGL((qconv_wv_kernel<0, 0, 1>), grid, block, 0, stream, a);
-        else
-            hipLaunchKernelGGL((qconv_wv_kernel<0, 0, 0>), grid, block, 0, stream, a);
-    } else {
-        if (fast)
-            hipLaunchKernelGGL((qconv_wv_kernel<0, 1, 1>), grid, block, 0, stream, a);
-        else
-            hipLaunchKernelGGL((qconv_wv_kernel<0, 1, 0>), grid, block, 0, stream, a);
-    }
+    if (wide)
+        launch_wv_modes<9>(a, fast, grid, stream);
+    else
+        launch_wv_modes<8>(a, fast, grid, stream);
     return hipGetLastError();
 }
 

@@ -162,16 +162,23 @@ def test_conv_stream_parity(torch, case, variant):
 
 # cin a multiple of 256, code outputs and at least 200 tiles of 256 x 128:
 # the register-fed kernel (weights read into registers, codes staged in LDS
-# four K steps at a time). The head-tower shape, two and four stages per
-# tap, stride 2, a partial channel tile, code skips with and without the
+# four K steps at a time), on 256 x 144 tiles (one round, one workgroup per
+# CU) where 256 x 128 tiles would be a little above one round, on 256 x 128
+# tiles otherwise. The head-tower shape, two and four stages per tap,
+# stride 2, a partial channel tile, code skips with and without the
 # upsample, 3-bit codes, ragged pixel tails.
 WV_CASES = [
     # (n, h, w, cin, cout, k, stride, bits_in, bits_w, wenc, bits_out, skip_bits, up2)
-    (2, 100, 167, 256, 256, 3, 1, 4, 4, 1, 4, 0, False),    # head-tower shape: 261 tiles
+    (2, 100, 167, 256, 256, 3, 1, 4, 4, 1, 4, 0, False),    # head-tower shape: 261 tiles (232 of 144 px)
     (1, 120, 230, 512, 256, 3, 1, 4, 4, 0, 4, 0, False),    # two stages per tap: 216 tiles
     (1, 150, 181, 1024, 256, 1, 1, 4, 4, 1, 4, 4, True),    # 1x1, four stages per tap, upsampled skip
     (2, 203, 131, 256, 288, 3, 2, 4, 4, 0, 4, 4, False),    # stride 2, a partial channel tile, skip
-    (8, 50, 84, 256, 256, 3, 1, 3, 3, 1, 3, 3, False),      # 3-bit codes and skip, batch 8
+    (8, 50, 84, 256, 256, 3, 1, 3, 3, 1, 3, 3, False),      # 3-bit codes and skip: 263 tiles (234 of 144)
+    (2, 150, 181, 1024, 256, 1, 1, 4, 4, 1, 4, 4, True),    # 425 tiles; upsampled skip
+    (4, 100, 167, 256, 256, 3, 1, 4, 4, 1, 4, 0, False),    # head-tower shape: 522 tiles
+    (5, 203, 131, 256, 288, 3, 2, 4, 4, 0, 4, 4, False),    # stride 2, a partial channel tile, skip
+    (5, 75, 90, 256, 256, 3, 1, 4, 4, 0, 4, 4, False),      # 264 tiles (235 of 144 px), skip
+    (4, 130, 130, 256, 288, 3, 2, 4, 4, 0, 4, 4, False),    # 266 tiles (236 of 144): stride 2, partial channel tile
 ]
 
 

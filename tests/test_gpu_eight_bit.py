@@ -78,6 +78,7 @@ def test_eight_bit_extremes(torch):
 WV8_CASES = [
     # 4-bit codes in, 8-bit codes out (the last tower layer before 8-bit predictions)
     (2, 50, 84, 256, 256, 3, 1),     # head-tower shape
+    (8, 50, 84, 256, 256, 3, 1),     # 263 tiles of 256 x 128: 256 x 144 tiles
     (1, 7, 9, 256, 256, 3, 1),       # one partial tile (a launch far below one round)
     (1, 20, 30, 512, 288, 1, 1),     # 1x1, two stages per tap, a partial channel tile
 ]
