@@ -38,10 +38,10 @@ B2B_REPS = 10               # back-to-back repeats of each dominant launch (sust
 # HBM traffic of one head-tower launch, from two rocprofv3 counter runs
 # (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain copy of
 # COPY_PROBE_BYTES; valid only for the kernel source it was measured on.
-HEAD_KERNEL = "qconv_wv_kernel<0, 0, 1>"
+HEAD_KERNEL = "qconv_wv_kernel<0, 0, 1, 8>"
 HEAD_KERNEL_SOURCES = ("qconv_wv.hip", "mfma_common.h")
-HEAD_TRAFFIC = {"kernel_sha256": "bdafddde26999011ea1c98e076a647f9e768992b3377d569be65e84243902dd7",
-                "fetch_bytes": 51019467, "write_bytes": 45670400}
+HEAD_TRAFFIC = {"kernel_sha256": "a24db71d5424a70e06d95f027780566bb7a03a58484218754b2dbfb5d9497b05",
+                "fetch_bytes": 51036615, "write_bytes": 45670400}
 
 
 def kernel_sha256():
@@ -52,6 +52,43 @@ def kernel_sha256():
         with open(os.path.join(ROOT, "paper_2007_06919_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
+
+
+def measured_peaks(torch, dev):
+    """The ceilings measured on this GPU next to the published figures: the
+    int8 matrix-core rate of a kernel of MFMAs alone (aqd_mfma_probe: two
+    workgroups of 4 waves per CU, operands of 4-bit magnitudes) and the HBM
+    rate of a device-to-device copy of COPY_PROBE_BYTES (read + write)."""
+    from paper_2007_06919_amd import aqd
+    wgs, iters = 2048, 1000
+    out = torch.empty(wgs * 256, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    aqd.mfma_probe(wgs, iters, out, stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(5):
+        aqd.mfma_probe(wgs, iters, out, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    mfma_ms = e0.elapsed_time(e1) / 5
+    mfma_tops = wgs * 4 * iters * 16 * 32768 / (mfma_ms / 1e3) / 1e12
+    src = torch.ones(COPY_PROBE_BYTES, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0.record(stream)
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    copy_ms = e0.elapsed_time(e1) / 5
+    del src, dst, out
+    log(f"[bench] measured ceilings: int8 MFMA {mfma_tops:.0f} TOPS, HBM copy "
+        f"{2 * COPY_PROBE_BYTES / (copy_ms / 1e3) / 1e9:.0f} GB/s")
+    return {"mfma_i8_tops": round(mfma_tops, 1),
+            "hbm_copy_gbs": round(2 * COPY_PROBE_BYTES / (copy_ms / 1e3) / 1e9, 1),
+            "mfma_probe": f"aqd_mfma_probe, {wgs} workgroups x 4 waves x {iters} x 16 MFMAs 16x16x64 i8, "
+                          f"mean of 5 launches",
+            "hbm_probe": f"device copy of {COPY_PROBE_BYTES} bytes (read + write), mean of 5"}
 
 
 def log(*a):
@@ -394,6 +431,8 @@ def main():
         traffic = HEAD_TRAFFIC["fetch_bytes"] + HEAD_TRAFFIC["write_bytes"]
     out["roofline"]["traffic"] = traffic
     gpu.close()
+    out["measured_peaks"] = measured_peaks(torch, dev)
+    out["roofline"]["frac_of_measured_mfma"] = round(achieved / out["measured_peaks"]["mfma_i8_tops"], 4)
     if args.copy_probe:
         src = torch.ones(COPY_PROBE_BYTES, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)

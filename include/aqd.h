@@ -300,6 +300,16 @@ typedef struct {
 aqd_status_t aqd_maxpool_run(const aqd_maxpool_desc_t *desc, const void *x, void *y,
                              aqd_stream_t stream);
 
+/* Diagnostic for measurements (the benchmark's measured ceiling next to the
+ * dense int8 peak figure): launches `workgroups` workgroups of 4 waves,
+ * each wave issuing iters x 16 independent 16x16x64 int8 MFMAs on register
+ * operands of 4-bit magnitudes, nothing else in its loop; every workgroup
+ * writes 256 int32 checksums to out (device, workgroups x 256 entries,
+ * caller-owned). Integer operations per launch: workgroups x 4 x iters x 16
+ * x 32768. Time it with events on `stream`. INVALID for workgroups outside
+ * 1..2^20, iters < 1 or a null out. */
+aqd_status_t aqd_mfma_probe(int workgroups, int iters, int32_t *out, aqd_stream_t stream);
+
 /* Exact per-channel sums of an int32 tensor [rows][c] on the device:
  * sums[ch] += sum_r v[r][ch], sums[c + ch] += sum_r v[r][ch]^2 (int64,
  * accumulated into the caller's zeroed array). These are the statistics a

@@ -87,6 +87,7 @@ def lib():
             "qadd_run": ([POINTER(QaddDesc), vp, vp, vp, POINTER(QaddParams), vp], st),
             "aqd_channel_sums": ([vp, c_int64, i, vp, vp], st),
             "aqd_maxpool_run": ([POINTER(MaxpoolDesc), vp, vp, vp], st),
+            "aqd_mfma_probe": ([i, i, vp, vp], st),
             "aqd_graph_begin": ([vp], st),
             "aqd_graph_end": ([vp, POINTER(c_void_p)], st),
             "aqd_graph_launch": ([vp, vp], st),
@@ -113,7 +114,7 @@ def exported_symbols():
     return ["qconv_create", "qconv_out_shape", "qconv_scales", "qconv_run", "qconv_run_group",
             "qconv_group_workspace", "qconv_run_group_ws", "qconv_run_group_static",
             "qconv_run_proj", "qconv_destroy", "qconv_path",
-            "qadd_run", "aqd_maxpool_run", "aqd_channel_sums", "aqd_graph_begin", "aqd_graph_end",
+            "qadd_run", "aqd_maxpool_run", "aqd_mfma_probe", "aqd_channel_sums", "aqd_graph_begin", "aqd_graph_end",
             "aqd_graph_launch", "aqd_graph_destroy", "aqd_last_error", "aqd_pack_codes",
             "aqd_unpack_codes", "aqd_approx_ratio", "aqd_normalize_multiplier",
             "aqd_bn_stats_from_sums", "aqd_fold_bn", "aqd_skip_params", "aqd_requant_params"]
@@ -256,6 +257,12 @@ def maxpool_run(n, h, w, c, bits, k, stride, pad, x, y, stream=None):
     """Max-pooling of a code tensor (see aqd.h)."""
     d = MaxpoolDesc(n, h, w, c, bits, k, stride, pad)
     _check(lib().aqd_maxpool_run(ctypes.byref(d), _addr(x), _addr(y), _stream(stream)))
+
+
+def mfma_probe(workgroups, iters, out, stream=None):
+    """The matrix-core rate probe (see aqd.h); out: device int32 tensor of
+    workgroups x 256 entries."""
+    _check(lib().aqd_mfma_probe(workgroups, iters, _addr(out), _stream(stream)))
 
 
 def graph_begin(stream):

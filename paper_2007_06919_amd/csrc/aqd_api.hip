@@ -1139,6 +1139,15 @@ aqd_status_t aqd_channel_sums(const int32_t *v, int64_t rows, int c, int64_t *su
     return AQD_OK;
 }
 
+aqd_status_t aqd_mfma_probe(int workgroups, int iters, int32_t *out, aqd_stream_t stream)
+{
+    REQUIRE(workgroups >= 1 && workgroups <= (1 << 20) && iters >= 1, "workgroups in 1..2^20, iters >= 1");
+    REQUIRE(out, "null pointer");
+    if (launch_mfma_probe(workgroups, iters, out, (hipStream_t)stream) != hipSuccess)
+        return fail(AQD_ERR_DEVICE, "probe launch failed");
+    return AQD_OK;
+}
+
 aqd_status_t aqd_maxpool_run(const aqd_maxpool_desc_t *desc, const void *x, void *y,
                              aqd_stream_t stream)
 {

@@ -98,6 +98,9 @@ hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
 // fused projection shortcut (4-bit, 256 x 64 tiles): tile counts use blk_px = 64
 constexpr int PROJ_BLK_PX = 64;
 hipError_t launch_qconv_proj(const MfmaArgs &a, hipStream_t stream);
+// the matrix-core rate probe (mfma_probe.hip): workgroups x 4 waves x iters
+// x 16 MFMAs of 16x16x64 int8; out: workgroups x 256 ints
+hipError_t launch_mfma_probe(int workgroups, int iters, int *out, hipStream_t stream);
 // TILE_WV launches (qconv_wv.hip)
 hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream);
 // TILE_FP4 (code_bits 2) and TILE_B8 (code_bits 8) launches (qconv_b16.hip);

@@ -165,3 +165,11 @@ def test_bn_fold_chain_agrees_with_oracle():
         mm1, sh1 = ref.requant_params(r1[3], 0.2)
         mm2, sh2 = aqd.requant_params(r2[3], 0.2)
         assert np.array_equal(mm1, mm2) and np.array_equal(sh1, sh2)
+
+
+def test_mfma_probe_rejects_bad_arguments():
+    """Argument checks of the probe run before any launch (no GPU needed)."""
+    L = aqd.lib()
+    assert L.aqd_mfma_probe(0, 1, None, None) == aqd.AQD_ERR_INVALID
+    assert L.aqd_mfma_probe(1, 0, None, None) == aqd.AQD_ERR_INVALID
+    assert L.aqd_mfma_probe(1, 1, None, None) == aqd.AQD_ERR_INVALID

@@ -646,3 +646,16 @@ def test_fused_projection_unsupported_pairs(torch):
     finally:
         aqd.qconv_destroy(hm)
         aqd.qconv_destroy(hp_)
+
+
+def test_mfma_probe_is_deterministic(torch):
+    """The matrix-core rate probe (a diagnostic the benchmark times) runs and
+    writes the same checksums twice."""
+    out = torch.zeros(4 * 256, dtype=torch.int32, device="cuda:0")
+    aqd.mfma_probe(4, 3, out)
+    torch.cuda.synchronize()
+    first = out.cpu().numpy().copy()
+    out.zero_()
+    aqd.mfma_probe(4, 3, out)
+    torch.cuda.synchronize()
+    assert np.array_equal(first, out.cpu().numpy()) and np.any(first != 0)

@@ -124,6 +124,13 @@ def test_three_bit_retinanet_scaled(torch):
     assert gpu.fused
 
 
+def test_three_bit_retinanet_full_size(torch):
+    """The 3-bit RetinaNet-R50 on one 800x1333 image: every tensor and
+    table."""
+    net, params = workloads.retinanet_config(1, 800, 1333, 3)
+    compare_network(torch, net, params)
+
+
 def test_graph_replay_matches_eager(torch):
     """The network recorded once into a HIP graph (aqd_graph_*): three
     replays, each after the output buffers were overwritten by eager work and
@@ -159,4 +166,10 @@ def test_fcos_scaled(torch):
     reduced image size: every tensor and epilogue table against the oracle
     (the 1-channel centerness prediction runs on the direct kernel)."""
     net, params = workloads.fcos_config(1, 192, 256)
+    compare_network(torch, net, params)
+
+
+def test_fcos_full_size(torch):
+    """The FCOS heads on ResNet-50 + FPN on one 800x1333 image."""
+    net, params = workloads.fcos_config(1, 800, 1333)
     compare_network(torch, net, params)
