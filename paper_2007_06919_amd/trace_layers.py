@@ -8,6 +8,8 @@ those passes, its share and its integer TOPS (the fused launches count the
 shortcut's MACs too).
 
 usage: python -m paper_2007_06919_amd.trace_layers <kernel_trace.csv> [workload] [top] [passes]
+workload: a workload number, or io8 for the fully quantized RetinaNet-R50
+(batch 8, 800x1333, 8-bit image, stem, pooling and predictions).
 """
 import csv
 import sys
@@ -44,10 +46,13 @@ def launch_list(net):
 
 
 def layer_table(trace_csv, workload=4, top=30, passes=5):
-    net, _ = workloads.config(workload)
+    if workload == "io8":
+        net = workloads.retinanet_r50_net(8, 800, 1333, 4, io_bits=8)
+    else:
+        net, _ = workloads.config(int(workload))
     launches = launch_list(net)
     rows = sorted((r for r in csv.DictReader(open(trace_csv))
-                   if any(k in r["Kernel_Name"] for k in ("qconv_", "splitk_", "maxpool_kernel"))),
+                   if any(k in r["Kernel_Name"] for k in ("qconv_", "splitk_", "maxpool"))),
                   key=lambda r: int(r["Dispatch_Id"]))  # enqueue order (launches on several streams overlap)
     # one entry per launch; a combining kernel belongs to the launch before it
     seq = []
@@ -77,6 +82,6 @@ def layer_table(trace_csv, workload=4, top=30, passes=5):
 
 
 if __name__ == "__main__":
-    print(layer_table(sys.argv[1], int(sys.argv[2]) if len(sys.argv) > 2 else 4,
+    print(layer_table(sys.argv[1], sys.argv[2] if len(sys.argv) > 2 else 4,
                       int(sys.argv[3]) if len(sys.argv) > 3 else 30,
                       int(sys.argv[4]) if len(sys.argv) > 4 else 5))
