@@ -81,6 +81,8 @@ WV8_CASES = [
     (8, 50, 84, 256, 256, 3, 1),     # 263 tiles of 256 x 128: 256 x 144 tiles
     (1, 7, 9, 256, 256, 3, 1),       # one partial tile (a launch far below one round)
     (1, 20, 30, 512, 288, 1, 1),     # 1x1, two stages per tap, a partial channel tile
+    (1, 20, 30, 256, 256, 1, 1),     # 1x1, one stage in all (the first is the last)
+    (8, 50, 84, 256, 256, 1, 1),     # one stage on 256 x 144 tiles
 ]
 
 
