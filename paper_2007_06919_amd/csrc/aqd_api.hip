@@ -683,7 +683,12 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
             t128 += (p + 127) / 128 * h0.co_tiles;
             t144 += (p + 143) / 144 * h0.co_tiles;
         }
-        if (t128 > 256 && t144 <= 256) {
+        if (h0.ksteps <= 8) {
+            // short K ranges: a tile's copies and epilogue outweigh its MFMAs;
+            // 256 x 64 tiles, three workgroups per CU
+            tile_cfg = TILE_WV64;
+            blk_px = 64;
+        } else if (t128 > 256 && t144 <= 256) {
             tile_cfg = TILE_WV144;
             blk_px = 144;
         }
@@ -752,7 +757,7 @@ void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
 {
     if (a.tile_cfg == TILE_256x64S || a.tile_cfg == TILE_256x64 || a.tile_cfg == TILE_STREAM ||
         a.tile_cfg == TILE_STREAM_C128 || a.tile_cfg == TILE_STREAM_C64 || a.tile_cfg == TILE_128x128_O3 ||
-        a.tile_cfg == TILE_64x256_O3 || a.tile_cfg == TILE_STREAM_H128 || a.tile_cfg == TILE_WV || a.tile_cfg == TILE_WV144 ||
+        a.tile_cfg == TILE_64x256_O3 || a.tile_cfg == TILE_STREAM_H128 || a.tile_cfg == TILE_WV || a.tile_cfg == TILE_WV144 || a.tile_cfg == TILE_WV64 ||
         a.tile_cfg == TILE_STEM) {  // never split
         *nparts = 1;
         *kchunk = a.ksteps;

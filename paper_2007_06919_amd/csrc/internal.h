@@ -40,7 +40,10 @@ enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
        TILE_STEM = 14,
        // TILE_WV's kernel on 256 x 144 tiles, one workgroup per CU: code
        // outputs of launches a little above one round of 256 x 128 tiles
-       TILE_WV144 = 15 };
+       TILE_WV144 = 15,
+       // TILE_WV's kernel on 256 x 64 tiles, three workgroups per CU: code
+       // outputs with at most 8 K steps
+       TILE_WV64 = 16 };
 constexpr int KC = 64;
 
 // tile shape of a configuration, and the channels one lane holds per pixel

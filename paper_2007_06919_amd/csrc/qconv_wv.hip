@@ -52,17 +52,19 @@ constexpr int WV_NBUF = 4;
 // codes (the last tower layer of the fully quantized heads; then SKK = 0);
 // SKK: 0 = no skip, 1 = code skip (4-bit); FAST: every shift >= 2 (32-bit
 // requantisation); NJ: column tiles of 16 pixels, 8 (256 x 128 tiles, two
-// workgroups per CU) or 9 (256 x 144 tiles, one per CU: launches a little
-// above one round of the smaller tile fit in one round; code outputs only)
+// workgroups per CU), 9 (256 x 144 tiles, one per CU: launches a little
+// above one round of the smaller tile fit in one round) or 4 (256 x 64
+// tiles, three per CU: short K ranges, where a tile's copies and epilogue
+// outweigh its MFMAs); 9 and 4 for code outputs only
 template <int OUTK, int SKK, int FAST, int NJ>
-__global__ void __launch_bounds__(256, NJ == 8 ? 2 : 1) qconv_wv_kernel(MfmaArgs A)
+__global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? 3 : 1) qconv_wv_kernel(MfmaArgs A)
 {
     static_assert(OUTK == 0 || SKK == 0, "int32 and 8-bit outputs have no skip");
-    static_assert(NJ == 8 || (NJ == 9 && OUTK != 1), "256 x 144 tiles: code outputs");
+    static_assert(NJ == 8 || ((NJ == 9 || NJ == 4) && OUTK != 1), "256 x 144 and 256 x 64 tiles: code outputs");
     constexpr int BI = 4, MI = 4;
     constexpr int WV_BPX = 16 * NJ;                // pixels per workgroup tile
-    constexpr int NPC = (WV_BPX + 31) / 32;        // copy pieces of 32 pixels per stage (4 or 5)
-    constexpr int WV_STAGE = 32 * NPC * WV_ROW;    // 16 or 20 KiB (rows past the tile unused)
+    constexpr int NPC = (WV_BPX + 31) / 32;        // copy pieces of 32 pixels per stage (2, 4 or 5)
+    constexpr int WV_STAGE = 32 * NPC * WV_ROW;    // 8, 16 or 20 KiB (rows past the tile unused)
     constexpr int WV_LDS = WV_NBUF * WV_STAGE;
     constexpr int BO = OUTK == 2 ? 8 : 4;          // output code width
     constexpr int QMAX = (1 << BO) - 1, OW = BO / 2;  // words of a lane's 16 channels
@@ -187,12 +189,14 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : 1) qconv_wv_kernel(MfmaArgs
         write_piece(0, m, load_piece(m));
     advance();
 #pragma unroll
-    for (int m = 0; m < 3; ++m)
+    for (int m = 0; m < (NPC < 3 ? NPC : 3); ++m)
         write_piece(1, m, load_piece(m));
 #pragma unroll
     for (int m = 3; m < NPC; ++m)
         rb[m] = load_piece(m);
-    rb[0] = rb[1] = rb[2] = rb[3];
+#pragma unroll
+    for (int m = 0; m < (NPC < 3 ? NPC : 3); ++m)
+        rb[m] = rb[NPC - 1];
     advance();  // copy state: stage 2
     v4i fa[4][MI];
 #pragma unroll
@@ -206,7 +210,7 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : 1) qconv_wv_kernel(MfmaArgs
         return v4i{(int)(w.x & 0x0F0F0F0Fu), (int)((w.x >> 4) & 0x0F0F0F0Fu),
                    (int)(w.y & 0x0F0F0F0Fu), (int)((w.y >> 4) & 0x0F0F0F0Fu)};
     };
-    constexpr int RA = 3;  // fragments are read RA column tiles ahead of their MFMAs
+    constexpr int RA = NJ == 4 ? 2 : 3;  // fragments are read RA column tiles ahead of their MFMAs
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 #pragma unroll
     for (int j = 0; j < RA; ++j)
@@ -234,7 +238,8 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : 1) qconv_wv_kernel(MfmaArgs
         static_for<4>([&](auto qc) {
             constexpr int q = decltype(qc)::value;
             const int k = 4 * gs + q;
-            rb[q] = load_piece(q);  // pieces of stage gs + 2
+            if constexpr (q < NPC)
+                rb[q] = load_piece(q);  // pieces of stage gs + 2
             if constexpr (q == 3 && NPC == 5)
                 rb[4] = load_piece(4);
             __builtin_amdgcn_sched_barrier(0);
@@ -269,7 +274,8 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : 1) qconv_wv_kernel(MfmaArgs
             // the pieces loaded one step earlier (at q = 0: the last ones of
             // stage gs + 1)
             if constexpr (q >= 1) {
-                write_piece((buf + 2) & 3, q - 1, rb[q - 1]);
+                if constexpr (q - 1 < NPC)
+                    write_piece((buf + 2) & 3, q - 1, rb[q - 1]);
             } else {
 #pragma unroll
                 for (int m = 3; m < NPC; ++m)
@@ -283,7 +289,7 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : 1) qconv_wv_kernel(MfmaArgs
         stage(gs);
     // the channel tile's epilogue table does not depend on the accumulators:
     // its loads are issued before the last stage, whose MFMAs hide their
-    // latency
+    // latency (after it on 256 x 64 tiles, within their register budget)
     constexpr int PRM_PER = EPI_FIELDS * WV_BCO / 256;
     int prm_r[PRM_PER];
     auto load_prm = [&]() {
@@ -294,9 +300,11 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : 1) qconv_wv_kernel(MfmaArgs
             prm_r[t] = S.epi[which * A.cout_pad + co_tile * WV_BCO + c];
         }
     };
-    if constexpr (OUTK != 1)
+    if constexpr (OUTK != 1 && NJ != 4)
         load_prm();
     stage(NST - 1);
+    if constexpr (OUTK != 1 && NJ == 4)
+        load_prm();
 
     if constexpr (OUTK == 1) {
         // int32 outputs v = acc + bias (the bias is in the accumulators), in
@@ -541,8 +549,8 @@ void launch_wv_modes(const MfmaArgs &a, bool fast, dim3 grid, hipStream_t stream
 
 hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream)
 {
-    const bool wide = a.tile_cfg == TILE_WV144;
-    if ((a.bits_out != 4 && a.bits_out != 8 && a.bits_out != 32) || (wide && a.bits_out == 32) ||
+    const bool wide = a.tile_cfg == TILE_WV144, narrow = a.tile_cfg == TILE_WV64;
+    if ((a.bits_out != 4 && a.bits_out != 8 && a.bits_out != 32) || ((wide || narrow) && a.bits_out == 32) ||
         (a.skip_bits != 0 && (a.skip_bits != 4 || a.bits_out != 4)) || a.cin % 256 != 0 ||
         a.ksteps % 4 != 0 || a.ksplit != 1 || a.part != 0 || a.kh > 16 || a.kw > 16)
         return hipErrorInvalidValue;
@@ -557,6 +565,8 @@ hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream)
         fast = fast && a.seg[i].fast;
     if (wide)
         launch_wv_modes<9>(a, fast, grid, stream);
+    else if (narrow)
+        launch_wv_modes<4>(a, fast, grid, stream);
     else
         launch_wv_modes<8>(a, fast, grid, stream);
     return hipGetLastError();

@@ -162,9 +162,9 @@ def test_conv_stream_parity(torch, case, variant):
 
 # cin a multiple of 256, code outputs and at least 200 tiles of 256 x 128:
 # the register-fed kernel (weights read into registers, codes staged in LDS
-# four K steps at a time), on 256 x 144 tiles (one round, one workgroup per
-# CU) where 256 x 128 tiles would be a little above one round, on 256 x 128
-# tiles otherwise. The head-tower shape, two and four stages per tap,
+# four K steps at a time), on 256 x 64 tiles for K ranges of at most 8
+# steps, on 256 x 144 tiles (one round, one workgroup per CU) where 256 x 128
+# tiles would be a little above one round, on 256 x 128 tiles otherwise. The head-tower shape, two and four stages per tap,
 # stride 2, a partial channel tile, code skips with and without the
 # upsample, 3-bit codes, ragged pixel tails.
 WV_CASES = [
@@ -179,6 +179,10 @@ WV_CASES = [
     (5, 203, 131, 256, 288, 3, 2, 4, 4, 0, 4, 4, False),    # stride 2, a partial channel tile, skip
     (5, 75, 90, 256, 256, 3, 1, 4, 4, 0, 4, 4, False),      # 264 tiles (235 of 144 px), skip
     (4, 130, 130, 256, 288, 3, 2, 4, 4, 0, 4, 4, False),    # 266 tiles (236 of 144): stride 2, partial channel tile
+    # 256 x 64 tiles (8 K steps)
+    (2, 100, 167, 512, 256, 1, 1, 4, 4, 1, 4, 4, True),     # 1x1 with an upsampled skip (FPN lateral shape)
+    (1, 60, 100, 512, 2048, 1, 1, 4, 4, 0, 4, 4, False),    # 1x1 512 -> 2048 with a skip, eight channel tiles
+    (3, 90, 100, 512, 288, 1, 1, 4, 4, 0, 4, 0, False),     # a partial channel tile
 ]
 
 
