@@ -16,7 +16,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libaqd.so")
-SOURCES = ["aqd_api.hip", "qconv_mfma.hip", "qconv_wv.hip", "qconv_b16.hip", "qconv_stem.hip", "qconv_splitk.hip", "qconv_direct.hip",
+SOURCES = ["aqd_api.hip", "qconv_mfma.hip", "qconv_wv.hip", "qconv_wvs.hip", "qconv_b16.hip", "qconv_stem.hip", "qconv_splitk.hip", "qconv_direct.hip",
            "qadd.hip", "qpool.hip", "mfma_probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

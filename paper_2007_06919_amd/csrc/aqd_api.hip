@@ -630,10 +630,19 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
             t128 += ((long long)segs[i].n * chk[i].ho * chk[i].wo + 127) / 128 * h0.co_tiles;
         const bool short_codes = h0.ksteps <= 4 && h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_in == 4 &&
                                  h0.d.bits_out == 4 && (h0.d.skip_bits == 0 || h0.d.skip_bits == 4);
+        // 1x1 layers with 256 input channels and 4-bit code outputs (one
+        // segment): weight-stationary persistent tiles
+        const bool wvs = count == 1 && h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_in == 4 &&
+                         h0.d.bits_out == 4 && (h0.d.skip_bits == 0 || h0.d.skip_bits == 4) && h0.d.kh == 1 &&
+                         h0.d.kw == 1 && h0.d.pad == 0 && h0.d.cin == 256 &&
+                         h0.d.cout % 256 == 0 && h0.co_tiles <= 256 && x_small;
         if (h0.d.out_mode == AQD_OUT_CODES && h0.d.bits_out == 8) {
             // 8-bit code outputs: only the register-fed kernel writes them
             REQUIRE(x_small, "8-bit code outputs take inputs of less than 2^31 bytes per segment");
             tile_cfg = TILE_WV;
+        } else if (wvs) {
+            tile_cfg = TILE_WVS;
+            blk_px = 64;
         } else if (short_codes && h0.ksteps <= 2 && h0.d.kh == 1 && h0.d.kw == 1 && h0.d.pad == 0 &&
                    h0.d.cout % 256 == 0) {
             tile_cfg = TILE_STREAM;
@@ -757,7 +766,7 @@ void plan_split(const MfmaArgs &a, int *nparts, int *kchunk)
 {
     if (a.tile_cfg == TILE_256x64S || a.tile_cfg == TILE_256x64 || a.tile_cfg == TILE_STREAM ||
         a.tile_cfg == TILE_STREAM_C128 || a.tile_cfg == TILE_STREAM_C64 || a.tile_cfg == TILE_128x128_O3 ||
-        a.tile_cfg == TILE_64x256_O3 || a.tile_cfg == TILE_STREAM_H128 || a.tile_cfg == TILE_WV || a.tile_cfg == TILE_WV144 || a.tile_cfg == TILE_WV64 ||
+        a.tile_cfg == TILE_64x256_O3 || a.tile_cfg == TILE_STREAM_H128 || a.tile_cfg == TILE_WV || a.tile_cfg == TILE_WV144 || a.tile_cfg == TILE_WV64 || a.tile_cfg == TILE_WVS ||
         a.tile_cfg == TILE_STEM) {  // never split
         *nparts = 1;
         *kchunk = a.ksteps;

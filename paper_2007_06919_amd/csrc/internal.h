@@ -43,7 +43,10 @@ enum { TILE_256x128 = 0, TILE_128x256 = 1, TILE_64x512 = 2,
        TILE_WV144 = 15,
        // TILE_WV's kernel on 256 x 64 tiles, three workgroups per CU: code
        // outputs with at most 8 K steps
-       TILE_WV64 = 16 };
+       TILE_WV64 = 16,
+       // 1x1, cin 256, 4-bit code outputs, cout a multiple of 256, one
+       // segment: weight-stationary persistent 256 x 64 tiles (qconv_wvs.hip)
+       TILE_WVS = 17 };
 constexpr int KC = 64;
 
 // tile shape of a configuration, and the channels one lane holds per pixel
@@ -104,6 +107,8 @@ hipError_t launch_qconv_proj(const MfmaArgs &a, hipStream_t stream);
 // the matrix-core rate probe (mfma_probe.hip): workgroups x 4 waves x iters
 // x 16 MFMAs of 16x16x64 int8; out: workgroups x 256 ints
 hipError_t launch_mfma_probe(int workgroups, int iters, int *out, hipStream_t stream);
+// TILE_WVS launches (qconv_wvs.hip)
+hipError_t launch_qconv_wvs(const MfmaArgs &a, hipStream_t stream);
 // TILE_WV launches (qconv_wv.hip)
 hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream);
 // TILE_FP4 (code_bits 2) and TILE_B8 (code_bits 8) launches (qconv_b16.hip);

@@ -1100,7 +1100,8 @@ void mfma_tile_shape(int tile_cfg, int *blk_co, int *blk_px, int *chan_per_lane)
     case TILE_256x128: *blk_co = 256; *blk_px = 128; *chan_per_lane = 32; return;
     case TILE_WV: *blk_co = 256; *blk_px = 128; *chan_per_lane = 16; return;
     case TILE_WV144: *blk_co = 256; *blk_px = 144; *chan_per_lane = 16; return;
-    case TILE_WV64: *blk_co = 256; *blk_px = 64; *chan_per_lane = 16; return;
+    case TILE_WV64:
+    case TILE_WVS: *blk_co = 256; *blk_px = 64; *chan_per_lane = 16; return;
     case TILE_FP4:
     case TILE_B8: *blk_co = 256; *blk_px = 128; *chan_per_lane = 32; return;
     case TILE_STEM: *blk_co = 64; *blk_px = 128; *chan_per_lane = 16; return;
@@ -1234,6 +1235,7 @@ hipError_t launch_qconv_mfma(int bits_in, const MfmaArgs &a, hipStream_t stream)
         case TILE_WV:
         case TILE_WV144:
         case TILE_WV64: return launch_qconv_wv(a, stream);
+        case TILE_WVS: return launch_qconv_wvs(a, stream);
         case TILE_256x64S: return launch_qconv_short(a, stream);
         case TILE_256x64: return launch_modes<4, 8, 2, 2, 2>(a, stream);
         case TILE_STREAM:

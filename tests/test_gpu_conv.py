@@ -137,6 +137,13 @@ STREAM_CASES = [
     (2, 16, 18, 256, 256, 1, 1, 4, 4, 0, 4, 4, True),       # upsampled code skip
     (1, 25, 21, 256, 256, 1, 2, 4, 4, 1, 4, 4, False),      # stride 2
     (8, 50, 84, 256, 1024, 1, 1, 4, 4, 1, 4, 4, False),     # ResNet-50 res4 conv3 at batch 8
+    # (the cin-256 cases above with cout a multiple of 256 run on the
+    # weight-stationary tiles: 1x1, cin 256, one segment, persistent 256 x 64
+    # tiles with the weights in registers)
+    (3, 77, 91, 256, 768, 1, 1, 4, 4, 1, 4, 4, False),      # weight-stationary: three channel tiles, skip
+    (1, 31, 29, 256, 512, 1, 2, 4, 4, 0, 4, 0, False),      # weight-stationary: stride 2, a ragged last tile
+    (1, 5, 7, 256, 256, 1, 1, 4, 4, 1, 4, 4, False),        # weight-stationary: fewer tiles than slots
+    (8, 100, 167, 256, 256, 1, 1, 4, 4, 0, 4, 4, True),     # weight-stationary: ~4 tiles per workgroup, upsampled skip
 ]
 
 
