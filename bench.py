@@ -40,8 +40,8 @@ B2B_REPS = 10               # back-to-back repeats of each dominant launch (sust
 # COPY_PROBE_BYTES; valid only for the kernel source it was measured on.
 HEAD_KERNEL = "qconv_wv_kernel<0, 0, 1, 8>"
 HEAD_KERNEL_SOURCES = ("qconv_wv.hip", "mfma_common.h")
-HEAD_TRAFFIC = {"kernel_sha256": "a24db71d5424a70e06d95f027780566bb7a03a58484218754b2dbfb5d9497b05",
-                "fetch_bytes": 51036615, "write_bytes": 45670400}
+HEAD_TRAFFIC = {"kernel_sha256": "fc7b3d5593cb909d10dfd82a1d2dc3e4c14fcfdd98ba7aa9c0bf03d6b7cbb7b0",
+                "fetch_bytes": 51036658, "write_bytes": 45670400}
 
 
 def kernel_sha256():
