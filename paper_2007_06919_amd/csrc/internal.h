@@ -111,6 +111,9 @@ hipError_t launch_mfma_probe(int workgroups, int iters, int *out, hipStream_t st
 hipError_t launch_qconv_wvs(const MfmaArgs &a, hipStream_t stream);
 // TILE_WV launches (qconv_wv.hip)
 hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream);
+// fused projection shortcut, both 1x1 with cin and cin2 multiples of 256, on
+// TILE_WV64's 256 x 64 tiles (qconv_wv.hip)
+hipError_t launch_qconv_wv_proj(const MfmaArgs &a, hipStream_t stream);
 // TILE_FP4 (code_bits 2) and TILE_B8 (code_bits 8) launches (qconv_b16.hip);
 // a.ksteps and a.kchunk in 64-channel steps, multiples of a stage (4 and 2)
 hipError_t launch_qconv_b16(int code_bits, const MfmaArgs &a, hipStream_t stream);

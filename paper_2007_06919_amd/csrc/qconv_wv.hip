@@ -50,16 +50,19 @@ constexpr int WV_NBUF = 4;
 
 // OUTK: 0 = 4-bit codes, 1 = int32 v = acc + bias (then SKK = 0), 2 = 8-bit
 // codes (the last tower layer of the fully quantized heads; then SKK = 0);
-// SKK: 0 = no skip, 1 = code skip (4-bit); FAST: every shift >= 2 (32-bit
+// SKK: 0 = no skip, 1 = code skip (4-bit), 2 = a residual block's projection
+// shortcut fused in (1x1 convolutions both, 256 x 64 tiles, 4-bit codes out:
+// two accumulator sets, two workgroups per CU); FAST: every shift >= 2 (32-bit
 // requantisation); NJ: column tiles of 16 pixels, 8 (256 x 128 tiles, two
 // workgroups per CU), 9 (256 x 144 tiles, one per CU: launches a little
 // above one round of the smaller tile fit in one round) or 4 (256 x 64
 // tiles, three per CU: short K ranges, where a tile's copies and epilogue
 // outweigh its MFMAs); 9 and 4 for code outputs only
 template <int OUTK, int SKK, int FAST, int NJ>
-__global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? 3 : 1) qconv_wv_kernel(MfmaArgs A)
+__global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? (SKK == 2 ? 2 : 3) : 1) qconv_wv_kernel(MfmaArgs A)
 {
     static_assert(OUTK == 0 || SKK == 0, "int32 and 8-bit outputs have no skip");
+    static_assert(SKK != 2 || NJ == 4, "the fused projection runs on 256 x 64 tiles");
     static_assert(NJ == 8 || ((NJ == 9 || NJ == 4) && OUTK != 1), "256 x 144 and 256 x 64 tiles: code outputs");
     constexpr int BI = 4, MI = 4;
     constexpr int WV_BPX = 16 * NJ;                // pixels per workgroup tile
@@ -89,11 +92,15 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? 3 : 1) qconv_wv_k
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, g = lane >> 4;
 
-    const int row_bytes = A.cin * BI / 8;
-    const int spt = A.cin / 256;                 // stages per tap
     const int KS = A.ksteps;
     const int NST = KS / 4;                      // stages (KS is a multiple of 4)
     const int hw = S.ho * S.wo;
+    // the fused projection shortcut (SKK 2): its 1x1 convolution of x2 (cin2
+    // channels, stride2, no padding) runs first, over K steps 0 .. KS2 - 1,
+    // into a second accumulator set; the main 1x1 convolution follows
+    const int KS2 = SKK == 2 ? A.ksteps2 : 0;
+    const int NST2 = KS2 / 4;
+    const int NSTT = NST2 + NST;                 // stages of both
 
     // ---- activation copies: piece m of a stage = pixels 32m .. 32m+31 of the
     // tile, lane tid copying 16-byte chunk tid % 8 of pixel 32m + tid / 8.
@@ -107,24 +114,37 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? 3 : 1) qconv_wv_k
     // holds n * h * w * row_bytes < 2^31 bytes (checked on the host)
     int xbase[NPC];
     uint32_t xvalid[NPC];
+    // geometry of the input being copied (the projection's x2 first under SKK 2)
+    int row_bytes = 0, spt = 0, c_w = 0;
+    buf_rsrc xr;
+    auto set_copy = [&](const bool proj) {
+        const uint8_t *src = proj ? S.x2 : S.x;
+        const int ch = proj ? A.cin2 : A.cin, ih = proj ? S.h2 : S.h, iw = proj ? S.w2 : S.w;
+        const int st = proj ? A.stride2 : A.stride, pd = proj ? 0 : A.pad;
+        const int kh = proj ? 1 : A.kh, kw = proj ? 1 : A.kw;
+        row_bytes = ch * BI / 8;
+        spt = ch / 256;                          // stages per tap
+        c_w = iw;
 #pragma unroll
-    for (int m = 0; m < NPC; ++m) {
-        const unsigned pl = (unsigned)(32 * m + (tid >> 3));    // pixel within the tile
-        const unsigned p = (unsigned)(px_tile * WV_BPX) + pl;
-        const bool ok = p < (unsigned)S.P && pl < (unsigned)WV_BPX;
-        const unsigned pn = ok ? p / (unsigned)hw : 0u;
-        const unsigned prem = ok ? p - pn * (unsigned)hw : 0u;
-        const int oh = (int)(prem / (unsigned)S.wo), ow = (int)prem - oh * S.wo;
-        const int ih0 = oh * A.stride - A.pad, iw0 = ow * A.stride - A.pad;
-        uint32_t v = 0;
-        for (int t = 0; t < A.kh; ++t)
-            v |= ((unsigned)(ih0 + t) < (unsigned)S.h ? 1u : 0u) << t;
-        for (int t = 0; t < A.kw; ++t)
-            v |= ((unsigned)(iw0 + t) < (unsigned)S.w ? 1u : 0u) << (16 + t);
-        xvalid[m] = ok ? v : 0u;
-        xbase[m] = (((int)pn * S.h + ih0) * S.w + iw0) * row_bytes + 16 * c16;
-    }
-    const buf_rsrc xr = make_rsrc(S.x, S.n * S.h * S.w * row_bytes);
+        for (int m = 0; m < NPC; ++m) {
+            const unsigned pl = (unsigned)(32 * m + (tid >> 3));    // pixel within the tile
+            const unsigned p = (unsigned)(px_tile * WV_BPX) + pl;
+            const bool ok = p < (unsigned)S.P && pl < (unsigned)WV_BPX;
+            const unsigned pn = ok ? p / (unsigned)hw : 0u;
+            const unsigned prem = ok ? p - pn * (unsigned)hw : 0u;
+            const int oh = (int)(prem / (unsigned)S.wo), ow = (int)prem - oh * S.wo;
+            const int ih0 = oh * st - pd, iw0 = ow * st - pd;
+            uint32_t v = 0;
+            for (int t = 0; t < kh; ++t)
+                v |= ((unsigned)(ih0 + t) < (unsigned)ih ? 1u : 0u) << t;
+            for (int t = 0; t < kw; ++t)
+                v |= ((unsigned)(iw0 + t) < (unsigned)iw ? 1u : 0u) << (16 + t);
+            xvalid[m] = ok ? v : 0u;
+            xbase[m] = (((int)pn * ih + ih0) * iw + iw0) * row_bytes + 16 * c16;
+        }
+        xr = make_rsrc(src, S.n * ih * iw * row_bytes);
+    };
+    set_copy(SKK == 2);
     // LDS byte offsets: eight-byte column c of pixel p at 128 p + 8 (c ^ (p & 15))
     const int wp = tid >> 3;                      // pixel within a piece (p & 15 == wp & 15)
     const uint32_t wo0 = WV_ROW * wp + 8 * ((2 * c16) ^ (wp & 15));
@@ -135,17 +155,25 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? 3 : 1) qconv_wv_k
     // copy state of the stage being loaded (uniform): tap (tr, tq), 128-byte
     // chunk th; its byte offset from a window origin and the window bits it needs
     int tr = 0, tq = 0, th = 0;
+    bool c_proj = SKK == 2;                       // the projection's stages are being copied
     int x_off = 0;
     uint32_t x_need = 0x10001u;
     auto advance = [&]() {
         if (++th == spt) {
             th = 0;
-            if (++tq == A.kw) {
+            if (++tq == (c_proj ? 1 : A.kw)) {
                 tq = 0;
                 ++tr;
             }
         }
-        x_off = (tr * S.w + tq) * row_bytes + WV_ROW * th;
+        if constexpr (SKK == 2) {
+            if (c_proj && tr == 1) {             // past the projection's one tap: the main input
+                c_proj = false;
+                tr = 0;
+                set_copy(false);
+            }
+        }
+        x_off = (tr * c_w + tq) * row_bytes + WV_ROW * th;
         x_need = (1u << tr) | (1u << (16 + tq));
     };
     auto load_piece = [&](int m) -> v4i {
@@ -165,19 +193,37 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? 3 : 1) qconv_wv_k
     // buffer's size and gets zeros, which no MFMA uses
     const buf_rsrc wr = make_rsrc(S.wt + (long long)co_tile * KS * WV_BCO * KC, KS * WV_BCO * KC);
     const int w_lane = (64 * wave + r) * KC + 16 * g;
-    auto load_w = [&](int k, int i) -> v4i { return load_b128(wr, w_lane + i * 1024, k * (WV_BCO * KC)); };
+    // under SKK 2, K steps 0 .. KS2 - 1 are the projection's (same tile layout)
+    buf_rsrc wr2 = wr;
+    if constexpr (SKK == 2)
+        wr2 = make_rsrc(S.wt2 + (long long)co_tile * KS2 * WV_BCO * KC, KS2 * WV_BCO * KC);
+    auto load_w = [&](int k, int i) -> v4i {
+        if constexpr (SKK == 2) {
+            if (k < KS2)
+                return load_b128(wr2, w_lane + i * 1024, k * (WV_BCO * KC));
+            return load_b128(wr, w_lane + i * 1024, (k - KS2) * (WV_BCO * KC));
+        }
+        return load_b128(wr, w_lane + i * 1024, k * (WV_BCO * KC));
+    };
 
     // ---- accumulators start at the bias (Eq. 6): lane group g of wave w holds
     // channels 128 (w >> 1) + 32 g + 16 (w & 1) + 4 i + e of the tile
     const int co_loc = 128 * (wave >> 1) + 32 * g + 16 * (wave & 1);
     const int co_glob = co_tile * WV_BCO + co_loc;
     v4i acc[MI][NJ];
+    v4i acc2[SKK == 2 ? MI : 1][SKK == 2 ? NJ : 1];  // the projection's, from its own bias
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
         const v4i b = *(const v4i *)(S.epi + EPI_BIAS * A.cout_pad + co_glob + 4 * i);
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
             acc[i][j] = b;
+        if constexpr (SKK == 2) {
+            const v4i b2 = *(const v4i *)(S.epi2 + EPI_BIAS * A.cout_pad + co_glob + 4 * i);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+                acc2[i][j] = b2;
+        }
     }
 
     // ---- prologue: stage 0 and pieces 0-2 of stage 1 in LDS (pieces 3 and 4
@@ -233,7 +279,8 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? 3 : 1) qconv_wv_k
     // load, fragment read, then the widening of the next fragment (two
     // instructions) between each of the other three MFMAs; the VALU work
     // then issues while the matrix core runs.
-    auto stage = [&](const int gs) {
+    auto stage = [&](const int gs, auto main_c) {
+        constexpr bool MAIN = decltype(main_c)::value;  // false: the projection's accumulators
         const int buf = gs & 3;
         static_for<4>([&](auto qc) {
             constexpr int q = decltype(qc)::value;
@@ -253,8 +300,12 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? 3 : 1) qconv_wv_k
                     fa[(q + 2) & 3][j] = load_w(k + 2, j);  // set (q + 2) % 4 was step k - 2's
                 const v4i bn = widen(fb[(j + 1) % NJ]);
 #pragma unroll
-                for (int i = 0; i < MI; ++i)
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[q][i], bw, acc[i][j], 0, 0, 0);
+                for (int i = 0; i < MI; ++i) {
+                    if constexpr (MAIN)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[q][i], bw, acc[i][j], 0, 0, 0);
+                    else
+                        acc2[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[q][i], bw, acc2[i][j], 0, 0, 0);
+                }
                 if constexpr (j + RA < NJ)
                     fb[j + RA] = *(const uint2 *)(lds + 2048 * (j + RA) + r_this);
                 else
@@ -285,8 +336,12 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? 3 : 1) qconv_wv_k
                 advance();
         });
     };
-    for (int gs = 0; gs < NST - 1; ++gs)
-        stage(gs);
+    int gs0 = 0;
+    if constexpr (SKK == 2)
+        for (; gs0 < NST2; ++gs0)
+            stage(gs0, std::false_type{});
+    for (int gs = gs0; gs < NSTT - 1; ++gs)
+        stage(gs, std::true_type{});
     // the channel tile's epilogue table does not depend on the accumulators:
     // its loads are issued before the last stage, whose MFMAs hide their
     // latency (after it on 256 x 64 tiles, within their register budget)
@@ -302,7 +357,7 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? 3 : 1) qconv_wv_k
     };
     if constexpr (OUTK != 1 && NJ != 4)
         load_prm();
-    stage(NST - 1);
+    stage(NSTT - 1, std::true_type{});
     if constexpr (OUTK != 1 && NJ == 4)
         load_prm();
 
@@ -432,6 +487,8 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? 3 : 1) qconv_wv_k
                 int kv = 0;
                 if constexpr (SKK == 1)
                     kv = (int)__builtin_amdgcn_ubfe(skw[j][kbit >> 5], kbit & 31, BI);
+                else if constexpr (SKK == 2)
+                    kv = acc2[i][j][e];  // the projection's int32 output (Eq. 7-8: the skip)
                 int y;
                 if constexpr (FAST) {
                     int u = v;
@@ -546,6 +603,28 @@ void launch_wv_modes(const MfmaArgs &a, bool fast, dim3 grid, hipStream_t stream
 }
 
 }  // namespace
+
+// fused projection shortcut on the register-fed 256 x 64 tiles: main and
+// projection 1x1 with cin and cin2 multiples of 256, 4-bit codes out
+hipError_t launch_qconv_wv_proj(const MfmaArgs &a, hipStream_t stream)
+{
+    if (a.bits_out != 4 || a.skip_bits != 32 || a.cin % 256 != 0 || a.cin2 % 256 != 0 || a.ksteps % 4 != 0 ||
+        a.ksteps2 % 4 != 0 || a.ksteps != a.cin / KC || a.ksteps2 != a.cin2 / KC || a.kh != 1 || a.kw != 1 ||
+        a.pad != 0 || a.ksplit != 1 || a.part != 0 || a.nseg != 1 || a.up2)
+        return hipErrorInvalidValue;
+    const MfmaSeg &m = a.seg[0];
+    if ((long long)m.n * m.h * m.w * (a.cin / 2) >= (1LL << 31) ||
+        (long long)m.n * m.h2 * m.w2 * (a.cin2 / 2) >= (1LL << 31) ||
+        (long long)a.co_tiles * a.ksteps2 * WV_BCO * KC >= (1LL << 31) ||
+        (long long)a.co_tiles * a.ksteps * WV_BCO * KC >= (1LL << 31))
+        return hipErrorInvalidValue;
+    const dim3 grid(8 * a.tiles_per_xcd), block(256);
+    if (m.fast)
+        hipLaunchKernelGGL((qconv_wv_kernel<0, 2, 1, 4>), grid, block, 0, stream, a);
+    else
+        hipLaunchKernelGGL((qconv_wv_kernel<0, 2, 0, 4>), grid, block, 0, stream, a);
+    return hipGetLastError();
+}
 
 hipError_t launch_qconv_wv(const MfmaArgs &a, hipStream_t stream)
 {

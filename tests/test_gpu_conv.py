@@ -578,6 +578,10 @@ PROJ_CASES = [
     (8, 120, 100, 64, 120, 100, 64, 1, 256, 1, 1),   # ~3 tiles per workgroup
     (2, 13, 17, 64, 26, 33, 64, 2, 512, 1, 0),       # stride 2 shortcut, 2 channel tiles
     (1, 9, 11, 64, 9, 11, 64, 1, 768, 1, 1),         # 3 channel tiles, ragged pixels
+    # both inputs in 256-channel chunks: register-fed 256 x 64 tiles
+    (2, 25, 21, 512, 50, 42, 1024, 2, 2048, 1, 1),   # res5.0 shape: 8 channel tiles
+    (4, 21, 27, 256, 21, 27, 256, 1, 512, 1, 0),     # stride 1 shortcut, one stage each
+    (8, 30, 41, 256, 60, 81, 512, 2, 1024, 1, 1),    # res4.0 shape: 616 tiles, ragged pixels
 ]
 
 
@@ -635,10 +639,10 @@ def test_fused_projection_parity(torch, case):
     assert_same(got, _run_proj(torch, main, proj, fused=False), f"fused vs separate {case}")
 
 
-@pytest.mark.parametrize("which", [1, 4])
+@pytest.mark.parametrize("which", [1, 2, 4, 7])
 def test_fused_projection_general_requant(torch, which):
     """Levels with shift < 2 take the 64-bit requantisation in the fused launch
-    (tiled kernel and streaming kernel)."""
+    (tiled kernel, register-fed kernel and streaming kernel)."""
     main, proj = _proj_case(PROJ_CASES[which], seed=23, general=True)
     assert_same(_run_proj(torch, main, proj), oracle_conv(main), "fused projection, shift < 2")
 
