@@ -657,10 +657,11 @@ aqd_status_t prepare_group(int count, const qconv_seg_t *segs, SegCheck *chk, Mf
         } else if (short_codes) {
             tile_cfg = TILE_256x64S;
             blk_px = 64;
-        } else if (t128 >= 64 && t128 < 200 && h0.d.bits_in == 4 && h0.d.cin % 256 == 0 &&
+        } else if (t128 >= 64 && t128 < 200 && h0.ksteps <= 80 && h0.d.bits_in == 4 && h0.d.cin % 256 == 0 &&
                    h0.d.out_mode == AQD_OUT_CODES && (h0.d.skip_bits == 0 || h0.d.skip_bits == 4) && x_small) {
             // fewer 256 x 128 tiles than CUs, 256-channel input chunks, code
             // outputs: register-fed 256 x 64 tiles, one round at three per CU
+            // (longer K ranges split K instead)
             tile_cfg = TILE_WV64;
             blk_px = 64;
         } else if (t128 >= 64 && t128 < 200 && h0.ksteps <= 80) {

@@ -52,12 +52,18 @@ __device__ __forceinline__ uint2 load_b64(buf_rsrc r, int voff, int soff)
 
 
 // round(a * c / 2^d), ties up, d in [0, 31], result modulo 2^32: one 64-bit
-// multiply-add (exact: |a*c| < 2^62) and a funnel shift
-__device__ __forceinline__ int rsm32(int a, int c, int d)
+// multiply-add (exact: |a*c| < 2^62) and a funnel shift. The rounding term
+// 2^(d-1) (0 for d = 0) is (2^d) / 2 in 32 bits (below 2^31: a zero high
+// word), the addend of the multiply-add.
+__device__ __forceinline__ long long rsm_rnd(int d) { return (long long)((1u << d) >> 1); }
+// with the rounding term computed once per channel (rnd = rsm_rnd(d))
+__device__ __forceinline__ int rsm32r(int a, int c, long long rnd, int d)
 {
-    const long long t = (long long)a * c + (d > 0 ? (1LL << (d - 1)) : 0LL);
+    long long t;
+    asm("v_mad_i64_i32 %0, vcc, %1, %2, %3" : "=v"(t) : "v"(a), "v"(c), "v"(rnd) : "vcc");
     return (int)__builtin_amdgcn_alignbit((unsigned)((unsigned long long)t >> 32), (unsigned)t, (unsigned)d);
 }
+__device__ __forceinline__ int rsm32(int a, int c, int d) { return rsm32r(a, c, rsm_rnd(d), d); }
 
 // Requantisation of u with shift >= 2, before the clamp: with d = 31 + shift,
 // floor((u*M + 2^(d-1)) / 2^d) = (high word of u*M + 2^(d-33) * 2^32) >> (d - 32),

@@ -438,12 +438,14 @@ __global__ void __launch_bounds__(256, 2) qconv_b16_kernel(MfmaArgs A)
             rnd[2] = (long long)r4.z << 32; rnd[3] = (long long)r4.w << 32;
         }
         int sc[4] = {0, 0, 0, 0}, sd[4] = {0, 0, 0, 0}, sside[4] = {0, 0, 0, 0};
+        long long srnd[4] = {0, 0, 0, 0};  // rounding terms of the alignment
         if constexpr (SKK != 0 && !LUT) {
             const int4 c4 = *(const int4 *)(prm + EPI_SKIP_C * F4_BCO + cl);
             const int4 d4 = *(const int4 *)(prm + EPI_SKIP_D * F4_BCO + cl);
             const int4 e4 = *(const int4 *)(prm + EPI_SKIP_SIDE * F4_BCO + cl);
             sc[0] = c4.x; sc[1] = c4.y; sc[2] = c4.z; sc[3] = c4.w;
             sd[0] = d4.x; sd[1] = d4.y; sd[2] = d4.z; sd[3] = d4.w;
+            srnd[0] = rsm_rnd(d4.x); srnd[1] = rsm_rnd(d4.y); srnd[2] = rsm_rnd(d4.z); srnd[3] = rsm_rnd(d4.w);
             sside[0] = e4.x; sside[1] = e4.y; sside[2] = e4.z; sside[3] = e4.w;
         }
 #pragma unroll
@@ -461,7 +463,7 @@ __global__ void __launch_bounds__(256, 2) qconv_b16_kernel(MfmaArgs A)
                     if constexpr (LUT) {
                         u = (int)((unsigned)v + (unsigned)lut_l[(4 * i + e) * (QMAX + 1) + kv]);
                     } else if constexpr (SKK != 0) {
-                        const int scaled = rsm32(sside[e] ? v : kv, sc[e], sd[e]);
+                        const int scaled = rsm32r(sside[e] ? v : kv, sc[e], srnd[e], sd[e]);
                         u = (int)((unsigned)scaled + (unsigned)(sside[e] ? kv : v));
                     }
                     y = requant32(u, mult[e], rnd[e], shf[e]);
