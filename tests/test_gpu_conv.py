@@ -186,6 +186,10 @@ WV_CASES = [
     (5, 203, 131, 256, 288, 3, 2, 4, 4, 0, 4, 4, False),    # stride 2, a partial channel tile, skip
     (5, 75, 90, 256, 256, 3, 1, 4, 4, 0, 4, 4, False),      # 264 tiles (235 of 144 px), skip
     (4, 130, 130, 256, 288, 3, 2, 4, 4, 0, 4, 4, False),    # 266 tiles (236 of 144): stride 2, partial channel tile
+    # more than one round of 256 x 128 tiles without a skip
+    (3, 100, 167, 256, 288, 3, 1, 4, 4, 0, 4, 0, False),    # 784 tiles, a partial channel tile
+    (16, 50, 84, 256, 256, 3, 1, 3, 3, 1, 3, 0, False),     # 3-bit codes: 528 tiles
+    (1, 150, 181, 1024, 512, 1, 1, 4, 4, 1, 4, 0, False),   # 1x1, four stages per tile: 426 tiles
     # 256 x 64 tiles (8 K steps)
     (2, 100, 167, 512, 256, 1, 1, 4, 4, 1, 4, 4, True),     # 1x1 with an upsampled skip (FPN lateral shape)
     (1, 60, 100, 512, 2048, 1, 1, 4, 4, 0, 4, 4, False),    # 1x1 512 -> 2048 with a skip, eight channel tiles
