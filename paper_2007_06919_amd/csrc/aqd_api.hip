@@ -1078,9 +1078,10 @@ aqd_status_t qconv_run_proj(qconv_t conv, qconv_t proj, int level, int n, int h,
     // one K step each (cin 64): persistent streaming tiles (same 256 x 64 tiles)
     const bool stream_tiles = conv->ksteps == 1 && proj->ksteps == 1 && d.kh == 1 && d.kw == 1 &&
                               d.pad == 0 && d.cout % 256 == 0;
-    // both inputs in 256-channel chunks, 1x1 stride 1: register-fed 256 x 64
-    // tiles (32-bit buffer offsets: inputs below 2^31 bytes)
-    const bool wv_tiles = d.cin % 256 == 0 && e.cin % 256 == 0 && d.kh == 1 && d.kw == 1 && d.stride == 1 &&
+    // both inputs in 256-channel chunks (the main one may have 128 channels:
+    // one padded stage), 1x1 stride 1: register-fed 256 x 64 tiles (32-bit
+    // buffer offsets: inputs below 2^31 bytes)
+    const bool wv_tiles = (d.cin % 256 == 0 || d.cin == 128) && e.cin % 256 == 0 && d.kh == 1 && d.kw == 1 && d.stride == 1 &&
                           d.pad == 0 && xbytes < (1ull << 31) && pbytes < (1ull << 31);
     hipError_t err;
     if (stream_tiles) {

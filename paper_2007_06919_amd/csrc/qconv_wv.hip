@@ -93,7 +93,10 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? (SKK == 2 ? 2 : 3
     const int r = lane & 15, g = lane >> 4;
 
     const int KS = A.ksteps;
-    const int NST = KS / 4;                      // stages (KS is a multiple of 4)
+    // stages (KS is a multiple of 4; under SKK 2 the main 1x1 convolution may
+    // have 128 input channels: one stage whose K steps 2-3 read the next
+    // pixel's codes against weights past the buffer's end, zeros)
+    const int NST = (KS + 3) / 4;
     const int hw = S.ho * S.wo;
     // the fused projection shortcut (SKK 2): its 1x1 convolution of x2 (cin2
     // channels, stride2, no padding) runs first, over K steps 0 .. KS2 - 1,
@@ -123,7 +126,7 @@ __global__ void __launch_bounds__(256, NJ == 8 ? 2 : NJ == 4 ? (SKK == 2 ? 2 : 3
         const int st = proj ? A.stride2 : A.stride, pd = proj ? 0 : A.pad;
         const int kh = proj ? 1 : A.kh, kw = proj ? 1 : A.kw;
         row_bytes = ch * BI / 8;
-        spt = ch / 256;                          // stages per tap
+        spt = (ch + 255) / 256;                  // stages per tap
         c_w = iw;
 #pragma unroll
         for (int m = 0; m < NPC; ++m) {
@@ -610,7 +613,8 @@ void launch_wv_modes(const MfmaArgs &a, bool fast, dim3 grid, hipStream_t stream
 // projection 1x1 with cin and cin2 multiples of 256, 4-bit codes out
 hipError_t launch_qconv_wv_proj(const MfmaArgs &a, hipStream_t stream)
 {
-    if (a.bits_out != 4 || a.skip_bits != 32 || a.cin % 256 != 0 || a.cin2 % 256 != 0 || a.ksteps % 4 != 0 ||
+    if (a.bits_out != 4 || a.skip_bits != 32 || (a.cin % 256 != 0 && a.cin != 128) || a.cin2 % 256 != 0 ||
+        (a.ksteps % 4 != 0 && a.cin != 128) ||
         a.ksteps2 % 4 != 0 || a.ksteps != a.cin / KC || a.ksteps2 != a.cin2 / KC || a.kh != 1 || a.kw != 1 ||
         a.pad != 0 || a.ksplit != 1 || a.part != 0 || a.nseg != 1 || a.up2)
         return hipErrorInvalidValue;

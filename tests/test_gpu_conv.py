@@ -586,6 +586,7 @@ PROJ_CASES = [
     (2, 25, 21, 512, 50, 42, 1024, 2, 2048, 1, 1),   # res5.0 shape: 8 channel tiles
     (4, 21, 27, 256, 21, 27, 256, 1, 512, 1, 0),     # stride 1 shortcut, one stage each
     (8, 30, 41, 256, 60, 81, 512, 2, 1024, 1, 1),    # res4.0 shape: 616 tiles, ragged pixels
+    (4, 50, 84, 128, 100, 167, 256, 2, 512, 1, 0),   # res3.0 shape (main cin 128: a padded stage)
 ]
 
 
@@ -643,7 +644,7 @@ def test_fused_projection_parity(torch, case):
     assert_same(got, _run_proj(torch, main, proj, fused=False), f"fused vs separate {case}")
 
 
-@pytest.mark.parametrize("which", [1, 2, 4, 7])
+@pytest.mark.parametrize("which", [1, 2, 4, 7, 10])
 def test_fused_projection_general_requant(torch, which):
     """Levels with shift < 2 take the 64-bit requantisation in the fused launch
     (tiled kernel, register-fed kernel and streaming kernel)."""
