@@ -40,8 +40,8 @@ B2B_REPS = 10               # back-to-back repeats of each dominant launch (sust
 # COPY_PROBE_BYTES; valid only for the kernel source it was measured on.
 HEAD_KERNEL = "qconv_wv_kernel<0, 0, 1, 8>"
 HEAD_KERNEL_SOURCES = ("qconv_wv.hip", "mfma_common.h")
-HEAD_TRAFFIC = {"kernel_sha256": "957fd062c821d209277d03164d47e65f455faed8a5cd0890a9c8ed9e5a628379",
-                "fetch_bytes": 51036809, "write_bytes": 45670400}
+HEAD_TRAFFIC = {"kernel_sha256": "402e1eba8ec83cff12c1afac0d594bd7148c0230c8e3c31c2a82a2e48be5d333",
+                "fetch_bytes": 51036641, "write_bytes": 45670400}
 
 
 def kernel_sha256():
