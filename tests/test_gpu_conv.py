@@ -194,6 +194,9 @@ WV_CASES = [
     (2, 100, 167, 512, 256, 1, 1, 4, 4, 1, 4, 4, True),     # 1x1 with an upsampled skip (FPN lateral shape)
     (1, 60, 100, 512, 2048, 1, 1, 4, 4, 0, 4, 4, False),    # 1x1 512 -> 2048 with a skip, eight channel tiles
     (3, 90, 100, 512, 288, 1, 1, 4, 4, 0, 4, 0, False),     # a partial channel tile
+    # 8 K steps, no skip, more than one round
+    (4, 100, 167, 512, 256, 1, 1, 4, 4, 0, 4, 0, False),    # res4.0 conv1 shape: 1044 tiles
+    (3, 90, 110, 512, 288, 1, 1, 3, 3, 1, 3, 0, False),     # 3-bit codes, a partial channel tile: 930 tiles
     # fewer 256 x 128 tiles than CUs: 256 x 64 tiles, one round (long K ranges)
     (1, 50, 84, 512, 512, 3, 1, 4, 4, 0, 4, 4, False),      # res5 3x3 shape: 132 tiles, 72 K steps, skip
     (1, 101, 167, 512, 288, 3, 2, 4, 4, 1, 4, 0, False),    # stride 2, a partial channel tile: 134 tiles
