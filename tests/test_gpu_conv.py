@@ -201,6 +201,7 @@ WV_CASES = [
     (1, 50, 84, 512, 512, 3, 1, 4, 4, 0, 4, 4, False),      # res5 3x3 shape: 132 tiles, 72 K steps, skip
     (1, 101, 167, 512, 288, 3, 2, 4, 4, 1, 4, 0, False),    # stride 2, a partial channel tile: 134 tiles
     (8, 25, 42, 2048, 512, 1, 1, 4, 4, 0, 4, 0, False),     # 1x1 2048 -> 512: 132 tiles, 32 K steps
+    (2, 50, 84, 1024, 256, 1, 1, 4, 4, 1, 4, 4, True),      # 1x1 with an upsampled skip: 132 tiles, 16 K steps
 ]
 
 
